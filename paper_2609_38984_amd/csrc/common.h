@@ -1,0 +1,149 @@
+// Internal helpers shared by the HIP sources of libswam (gfx950 only).
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#define SWAM_SEL_MAXNP 4096   // selection sort capacity (next power of two >= N_s)
+#define SWAM_MAX_NS_DEV 4096
+
+namespace swam {
+
+typedef uint16_t bf16_t;  // raw bf16 storage
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+
+__device__ __forceinline__ float bf16_to_f32(bf16_t v) {
+  return __uint_as_float(((uint32_t)v) << 16);
+}
+
+// Round to nearest even (inputs are finite in this library).
+__device__ __forceinline__ bf16_t f32_to_bf16(float f) {
+  uint32_t u = __float_as_uint(f);
+  u += 0x7FFFu + ((u >> 16) & 1u);
+  return (bf16_t)(u >> 16);
+}
+
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  return (uint32_t)f32_to_bf16(lo) | ((uint32_t)f32_to_bf16(hi) << 16);
+}
+
+template <typename T> struct Elem;
+template <> struct Elem<float> {
+  __device__ __forceinline__ static float load(const float* p) { return *p; }
+  __device__ __forceinline__ static void store(float* p, float v) { *p = v; }
+};
+template <> struct Elem<bf16_t> {
+  __device__ __forceinline__ static float load(const bf16_t* p) { return bf16_to_f32(*p); }
+  __device__ __forceinline__ static void store(bf16_t* p, float v) { *p = f32_to_bf16(v); }
+};
+
+__device__ __forceinline__ float warp_sum(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+  return v;
+}
+__device__ __forceinline__ float warp_max(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));
+  return v;
+}
+__device__ __forceinline__ double warp_sum_d(double v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+  return v;
+}
+
+// ---------------------------------------------------------------------------
+// launchers (host side), one per kernel family; all asynchronous on `st`
+// ---------------------------------------------------------------------------
+enum Epilogue { EPI_BIAS = 0, EPI_BIAS_GELU = 1, EPI_BIAS_GATED_RESIDUAL = 2 };
+
+// C[M][N] = epi(A[M][K] . B[N][K]^T + bias[N]); for the gated residual
+// C[m][n] = C[m][n] + gate[n] * (acc + bias[n]) (C read then written).
+hipError_t launch_gemm(int dtype, int epi, const void* A, int64_t lda, const void* B,
+                       int64_t ldb, const void* bias, const float* gate, void* C,
+                       int64_t ldc, int64_t M, int64_t N, int64_t K, hipStream_t st);
+
+// mod[blk][6d] = W_ada[blk] SiLU(temb) + b_ada[blk] for n_blk blocks at once.
+struct AdalnArgs {
+  const void* w[64];
+  const void* b[64];
+};
+hipError_t launch_adaln(int dtype, const AdalnArgs& a, int n_blk, const float* temb,
+                        int d_temb, int d6, float* mod, hipStream_t st);
+
+// h[r] = LN(x[r]) (1 + scale) + shift
+hipError_t launch_ln_mod(int dtype, const void* x, void* h, const float* shift,
+                         const float* scale, int64_t rows, int d, hipStream_t st);
+
+// o = softmax(q k^T / 8) v per head inside each sequence; lse (optional).
+// Sequence bounds are clamped to [0, n_rows].
+hipError_t launch_attention(int dtype, const void* qkv, void* o, float* lse,
+                            const int32_t* cu_seqlens, int n_seqs, int64_t n_rows,
+                            int n_heads, hipStream_t st);
+
+// Score kernels (mode A with lse, mode B computes lse first into lse_ws).
+struct ScoreArgs {
+  const void* q; int64_t q_seq, q_row;
+  const void* k; int64_t k_seq, k_row;
+  const float* lse;           // sequence b, query i, head h at lse + b*lse_seq + i*N_h + h
+  int64_t lse_seq;
+  float* s_out;               // sequence b, frame f at s_out + b*s_seq + f*N_s
+  int64_t s_seq;
+  const float* alpha;         // [g] device
+  int B, F, n_s, H, n_heads;
+};
+hipError_t launch_score(int dtype, const ScoreArgs& a, hipStream_t st);
+hipError_t launch_lse_all(int dtype, const void* q, int64_t q_seq, int64_t q_row,
+                          const void* kall, int64_t k_seq, int64_t k_row, int64_t n_keys,
+                          int B, int H, int n_heads, float* lse_out, float* part_ws,
+                          hipStream_t st);
+
+// Score reduction (layer quality, core layers, V, A).
+struct ReduceArgs {
+  const float* s_all;  // [B][L][F][N_s]
+  double* frame_sum;   // ws [B][L][F]
+  double* frame_ent;   // ws [B][L][F]
+  float* q;            // [B][L]
+  int32_t* core;       // [B][k_layer_eff]
+  double* qd;          // ws [B][L] float64 quality
+  float* v;            // [B][F][N_s]
+  float* a;            // [B][N_s]
+  int B, L, F, n_s, k_layer;
+  float cv_penalty;
+};
+hipError_t launch_score_reduce(const ReduceArgs& a, hipStream_t st);
+
+// Selection and packing metadata.
+struct SelectArgs {
+  const float* v;      // [B][F][N_s]
+  const float* a;      // [B][N_s]
+  uint8_t* pool;       // ws [B][N_s]
+  uint8_t* core;       // ws [B][F][N_s]
+  int32_t* keep_idx;   // [B][F][k_max]
+  int32_t* keep_cnt;   // [B][F]
+  int32_t* keep;       // ws [B*L_full] 0/1
+  int B, F, n_s, k_core, k_anchor, k_max;
+  int mass_num, mass_den;  // mass threshold as a fraction; den == 0: fixed K_c
+  int n_ctx, n_act;
+};
+hipError_t launch_select(const SelectArgs& a, hipStream_t st);
+// keep flags from an imported selection; rewrites keep_idx / keep_cnt ascending
+hipError_t launch_keep_from_idx(const int32_t* in_idx, int32_t* keep_idx, int32_t* keep_cnt,
+                                int32_t* keep, int B, int F, int n_s, int k_max, int n_ctx,
+                                int n_act, hipStream_t st);
+// exclusive scan of keep flags -> pack_pos, gather, cu_seqlens
+hipError_t launch_packmap(const int32_t* keep, int32_t* pack_pos, int32_t* gather,
+                          int32_t* cu, int B, int64_t l_full, hipStream_t st);
+hipError_t launch_pack(const void* x_full, void* x_packed, const int32_t* gather,
+                       int64_t rows, int64_t row_bytes, hipStream_t st);
+hipError_t launch_unpack_scatter(const void* y_packed, void* y_full, const int32_t* gather,
+                                 int64_t rows, int64_t row_bytes, hipStream_t st);
+hipError_t launch_unpack_merge(const void* y_packed, const void* x_full, void* y_full,
+                               const int32_t* pack_pos, int64_t rows, int64_t row_bytes,
+                               hipStream_t st);
+hipError_t launch_copy(const void* src, void* dst, int64_t bytes, hipStream_t st);
+
+}  // namespace swam

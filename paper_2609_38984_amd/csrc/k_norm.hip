@@ -1,0 +1,132 @@
+// adaLN modulation vectors and the modulated LayerNorm of the DiT block.
+//   mod = W_ada SiLU(t_emb) + b_ada        (all blocks of a step in one launch)
+//   h   = LN(x) (1 + scale) + shift       (biased variance, eps 1e-6, no affine)
+// One wavefront per output row (modulation) or per token row (LN); the row
+// stays in registers between the mean and the variance pass.
+#include "common.h"
+
+namespace swam {
+
+template <typename T>
+__global__ void __launch_bounds__(256)
+adaln_kernel(AdalnArgs args, const float* __restrict__ temb, int d_temb, int d6,
+             float* __restrict__ mod) {
+  const int blk = blockIdx.y;
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (row >= d6) return;
+  const T* w = (const T*)args.w[blk] + (int64_t)row * d_temb;
+  float acc = 0.0f;
+  for (int k = lane; k < d_temb; k += 64) {
+    const float t = temb[k];
+    acc = fmaf(Elem<T>::load(w + k), t / (1.0f + expf(-t)), acc);
+  }
+  acc = warp_sum(acc);
+  if (lane == 0) mod[(int64_t)blk * d6 + row] = acc + Elem<T>::load((const T*)args.b[blk] + row);
+}
+
+hipError_t launch_adaln(int dtype, const AdalnArgs& a, int n_blk, const float* temb,
+                        int d_temb, int d6, float* mod, hipStream_t st) {
+  dim3 grid((d6 + 3) / 4, n_blk);
+  if (dtype == 1)
+    hipLaunchKernelGGL(adaln_kernel<bf16_t>, grid, dim3(256), 0, st, a, temb, d_temb, d6, mod);
+  else
+    hipLaunchKernelGGL(adaln_kernel<float>, grid, dim3(256), 0, st, a, temb, d_temb, d6, mod);
+  return hipGetLastError();
+}
+
+// bf16 rows: 16-byte chunks of 8 elements, up to CH chunks per lane (d <= 512 CH)
+template <int CH>
+__global__ void __launch_bounds__(256)
+ln_mod_bf16(const bf16_t* __restrict__ x, bf16_t* __restrict__ h,
+            const float* __restrict__ shift, const float* __restrict__ scale, int64_t rows,
+            int d) {
+  const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (row >= rows) return;
+  const int nch = d >> 3;
+  const uint4* xr = (const uint4*)(x + row * d);
+  float v[CH][8];
+  float s = 0.0f;
+#pragma unroll
+  for (int c = 0; c < CH; ++c) {
+    const int ci = lane + 64 * c;
+    if (ci < nch) {
+      const uint4 w = xr[ci];
+      const uint32_t p[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        v[c][2 * e] = __uint_as_float(p[e] << 16);
+        v[c][2 * e + 1] = __uint_as_float(p[e] & 0xFFFF0000u);
+        s += v[c][2 * e] + v[c][2 * e + 1];
+      }
+    }
+  }
+  const float mean = warp_sum(s) / d;
+  float q = 0.0f;
+#pragma unroll
+  for (int c = 0; c < CH; ++c)
+    if (lane + 64 * c < nch)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) { const float t = v[c][e] - mean; q += t * t; }
+  const float rstd = rsqrtf(warp_sum(q) / d + 1e-6f);
+  uint4* hr = (uint4*)(h + row * d);
+#pragma unroll
+  for (int c = 0; c < CH; ++c) {
+    const int ci = lane + 64 * c;
+    if (ci < nch) {
+      const int col = ci * 8;
+      float o[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e)
+        o[e] = (v[c][e] - mean) * rstd * (1.0f + scale[col + e]) + shift[col + e];
+      uint4 w;
+      w.x = pack_bf16x2(o[0], o[1]);
+      w.y = pack_bf16x2(o[2], o[3]);
+      w.z = pack_bf16x2(o[4], o[5]);
+      w.w = pack_bf16x2(o[6], o[7]);
+      hr[ci] = w;
+    }
+  }
+}
+
+// fp32 rows: two passes over global memory (rows are L1/L2 resident)
+__global__ void __launch_bounds__(256)
+ln_mod_f32(const float* __restrict__ x, float* __restrict__ h, const float* __restrict__ shift,
+           const float* __restrict__ scale, int64_t rows, int d) {
+  const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (row >= rows) return;
+  const float* xr = x + row * d;
+  float s = 0.0f;
+  for (int c = lane; c < d; c += 64) s += xr[c];
+  const float mean = warp_sum(s) / d;
+  float q = 0.0f;
+  for (int c = lane; c < d; c += 64) { const float t = xr[c] - mean; q += t * t; }
+  const float rstd = 1.0f / sqrtf(warp_sum(q) / d + 1e-6f);
+  for (int c = lane; c < d; c += 64)
+    h[row * d + c] = (xr[c] - mean) * rstd * (1.0f + scale[c]) + shift[c];
+}
+
+hipError_t launch_ln_mod(int dtype, const void* x, void* h, const float* shift,
+                         const float* scale, int64_t rows, int d, hipStream_t st) {
+  if (rows <= 0) return hipSuccess;
+  dim3 grid((unsigned)((rows + 3) / 4));
+  if (dtype == 1) {
+    if (d <= 1024)
+      hipLaunchKernelGGL(ln_mod_bf16<2>, grid, dim3(256), 0, st, (const bf16_t*)x, (bf16_t*)h,
+                         shift, scale, rows, d);
+    else if (d <= 2048)
+      hipLaunchKernelGGL(ln_mod_bf16<4>, grid, dim3(256), 0, st, (const bf16_t*)x, (bf16_t*)h,
+                         shift, scale, rows, d);
+    else
+      hipLaunchKernelGGL(ln_mod_bf16<8>, grid, dim3(256), 0, st, (const bf16_t*)x, (bf16_t*)h,
+                         shift, scale, rows, d);
+  } else {
+    hipLaunchKernelGGL(ln_mod_f32, grid, dim3(256), 0, st, (const float*)x, (float*)h, shift,
+                       scale, rows, d);
+  }
+  return hipGetLastError();
+}
+
+}  // namespace swam

@@ -1,0 +1,207 @@
+// Action-to-future spatial scores of one layer (reused-normaliser scorer):
+//   S(f,j) = (1/N_h) sum_{i in I_f} sum_h alpha_i exp(q_h(i).k_h(f,j)/8 - lambda_h(i))
+// Only frame-f keys against frame-f's query group are formed; no attention
+// matrix, no value product.  The work is a thin contraction (g <= 16 queries
+// against a stream of keys), so it is bound by the single read of the future
+// keys; MFMA only keeps the dot products off the VALU.
+//
+// bf16: workgroup = 4 waves on 16 keys of one frame.  Each wave takes every
+// 4th head: two 16x16x32 MFMAs per head with the keys as the A operand
+// (lane -> key lane&15, 8 hd at 8*(lane>>4)) and the group's queries as the
+// B operand, so the accumulator gives each lane one query (lane & 15) and
+// four keys.  exp2 of the scaled logit minus the query's normaliser is
+// weighted by alpha (0 for padding queries), summed over the wave's heads in
+// registers, reduced over queries with lane shuffles and over waves in LDS in
+// a fixed order (deterministic).
+// fp32: one thread per key.
+// Mode B normaliser: lambda over all keys of the sequence, per (query, head),
+// as an online max/sum split over key chunks with wavefront-shuffle
+// reductions, combined in a second pass.
+#include "common.h"
+
+namespace swam {
+
+constexpr float LOG2E = 1.4426950408889634f;
+
+__global__ void __launch_bounds__(256)
+score_bf16(const bf16_t* __restrict__ q, int64_t q_seq, int64_t q_row,
+           const bf16_t* __restrict__ k, int64_t k_seq, int64_t k_row,
+           const float* __restrict__ lse, int64_t lse_seq, float* __restrict__ s_out,
+           int64_t s_seq, const float* __restrict__ alpha, int F, int n_s, int H, int n_heads) {
+  __shared__ float part[4][16];
+  const int ktiles = (n_s + 15) >> 4;
+  const int kt = blockIdx.x % ktiles;
+  const int f = (blockIdx.x / ktiles) % F;
+  const int b = blockIdx.x / (ktiles * F);
+  const int g = H / F;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int j0 = kt * 16;
+  const int key = min(j0 + (lane & 15), n_s - 1);
+  const bf16_t* kp = k + b * k_seq + (int64_t)(f * n_s + key) * k_row + 8 * (lane >> 4);
+  const int qi = lane & 15;                 // query slot within the group (C column)
+  const int ql = min(qi, g - 1);            // loaded row (padding slots reuse a valid row)
+  const float aw = qi < g ? alpha[qi] : 0.0f;
+  const int qa = f * g + ql;
+  const bf16_t* qp = q + b * q_seq + (int64_t)qa * q_row + 8 * (lane >> 4);
+  const float* lp = lse + (int64_t)b * lse_seq + (int64_t)qa * n_heads;
+
+  float acc[4] = {0.f, 0.f, 0.f, 0.f};
+  for (int h = wave; h < n_heads; h += 4) {
+    const bf16x8 k0 = __builtin_bit_cast(bf16x8, *(const uint4*)(kp + h * 64));
+    const bf16x8 k1 = __builtin_bit_cast(bf16x8, *(const uint4*)(kp + h * 64 + 32));
+    const bf16x8 q0 = __builtin_bit_cast(bf16x8, *(const uint4*)(qp + h * 64));
+    const bf16x8 q1 = __builtin_bit_cast(bf16x8, *(const uint4*)(qp + h * 64 + 32));
+    f32x4 c = {0.f, 0.f, 0.f, 0.f};
+    c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k0, q0, c, 0, 0, 0);
+    c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k1, q1, c, 0, 0, 0);
+    const float lam = lp[h] * LOG2E;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) acc[r] += aw * exp2f(c[r] * (0.125f * LOG2E) - lam);
+  }
+  // sum over the 16 query columns (lanes with equal lane >> 4)
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    float v = acc[r];
+    v += __shfl_xor(v, 8);
+    v += __shfl_xor(v, 4);
+    v += __shfl_xor(v, 2);
+    v += __shfl_xor(v, 1);
+    acc[r] = v;
+  }
+  if ((lane & 15) == 0) {
+#pragma unroll
+    for (int r = 0; r < 4; ++r) part[wave][4 * (lane >> 4) + r] = acc[r];
+  }
+  __syncthreads();
+  if (threadIdx.x < 16) {
+    const int j = j0 + threadIdx.x;
+    if (j < n_s) {
+      const float s = ((part[0][threadIdx.x] + part[1][threadIdx.x]) +
+                       (part[2][threadIdx.x] + part[3][threadIdx.x])) / (float)n_heads;
+      s_out[(int64_t)b * s_seq + (int64_t)f * n_s + j] = s;
+    }
+  }
+}
+
+__global__ void __launch_bounds__(256)
+score_f32(const float* __restrict__ q, int64_t q_seq, int64_t q_row,
+          const float* __restrict__ k, int64_t k_seq, int64_t k_row,
+          const float* __restrict__ lse, int64_t lse_seq, float* __restrict__ s_out,
+          int64_t s_seq, const float* __restrict__ alpha, int B, int F, int n_s, int H,
+          int n_heads) {
+  const int64_t id = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (id >= (int64_t)B * F * n_s) return;
+  const int j = id % n_s, f = (id / n_s) % F, b = id / ((int64_t)n_s * F);
+  const int g = H / F;
+  const float* kr = k + b * k_seq + (int64_t)(f * n_s + j) * k_row;
+  float s = 0.0f;
+  for (int h = 0; h < n_heads; ++h) {
+    for (int a = 0; a < g; ++a) {
+      const int qa = f * g + a;
+      const float* qr = q + b * q_seq + (int64_t)qa * q_row + h * 64;
+      float x = 0.0f;
+      for (int e = 0; e < 64; ++e) x = fmaf(qr[e], kr[h * 64 + e], x);
+      s += alpha[a] * expf(x * 0.125f - lse[(int64_t)b * lse_seq + (int64_t)qa * n_heads + h]);
+    }
+  }
+  s_out[(int64_t)b * s_seq + (int64_t)f * n_s + j] = s / (float)n_heads;
+}
+
+// ---------------------------------------------------------------------------
+// mode B normaliser: partial (max, sum) per key chunk, then combine
+// ---------------------------------------------------------------------------
+constexpr int LSE_CHUNK = 256;
+
+template <typename T>
+__global__ void __launch_bounds__(256)
+lse_partial(const T* __restrict__ q, int64_t q_seq, int64_t q_row, const T* __restrict__ k,
+            int64_t k_seq, int64_t k_row, int64_t n_keys, int H, int n_heads,
+            float* __restrict__ part) {
+  // part layout [B][chunks][H][N_h][2]
+  __shared__ float qs[64];
+  __shared__ float red[2][4];
+  const int chunks = (int)((n_keys + LSE_CHUNK - 1) / LSE_CHUNK);
+  const int ch = blockIdx.x % chunks;
+  const int i = (blockIdx.x / chunks) % H;
+  const int b = blockIdx.x / (chunks * H);
+  const int h = blockIdx.y;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  if (tid < 64) qs[tid] = Elem<T>::load(q + b * q_seq + (int64_t)i * q_row + h * 64 + tid);
+  __syncthreads();
+  const int64_t j = (int64_t)ch * LSE_CHUNK + tid;
+  float x = -INFINITY;
+  if (j < n_keys) {
+    const T* kr = k + b * k_seq + j * k_row + h * 64;
+    float acc = 0.0f;
+    for (int e = 0; e < 64; ++e) acc = fmaf(qs[e], Elem<T>::load(kr + e), acc);
+    x = acc * 0.125f;
+  }
+  float m = warp_max(x);
+  if (lane == 0) red[0][wave] = m;
+  __syncthreads();
+  m = fmaxf(fmaxf(red[0][0], red[0][1]), fmaxf(red[0][2], red[0][3]));
+  float e = (j < n_keys) ? expf(x - m) : 0.0f;
+  e = warp_sum(e);
+  if (lane == 0) red[1][wave] = e;
+  __syncthreads();
+  if (tid == 0) {
+    float* p = part + ((((int64_t)b * chunks + ch) * H + i) * n_heads + h) * 2;
+    p[0] = m;
+    p[1] = (red[1][0] + red[1][1]) + (red[1][2] + red[1][3]);
+  }
+}
+
+__global__ void lse_combine(const float* __restrict__ part, int chunks, int B, int H,
+                            int n_heads, float* __restrict__ lse) {
+  const int id = blockIdx.x * blockDim.x + threadIdx.x;
+  if (id >= B * H * n_heads) return;
+  const int h = id % n_heads, i = (id / n_heads) % H, b = id / (n_heads * H);
+  float m = -INFINITY;
+  for (int c = 0; c < chunks; ++c)
+    m = fmaxf(m, part[((((int64_t)b * chunks + c) * H + i) * n_heads + h) * 2]);
+  float s = 0.0f;
+  for (int c = 0; c < chunks; ++c) {
+    const float* p = part + ((((int64_t)b * chunks + c) * H + i) * n_heads + h) * 2;
+    s += p[1] * expf(p[0] - m);
+  }
+  lse[id] = m + logf(s);
+}
+
+hipError_t launch_score(int dtype, const ScoreArgs& a, hipStream_t st) {
+  if (dtype == 1) {
+    const int ktiles = (a.n_s + 15) / 16;
+    hipLaunchKernelGGL(score_bf16, dim3(a.B * a.F * ktiles), dim3(256), 0, st,
+                       (const bf16_t*)a.q, a.q_seq, a.q_row, (const bf16_t*)a.k, a.k_seq,
+                       a.k_row, a.lse, a.lse_seq, a.s_out, a.s_seq, a.alpha, a.F, a.n_s, a.H,
+                       a.n_heads);
+  } else {
+    const int64_t n = (int64_t)a.B * a.F * a.n_s;
+    hipLaunchKernelGGL(score_f32, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st,
+                       (const float*)a.q, a.q_seq, a.q_row, (const float*)a.k, a.k_seq,
+                       a.k_row, a.lse, a.lse_seq, a.s_out, a.s_seq, a.alpha, a.B, a.F, a.n_s,
+                       a.H, a.n_heads);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_lse_all(int dtype, const void* q, int64_t q_seq, int64_t q_row,
+                          const void* kall, int64_t k_seq, int64_t k_row, int64_t n_keys,
+                          int B, int H, int n_heads, float* lse_out, float* part_ws,
+                          hipStream_t st) {
+  const int chunks = (int)((n_keys + LSE_CHUNK - 1) / LSE_CHUNK);
+  dim3 grid(B * H * chunks, n_heads);
+  if (dtype == 1)
+    hipLaunchKernelGGL(lse_partial<bf16_t>, grid, dim3(256), 0, st, (const bf16_t*)q, q_seq,
+                       q_row, (const bf16_t*)kall, k_seq, k_row, n_keys, H, n_heads, part_ws);
+  else
+    hipLaunchKernelGGL(lse_partial<float>, grid, dim3(256), 0, st, (const float*)q, q_seq,
+                       q_row, (const float*)kall, k_seq, k_row, n_keys, H, n_heads, part_ws);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const int n = B * H * n_heads;
+  hipLaunchKernelGGL(lse_combine, dim3((n + 255) / 256), dim3(256), 0, st, part_ws, chunks, B,
+                     H, n_heads, lse_out);
+  return hipGetLastError();
+}
+
+}  // namespace swam

@@ -1,0 +1,733 @@
+// C ABI of libswam: validation, workspace, the five parts of the sparse
+// denoising step and the step orchestrator.  Every device pointer argument
+// is owned by the caller; the context owns one workspace arena allocated at
+// creation.  All work is enqueued on the context's stream.
+#include <math.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <algorithm>
+#include <numeric>
+#include <string>
+#include <vector>
+
+#include "../../include/swam.h"
+#include "common.h"
+
+using namespace swam;
+
+namespace {
+
+thread_local std::string g_err;
+
+struct Derived {
+  int64_t n_s, g, l_full, rows_full, k_max, k_eff, d, hidden, esz, t_pack_fixed;
+  int mass_num, mass_den;
+};
+
+// workspace layout (offsets into one arena)
+struct Layout {
+  size_t qkv, h, o, u, xp, lse, mod, alpha, lse_act, lse_part, s_all, q, qd, core, v, a, fsum,
+      fent, pool, corefl, keep_idx, keep_cnt, keep, pack_pos, gather, cu_packed, cu_dense, total;
+};
+
+size_t align_up(size_t x) { return (x + 255) & ~(size_t)255; }
+
+int fail(std::string* err, int code, const std::string& msg) {
+  if (err) *err = msg;
+  return code;
+}
+
+int derive(const swam_config* c, Derived* dv, std::string* err) {
+  if (!c) return fail(err, SWAM_E_INVALID, "config is NULL");
+  if (c->dtype != SWAM_F32 && c->dtype != SWAM_BF16)
+    return fail(err, SWAM_E_DTYPE, "dtype must be SWAM_F32 or SWAM_BF16");
+  if (c->batch < 1 || c->batch > SWAM_MAX_BATCH)
+    return fail(err, SWAM_E_SHAPE, "batch must be in [1, 64]");
+  if (c->head_dim != 64) return fail(err, SWAM_E_SHAPE, "head_dim must be 64");
+  if (c->n_heads < 1 || c->d_model != c->n_heads * 64)
+    return fail(err, SWAM_E_INVALID, "d_model must equal n_heads * 64");
+  if (c->mlp_ratio < 1 || c->mlp_ratio > 16) return fail(err, SWAM_E_SHAPE, "mlp_ratio in [1, 16]");
+  if (c->n_blocks < 1 || c->n_blocks > SWAM_MAX_BLOCKS)
+    return fail(err, SWAM_E_SHAPE, "n_blocks must be in [1, 64]");
+  if (c->d_temb < 1 || c->d_temb > 1024) return fail(err, SWAM_E_SHAPE, "d_temb in [1, 1024]");
+  if (c->n_ctx < 0) return fail(err, SWAM_E_INVALID, "n_ctx < 0");
+  if (c->n_frames < 1 || c->n_frames > SWAM_MAX_FRAMES)
+    return fail(err, SWAM_E_SHAPE, "n_frames must be in [1, 64]");
+  if (c->frame_h < 1 || c->frame_w < 1) return fail(err, SWAM_E_INVALID, "frame size < 1");
+  const int64_t n_s = (int64_t)c->frame_h * c->frame_w;
+  if (n_s < 2 || n_s > SWAM_MAX_NS)
+    return fail(err, SWAM_E_SHAPE, "tokens per frame must be in [2, 4096]");
+  if (c->n_act < 1 || c->n_act % c->n_frames)
+    return fail(err, SWAM_E_INVALID, "n_act must be a positive multiple of n_frames");
+  const int64_t g = c->n_act / c->n_frames;
+  if (g > 16) return fail(err, SWAM_E_SHAPE, "at most 16 action queries per frame group");
+  if (!(c->mass_threshold >= 0.0f && c->mass_threshold <= 1.0f))
+    return fail(err, SWAM_E_INVALID, "mass_threshold must be in [0, 1]");
+  if (c->k_anchor < 0 || c->k_anchor >= n_s)
+    return fail(err, SWAM_E_INVALID, "k_anchor must be in [0, N_s)");
+  if (c->mass_threshold == 0.0f && (c->k_core < 0 || c->k_core + c->k_anchor > n_s))
+    return fail(err, SWAM_E_INVALID, "k_core + k_anchor must be in [0, N_s]");
+  if (c->k_layer < 1) return fail(err, SWAM_E_INVALID, "k_layer must be >= 1");
+  if (!(c->cv_penalty >= 0.0f) || !isfinite(c->cv_penalty))
+    return fail(err, SWAM_E_INVALID, "cv_penalty must be finite and >= 0");
+  if (c->reuse_R < 1) return fail(err, SWAM_E_INVALID, "reuse_R must be >= 1");
+  const int64_t d = c->d_model;
+  if (c->dtype == SWAM_BF16 && d > 4096) return fail(err, SWAM_E_SHAPE, "bf16 d_model <= 4096");
+  const int64_t l_full = c->n_ctx + (int64_t)c->n_frames * n_s + c->n_act;
+  const int64_t rows = (int64_t)c->batch * l_full;
+  if (rows >= (1ll << 30)) return fail(err, SWAM_E_SHAPE, "batch * tokens exceeds 2^30");
+  dv->n_s = n_s;
+  dv->g = g;
+  dv->l_full = l_full;
+  dv->rows_full = rows;
+  dv->d = d;
+  dv->hidden = (int64_t)c->mlp_ratio * d;
+  dv->esz = c->dtype == SWAM_BF16 ? 2 : 4;
+  dv->k_eff = std::min(c->k_layer, c->n_blocks);
+  if (c->mass_threshold > 0.0f) {
+    int num = (int)lrintf(c->mass_threshold * 1000.0f), den = 1000;
+    if (num < 1) num = 1;
+    const int gg = std::gcd(num, den);
+    dv->mass_num = num / gg;
+    dv->mass_den = den / gg;
+    dv->k_max = n_s;
+    dv->t_pack_fixed = -1;
+  } else {
+    dv->mass_num = 0;
+    dv->mass_den = 0;
+    dv->k_max = std::max<int64_t>(1, c->k_core + c->k_anchor);
+    dv->t_pack_fixed = c->n_ctx + (int64_t)c->n_frames * (c->k_core + c->k_anchor) + c->n_act;
+  }
+  return SWAM_OK;
+}
+
+Layout layout_for(const swam_config* c, const Derived& dv) {
+  Layout L{};
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t o = off;
+    off += align_up(bytes);
+    return o;
+  };
+  const int64_t R = dv.rows_full, B = c->batch, F = c->n_frames, Lb = c->n_blocks;
+  const int64_t chunks = (dv.l_full + 255) / 256;
+  L.qkv = take(R * 3 * dv.d * dv.esz);
+  L.h = take(R * dv.d * dv.esz);
+  L.o = take(R * dv.d * dv.esz);
+  L.u = take(R * dv.hidden * dv.esz);
+  L.xp = take(R * dv.d * dv.esz);
+  L.lse = take(R * c->n_heads * 4);
+  L.mod = take(Lb * 6 * dv.d * 4);
+  L.alpha = take(16 * 4);
+  L.lse_act = take(B * c->n_act * c->n_heads * 4);
+  L.lse_part = take(B * chunks * c->n_act * c->n_heads * 2 * 4);
+  L.s_all = take(B * Lb * F * dv.n_s * 4);
+  L.q = take(B * Lb * 4);
+  L.qd = take(B * Lb * 8);
+  L.core = take(B * dv.k_eff * 4);
+  L.v = take(B * F * dv.n_s * 4);
+  L.a = take(B * dv.n_s * 4);
+  L.fsum = take((B * Lb * F + 2 * B) * 8);
+  L.fent = take(B * Lb * F * 8);
+  L.pool = take(B * dv.n_s);
+  L.corefl = take(B * F * dv.n_s);
+  L.keep_idx = take(B * F * dv.k_max * 4);
+  L.keep_cnt = take(B * F * 4);
+  L.keep = take(R * 4);
+  L.pack_pos = take(R * 4);
+  L.gather = take(R * 4);
+  L.cu_packed = take((B + 1) * 4);
+  L.cu_dense = take((B + 1) * 4);
+  L.total = off;
+  return L;
+}
+
+}  // namespace
+
+struct swam_ctx {
+  swam_config cfg;
+  Derived dv;
+  Layout lay;
+  hipStream_t st = nullptr;
+  int device = 0;
+  char* arena = nullptr;
+  int32_t* host_cu = nullptr;   // pinned
+  bool sel_valid = false, scores_valid = false;
+  int64_t packed_rows = 0;
+  std::string err;
+  // timers
+  uint32_t tmask = 0;
+  int tcap = 0, tused = 0;
+  std::vector<hipEvent_t> ev;   // 2 per slot
+  std::vector<int> ev_cls;
+
+  template <typename T> T* ptr(size_t off) { return (T*)(arena + off); }
+};
+
+namespace {
+
+int set_err(swam_ctx* c, int code, const std::string& msg) {
+  if (c) c->err = msg; else g_err = msg;
+  return code;
+}
+
+int hip_check(swam_ctx* c, hipError_t e, const char* what) {
+  if (e == hipSuccess) return SWAM_OK;
+  return set_err(c, SWAM_E_HIP, std::string(what) + ": " + hipGetErrorString(e));
+}
+
+#define SWAM_HIP(ctx, expr, what)                        \
+  do {                                                   \
+    const int rc_ = hip_check((ctx), (expr), (what));    \
+    if (rc_ != SWAM_OK) return rc_;                      \
+  } while (0)
+
+// brackets one launch (or phase) of a timed class with events on the stream
+struct Timed {
+  swam_ctx* c;
+  int slot = -1;
+  Timed(swam_ctx* ctx, int cls) : c(ctx) {
+    if (((c->tmask >> cls) & 1u) && c->tused < c->tcap) {
+      slot = c->tused++;
+      c->ev_cls[slot] = cls;
+      hipEventRecord(c->ev[2 * slot], c->st);
+    }
+  }
+  ~Timed() {
+    if (slot >= 0) hipEventRecord(c->ev[2 * slot + 1], c->st);
+  }
+};
+
+bool any_null_block(const swam_block_weights* w) {
+  return !w || !w->w_ada || !w->b_ada || !w->w_qkv || !w->b_qkv || !w->w_o || !w->b_o ||
+         !w->w_1 || !w->b_1 || !w->w_2 || !w->b_2;
+}
+
+// one block in place on x [n_rows][d]; mod = this block's [6][d] modulation
+int run_block(swam_ctx* c, const swam_block_weights* w, const float* mod, void* x,
+              int64_t n_rows, const int32_t* cu, int n_seqs, float* lse_out, void* qkv,
+              int layer_for_score /* -1: no scoring */) {
+  const int dt = c->cfg.dtype;
+  const int64_t d = c->dv.d, hid = c->dv.hidden;
+  void* h = c->ptr<char>(c->lay.h);
+  void* o = c->ptr<char>(c->lay.o);
+  void* u = c->ptr<char>(c->lay.u);
+  hipStream_t st = c->st;
+  const float *sh1 = mod, *sc1 = mod + d, *g1 = mod + 2 * d;
+  const float *sh2 = mod + 3 * d, *sc2 = mod + 4 * d, *g2 = mod + 5 * d;
+  if (n_rows <= 0) return SWAM_OK;
+  {
+    Timed t(c, SWAM_T_LNMOD);
+    SWAM_HIP(c, launch_ln_mod(dt, x, h, sh1, sc1, n_rows, (int)d, st), "ln_mod");
+  }
+  {
+    Timed t(c, SWAM_T_GEMM_QKV);
+    SWAM_HIP(c, launch_gemm(dt, EPI_BIAS, h, d, w->w_qkv, d, w->b_qkv, nullptr, qkv, 3 * d,
+                            n_rows, 3 * d, d, st), "gemm qkv");
+  }
+  {
+    Timed t(c, SWAM_T_ATTN);
+    SWAM_HIP(c, launch_attention(dt, qkv, o, lse_out, cu, n_seqs, n_rows, c->cfg.n_heads, st),
+             "attention");
+  }
+  if (layer_for_score >= 0) {
+    // scores of this layer from the dense forward's q, k and normalisers
+    Timed t(c, SWAM_T_SCORE);
+    const swam_config& cf = c->cfg;
+    const int64_t ld = 3 * d, es = c->dv.esz;
+    ScoreArgs a{};
+    const int64_t act0 = cf.n_ctx + (int64_t)cf.n_frames * c->dv.n_s;
+    a.q = (const char*)qkv + act0 * ld * es;
+    a.q_seq = c->dv.l_full * ld;
+    a.q_row = ld;
+    a.k = (const char*)qkv + (cf.n_ctx * ld + d) * es;
+    a.k_seq = c->dv.l_full * ld;
+    a.k_row = ld;
+    a.lse = lse_out + act0 * cf.n_heads;
+    a.lse_seq = c->dv.l_full * cf.n_heads;
+    a.s_out = c->ptr<float>(c->lay.s_all) + (int64_t)layer_for_score * cf.n_frames * c->dv.n_s;
+    a.s_seq = (int64_t)cf.n_blocks * cf.n_frames * c->dv.n_s;
+    a.alpha = c->ptr<float>(c->lay.alpha);
+    a.B = cf.batch;
+    a.F = cf.n_frames;
+    a.n_s = (int)c->dv.n_s;
+    a.H = cf.n_act;
+    a.n_heads = cf.n_heads;
+    SWAM_HIP(c, launch_score(dt, a, st), "score");
+  }
+  {
+    Timed t(c, SWAM_T_GEMM_OUT);
+    SWAM_HIP(c, launch_gemm(dt, EPI_BIAS_GATED_RESIDUAL, o, d, w->w_o, d, w->b_o, g1, x, d,
+                            n_rows, d, d, st), "gemm out");
+  }
+  {
+    Timed t(c, SWAM_T_LNMOD);
+    SWAM_HIP(c, launch_ln_mod(dt, x, h, sh2, sc2, n_rows, (int)d, st), "ln_mod 2");
+  }
+  {
+    Timed t(c, SWAM_T_GEMM_UP);
+    SWAM_HIP(c, launch_gemm(dt, EPI_BIAS_GELU, h, d, w->w_1, d, w->b_1, nullptr, u, hid, n_rows,
+                            hid, d, st), "gemm up");
+  }
+  {
+    Timed t(c, SWAM_T_GEMM_DOWN);
+    SWAM_HIP(c, launch_gemm(dt, EPI_BIAS_GATED_RESIDUAL, u, hid, w->w_2, hid, w->b_2, g2, x, d,
+                            n_rows, d, hid, st), "gemm down");
+  }
+  return SWAM_OK;
+}
+
+int run_adaln(swam_ctx* c, const swam_block_weights* blocks, int n_blk, const float* temb) {
+  AdalnArgs a{};
+  for (int i = 0; i < n_blk; ++i) {
+    a.w[i] = blocks[i].w_ada;
+    a.b[i] = blocks[i].b_ada;
+  }
+  Timed t(c, SWAM_T_ADALN);
+  SWAM_HIP(c, launch_adaln(c->cfg.dtype, a, n_blk, temb, c->cfg.d_temb, (int)(6 * c->dv.d),
+                           c->ptr<float>(c->lay.mod), c->st), "adaln");
+  return SWAM_OK;
+}
+
+int run_reduce(swam_ctx* c, const float* s_all) {
+  const swam_config& cf = c->cfg;
+  ReduceArgs r{};
+  r.s_all = s_all;
+  r.frame_sum = c->ptr<double>(c->lay.fsum);
+  r.frame_ent = c->ptr<double>(c->lay.fent);
+  r.q = c->ptr<float>(c->lay.q);
+  r.core = c->ptr<int32_t>(c->lay.core);
+  r.qd = c->ptr<double>(c->lay.qd);
+  r.v = c->ptr<float>(c->lay.v);
+  r.a = c->ptr<float>(c->lay.a);
+  r.B = cf.batch;
+  r.L = cf.n_blocks;
+  r.F = cf.n_frames;
+  r.n_s = (int)c->dv.n_s;
+  r.k_layer = cf.k_layer;
+  r.cv_penalty = cf.cv_penalty;
+  Timed t(c, SWAM_T_REDUCE);
+  SWAM_HIP(c, launch_score_reduce(r, c->st), "score_reduce");
+  return SWAM_OK;
+}
+
+// read the packed sequence offsets back to the host (one synchronisation)
+int read_packed_rows(swam_ctx* c) {
+  const int B = c->cfg.batch;
+  SWAM_HIP(c, hipMemcpyAsync(c->host_cu, c->ptr<int32_t>(c->lay.cu_packed), (B + 1) * 4,
+                             hipMemcpyDeviceToHost, c->st), "read cu_seqlens");
+  SWAM_HIP(c, hipStreamSynchronize(c->st), "synchronise");
+  c->packed_rows = c->host_cu[B];
+  return SWAM_OK;
+}
+
+int run_select(swam_ctx* c, const float* v, const float* a) {
+  const swam_config& cf = c->cfg;
+  SelectArgs s{};
+  s.v = v;
+  s.a = a;
+  s.pool = c->ptr<uint8_t>(c->lay.pool);
+  s.core = c->ptr<uint8_t>(c->lay.corefl);
+  s.keep_idx = c->ptr<int32_t>(c->lay.keep_idx);
+  s.keep_cnt = c->ptr<int32_t>(c->lay.keep_cnt);
+  s.keep = c->ptr<int32_t>(c->lay.keep);
+  s.B = cf.batch;
+  s.F = cf.n_frames;
+  s.n_s = (int)c->dv.n_s;
+  s.k_core = cf.k_core;
+  s.k_anchor = cf.k_anchor;
+  s.k_max = (int)c->dv.k_max;
+  s.mass_num = c->dv.mass_num;
+  s.mass_den = c->dv.mass_den;
+  s.n_ctx = cf.n_ctx;
+  s.n_act = cf.n_act;
+  {
+    Timed t(c, SWAM_T_SELECT);
+    SWAM_HIP(c, launch_select(s, c->st), "select");
+    SWAM_HIP(c, launch_packmap(s.keep, c->ptr<int32_t>(c->lay.pack_pos),
+                               c->ptr<int32_t>(c->lay.gather), c->ptr<int32_t>(c->lay.cu_packed),
+                               cf.batch, c->dv.l_full, c->st), "packmap");
+  }
+  if (c->dv.mass_den > 0) {
+    const int rc = read_packed_rows(c);
+    if (rc != SWAM_OK) return rc;
+  } else {
+    c->packed_rows = (int64_t)cf.batch * c->dv.t_pack_fixed;
+  }
+  c->sel_valid = true;
+  return SWAM_OK;
+}
+
+int copy_out(swam_ctx* c, void* dst, size_t src_off, size_t bytes, const char* what) {
+  if (!dst) return SWAM_OK;
+  SWAM_HIP(c, hipMemcpyAsync(dst, c->arena + src_off, bytes, hipMemcpyDeviceToDevice, c->st),
+           what);
+  return SWAM_OK;
+}
+
+void fill_alpha(int g, float* out) {
+  // central half (|i - (g-1)/2| < g/4) weighs twice the outer quarters
+  double w[16], s = 0.0;
+  for (int i = 0; i < g; ++i) {
+    w[i] = fabs(i - (g - 1) / 2.0) < g / 4.0 ? 2.0 : 1.0;
+    s += w[i];
+  }
+  for (int i = 0; i < 16; ++i) out[i] = i < g ? (float)(w[i] / s) : 0.0f;
+}
+
+}  // namespace
+
+// ===========================================================================
+// C ABI
+// ===========================================================================
+extern "C" {
+
+const char* swam_status_str(int status) {
+  switch (status) {
+    case SWAM_OK: return "SWAM_OK";
+    case SWAM_E_INVALID: return "SWAM_E_INVALID";
+    case SWAM_E_SHAPE: return "SWAM_E_SHAPE";
+    case SWAM_E_DTYPE: return "SWAM_E_DTYPE";
+    case SWAM_E_STATE: return "SWAM_E_STATE";
+    case SWAM_E_HIP: return "SWAM_E_HIP";
+    case SWAM_E_NOMEM: return "SWAM_E_NOMEM";
+    case SWAM_E_UNSUPPORTED: return "SWAM_E_UNSUPPORTED";
+    default: return "SWAM_E_UNKNOWN";
+  }
+}
+
+const char* swam_last_error(const swam_ctx* ctx) {
+  return ctx ? ctx->err.c_str() : g_err.c_str();
+}
+
+int swam_plan(const swam_config* cfg, swam_plan_info* out) {
+  if (!out) return set_err(nullptr, SWAM_E_INVALID, "out is NULL");
+  Derived dv{};
+  const int rc = derive(cfg, &dv, &g_err);
+  if (rc != SWAM_OK) return rc;
+  const Layout L = layout_for(cfg, dv);
+  out->n_s = dv.n_s;
+  out->group_size = dv.g;
+  out->l_full = dv.l_full;
+  out->rows_full = dv.rows_full;
+  out->k_max = dv.k_max;
+  out->t_pack_fixed = dv.t_pack_fixed;
+  out->k_layer_eff = dv.k_eff;
+  out->workspace_bytes = (int64_t)L.total;
+  return SWAM_OK;
+}
+
+int swam_create(const swam_config* cfg, void* stream, swam_ctx** out) {
+  if (!out) return set_err(nullptr, SWAM_E_INVALID, "out is NULL");
+  *out = nullptr;
+  Derived dv{};
+  int rc = derive(cfg, &dv, &g_err);
+  if (rc != SWAM_OK) return rc;
+  swam_ctx* c = new swam_ctx();
+  c->cfg = *cfg;
+  c->dv = dv;
+  c->lay = layout_for(cfg, dv);
+  c->st = (hipStream_t)stream;
+  hipError_t e = hipGetDevice(&c->device);
+  if (e == hipSuccess) e = hipMalloc((void**)&c->arena, c->lay.total);
+  if (e != hipSuccess) {
+    g_err = std::string("workspace allocation: ") + hipGetErrorString(e);
+    delete c;
+    return e == hipErrorOutOfMemory ? SWAM_E_NOMEM : SWAM_E_HIP;
+  }
+  e = hipHostMalloc((void**)&c->host_cu, (cfg->batch + 1) * sizeof(int32_t), 0);
+  if (e == hipSuccess) {
+    float alpha[16];
+    fill_alpha((int)dv.g, alpha);
+    e = hipMemcpy(c->ptr<float>(c->lay.alpha), alpha, sizeof(alpha), hipMemcpyHostToDevice);
+  }
+  if (e == hipSuccess) {
+    std::vector<int32_t> cu(cfg->batch + 1);
+    for (int b = 0; b <= cfg->batch; ++b) cu[b] = (int32_t)(b * dv.l_full);
+    e = hipMemcpy(c->ptr<int32_t>(c->lay.cu_dense), cu.data(), cu.size() * 4,
+                  hipMemcpyHostToDevice);
+  }
+  if (e != hipSuccess) {
+    g_err = std::string("context setup: ") + hipGetErrorString(e);
+    swam_destroy(c);
+    return SWAM_E_HIP;
+  }
+  *out = c;
+  return SWAM_OK;
+}
+
+int swam_destroy(swam_ctx* c) {
+  if (!c) return SWAM_OK;
+  for (hipEvent_t ev : c->ev) hipEventDestroy(ev);
+  if (c->arena) hipFree(c->arena);
+  if (c->host_cu) hipHostFree(c->host_cu);
+  delete c;
+  return SWAM_OK;
+}
+
+int swam_set_stream(swam_ctx* c, void* stream) {
+  if (!c) return set_err(nullptr, SWAM_E_INVALID, "ctx is NULL");
+  c->st = (hipStream_t)stream;
+  return SWAM_OK;
+}
+
+int swam_score(swam_ctx* c, const void* q_act, int64_t q_seq_stride, int64_t q_row_stride,
+               const void* k_fut, int64_t k_seq_stride, int64_t k_row_stride,
+               const float* lse_act, const void* k_all, int64_t kall_seq_stride, float* s_out) {
+  if (!c) return set_err(nullptr, SWAM_E_INVALID, "ctx is NULL");
+  if (!q_act || !k_fut || !s_out) return set_err(c, SWAM_E_INVALID, "q_act, k_fut, s_out required");
+  if (!lse_act && !k_all) return set_err(c, SWAM_E_INVALID, "need lse_act (mode A) or k_all (mode B)");
+  const int64_t d = c->dv.d;
+  if (q_row_stride < d || k_row_stride < d || q_seq_stride < 0 || k_seq_stride < 0 ||
+      (!lse_act && kall_seq_stride < 0))
+    return set_err(c, SWAM_E_INVALID, "row strides must be >= d_model and seq strides >= 0");
+  const swam_config& cf = c->cfg;
+  const float* lse = lse_act;
+  int64_t lse_seq = (int64_t)cf.n_act * cf.n_heads;
+  if (!lse_act) {
+    Timed t(c, SWAM_T_SCORE);
+    float* ws = c->ptr<float>(c->lay.lse_act);
+    SWAM_HIP(c, launch_lse_all(cf.dtype, q_act, q_seq_stride, q_row_stride, k_all,
+                               kall_seq_stride, k_row_stride, c->dv.l_full, cf.batch, cf.n_act,
+                               cf.n_heads, ws, c->ptr<float>(c->lay.lse_part), c->st),
+             "lse (mode B)");
+    lse = ws;
+  }
+  ScoreArgs a{};
+  a.q = q_act; a.q_seq = q_seq_stride; a.q_row = q_row_stride;
+  a.k = k_fut; a.k_seq = k_seq_stride; a.k_row = k_row_stride;
+  a.lse = lse; a.lse_seq = lse_seq;
+  a.s_out = s_out; a.s_seq = (int64_t)cf.n_frames * c->dv.n_s;
+  a.alpha = c->ptr<float>(c->lay.alpha);
+  a.B = cf.batch; a.F = cf.n_frames; a.n_s = (int)c->dv.n_s; a.H = cf.n_act;
+  a.n_heads = cf.n_heads;
+  Timed t(c, SWAM_T_SCORE);
+  SWAM_HIP(c, launch_score(cf.dtype, a, c->st), "score");
+  return SWAM_OK;
+}
+
+int swam_score_reduce(swam_ctx* c, const float* s_all, float* q_out, float* v_out, float* a_out,
+                      int32_t* core_out) {
+  if (!c) return set_err(nullptr, SWAM_E_INVALID, "ctx is NULL");
+  if (!s_all || !v_out || !a_out) return set_err(c, SWAM_E_INVALID, "s_all, v_out, a_out required");
+  int rc = run_reduce(c, s_all);
+  if (rc != SWAM_OK) return rc;
+  const swam_config& cf = c->cfg;
+  const int64_t B = cf.batch;
+  if ((rc = copy_out(c, q_out, c->lay.q, B * cf.n_blocks * 4, "copy Q"))) return rc;
+  if ((rc = copy_out(c, v_out, c->lay.v, B * cf.n_frames * c->dv.n_s * 4, "copy V"))) return rc;
+  if ((rc = copy_out(c, a_out, c->lay.a, B * c->dv.n_s * 4, "copy A"))) return rc;
+  if ((rc = copy_out(c, core_out, c->lay.core, B * c->dv.k_eff * 4, "copy core"))) return rc;
+  return SWAM_OK;
+}
+
+int swam_select(swam_ctx* c, const float* v, const float* a, int32_t* keep_idx,
+                int32_t* keep_cnt, int32_t* pack_pos, int32_t* gather, int32_t* cu_seqlens) {
+  if (!c) return set_err(nullptr, SWAM_E_INVALID, "ctx is NULL");
+  if ((v == nullptr) != (a == nullptr))
+    return set_err(c, SWAM_E_INVALID, "v and a must both be given or both NULL");
+  if (!v) {
+    v = c->ptr<float>(c->lay.v);
+    a = c->ptr<float>(c->lay.a);
+  }
+  int rc = run_select(c, v, a);
+  if (rc != SWAM_OK) return rc;
+  return swam_export(c, nullptr, nullptr, nullptr, nullptr, keep_idx, keep_cnt, pack_pos, gather,
+                     cu_seqlens);
+}
+
+int swam_set_selection(swam_ctx* c, const int32_t* keep_idx, const int32_t* keep_cnt) {
+  if (!c) return set_err(nullptr, SWAM_E_INVALID, "ctx is NULL");
+  if (!keep_idx) return set_err(c, SWAM_E_INVALID, "keep_idx is NULL");
+  (void)keep_cnt;  // counts are recomputed from the indices
+  const swam_config& cf = c->cfg;
+  int32_t* own = c->ptr<int32_t>(c->lay.keep_idx);
+  if (keep_idx == own) return set_err(c, SWAM_E_INVALID, "keep_idx aliases the context cache");
+  {
+    Timed t(c, SWAM_T_SELECT);
+    SWAM_HIP(c, launch_keep_from_idx(keep_idx, own, c->ptr<int32_t>(c->lay.keep_cnt),
+                                     c->ptr<int32_t>(c->lay.keep), cf.batch, cf.n_frames,
+                                     (int)c->dv.n_s, (int)c->dv.k_max, cf.n_ctx, cf.n_act, c->st),
+             "import selection");
+    SWAM_HIP(c, launch_packmap(c->ptr<int32_t>(c->lay.keep), c->ptr<int32_t>(c->lay.pack_pos),
+                               c->ptr<int32_t>(c->lay.gather), c->ptr<int32_t>(c->lay.cu_packed),
+                               cf.batch, c->dv.l_full, c->st), "packmap");
+  }
+  const int rc = read_packed_rows(c);
+  if (rc != SWAM_OK) return rc;
+  c->sel_valid = true;
+  return SWAM_OK;
+}
+
+int swam_packed_rows(swam_ctx* c, int64_t* rows) {
+  if (!c || !rows) return set_err(c, SWAM_E_INVALID, "NULL argument");
+  if (!c->sel_valid) return set_err(c, SWAM_E_STATE, "no selection cached");
+  *rows = c->packed_rows;
+  return SWAM_OK;
+}
+
+int swam_export(swam_ctx* c, float* s_all, float* q, float* v, float* a, int32_t* keep_idx,
+                int32_t* keep_cnt, int32_t* pack_pos, int32_t* gather, int32_t* cu_seqlens) {
+  if (!c) return set_err(nullptr, SWAM_E_INVALID, "ctx is NULL");
+  const swam_config& cf = c->cfg;
+  const int64_t B = cf.batch, F = cf.n_frames, n_s = c->dv.n_s;
+  if ((keep_idx || keep_cnt || pack_pos || gather || cu_seqlens) && !c->sel_valid)
+    return set_err(c, SWAM_E_STATE, "no selection cached");
+  int rc;
+  if ((rc = copy_out(c, s_all, c->lay.s_all, B * cf.n_blocks * F * n_s * 4, "copy S"))) return rc;
+  if ((rc = copy_out(c, q, c->lay.q, B * cf.n_blocks * 4, "copy Q"))) return rc;
+  if ((rc = copy_out(c, v, c->lay.v, B * F * n_s * 4, "copy V"))) return rc;
+  if ((rc = copy_out(c, a, c->lay.a, B * n_s * 4, "copy A"))) return rc;
+  if ((rc = copy_out(c, keep_idx, c->lay.keep_idx, B * F * c->dv.k_max * 4, "copy keep_idx"))) return rc;
+  if ((rc = copy_out(c, keep_cnt, c->lay.keep_cnt, B * F * 4, "copy keep_cnt"))) return rc;
+  if ((rc = copy_out(c, pack_pos, c->lay.pack_pos, c->dv.rows_full * 4, "copy pack_pos"))) return rc;
+  if ((rc = copy_out(c, gather, c->lay.gather, c->dv.rows_full * 4, "copy gather"))) return rc;
+  if ((rc = copy_out(c, cu_seqlens, c->lay.cu_packed, (B + 1) * 4, "copy cu"))) return rc;
+  return SWAM_OK;
+}
+
+int swam_pack(swam_ctx* c, const void* x_full, void* x_packed) {
+  if (!c) return set_err(nullptr, SWAM_E_INVALID, "ctx is NULL");
+  if (!x_full || !x_packed) return set_err(c, SWAM_E_INVALID, "NULL tensor");
+  if (!c->sel_valid) return set_err(c, SWAM_E_STATE, "no selection cached");
+  Timed t(c, SWAM_T_PACK);
+  SWAM_HIP(c, launch_pack(x_full, x_packed, c->ptr<int32_t>(c->lay.gather), c->packed_rows,
+                          c->dv.d * c->dv.esz, c->st), "pack");
+  return SWAM_OK;
+}
+
+int swam_unpack(swam_ctx* c, const void* y_packed, const void* x_full, void* y_full) {
+  if (!c) return set_err(nullptr, SWAM_E_INVALID, "ctx is NULL");
+  if (!y_packed || !x_full || !y_full) return set_err(c, SWAM_E_INVALID, "NULL tensor");
+  if (!c->sel_valid) return set_err(c, SWAM_E_STATE, "no selection cached");
+  Timed t(c, SWAM_T_UNPACK);
+  const int64_t rb = c->dv.d * c->dv.esz;
+  if (y_full == x_full)
+    SWAM_HIP(c, launch_unpack_scatter(y_packed, y_full, c->ptr<int32_t>(c->lay.gather),
+                                      c->packed_rows, rb, c->st), "unpack");
+  else
+    SWAM_HIP(c, launch_unpack_merge(y_packed, x_full, y_full, c->ptr<int32_t>(c->lay.pack_pos),
+                                    c->dv.rows_full, rb, c->st), "unpack");
+  return SWAM_OK;
+}
+
+int swam_block(swam_ctx* c, const swam_block_weights* w, const float* temb, void* x,
+               int64_t n_rows, const int32_t* cu_seqlens, int32_t n_seqs, float* lse_out,
+               void* qkv_out) {
+  if (!c) return set_err(nullptr, SWAM_E_INVALID, "ctx is NULL");
+  if (any_null_block(w) || !temb || !x) return set_err(c, SWAM_E_INVALID, "NULL weight or tensor");
+  if (n_rows < 0 || n_rows > c->dv.rows_full)
+    return set_err(c, SWAM_E_SHAPE, "n_rows must be in [0, batch * l_full]");
+  const int32_t* cu = cu_seqlens;
+  if (!cu) {
+    if (n_rows != c->dv.rows_full)
+      return set_err(c, SWAM_E_SHAPE, "dense layout needs n_rows == batch * l_full");
+    cu = c->ptr<int32_t>(c->lay.cu_dense);
+    n_seqs = c->cfg.batch;
+  } else if (n_seqs < 1 || n_seqs > SWAM_MAX_BATCH) {
+    return set_err(c, SWAM_E_SHAPE, "n_seqs must be in [1, 64]");
+  }
+  int rc = run_adaln(c, w, 1, temb);
+  if (rc != SWAM_OK) return rc;
+  void* qkv = qkv_out ? qkv_out : c->ptr<char>(c->lay.qkv);
+  return run_block(c, w, c->ptr<float>(c->lay.mod), x, n_rows, cu, n_seqs, lse_out, qkv, -1);
+}
+
+int swam_step(swam_ctx* c, const swam_model* model, const void* x_full, const float* temb,
+              int32_t tau, void* y_full, int32_t flags, int32_t* kind_out) {
+  if (!c) return set_err(nullptr, SWAM_E_INVALID, "ctx is NULL");
+  const swam_config& cf = c->cfg;
+  if (!model || !model->blocks || model->n_blocks != cf.n_blocks)
+    return set_err(c, SWAM_E_INVALID, "model must have config.n_blocks blocks");
+  for (int l = 0; l < cf.n_blocks; ++l)
+    if (any_null_block(&model->blocks[l])) return set_err(c, SWAM_E_INVALID, "NULL block weight");
+  if (!x_full || !y_full || !temb) return set_err(c, SWAM_E_INVALID, "NULL tensor");
+  if (tau < 0) return set_err(c, SWAM_E_INVALID, "tau < 0");
+  int kind;
+  if (flags & SWAM_STEP_FORCE_DENSE) kind = SWAM_KIND_DENSE;
+  else if ((flags & SWAM_STEP_FORCE_REFRESH) || tau % cf.reuse_R == 0) kind = SWAM_KIND_REFRESH;
+  else kind = SWAM_KIND_SPARSE;
+  if (kind == SWAM_KIND_SPARSE && !c->sel_valid)
+    return set_err(c, SWAM_E_STATE, "sparse step before any selection (run a refresh first)");
+  int rc = run_adaln(c, model->blocks, cf.n_blocks, temb);
+  if (rc != SWAM_OK) return rc;
+  const int64_t d = c->dv.d;
+  const float* mod = c->ptr<float>(c->lay.mod);
+  void* qkv = c->ptr<char>(c->lay.qkv);
+  if (kind != SWAM_KIND_SPARSE) {
+    {
+      Timed t(c, SWAM_T_COPY);
+      SWAM_HIP(c, launch_copy(x_full, y_full, c->dv.rows_full * d * c->dv.esz, c->st), "copy");
+    }
+    const bool score = kind == SWAM_KIND_REFRESH;
+    for (int l = 0; l < cf.n_blocks; ++l) {
+      rc = run_block(c, &model->blocks[l], mod + (int64_t)l * 6 * d, y_full, c->dv.rows_full,
+                     c->ptr<int32_t>(c->lay.cu_dense), cf.batch,
+                     score ? c->ptr<float>(c->lay.lse) : nullptr, qkv, score ? l : -1);
+      if (rc != SWAM_OK) return rc;
+    }
+    if (score) {
+      c->scores_valid = true;
+      if ((rc = run_reduce(c, c->ptr<float>(c->lay.s_all))) != SWAM_OK) return rc;
+      if ((rc = run_select(c, c->ptr<float>(c->lay.v), c->ptr<float>(c->lay.a))) != SWAM_OK)
+        return rc;
+    }
+  } else {
+    void* xp = c->ptr<char>(c->lay.xp);
+    if ((rc = swam_pack(c, x_full, xp)) != SWAM_OK) return rc;
+    for (int l = 0; l < cf.n_blocks; ++l) {
+      rc = run_block(c, &model->blocks[l], mod + (int64_t)l * 6 * d, xp, c->packed_rows,
+                     c->ptr<int32_t>(c->lay.cu_packed), cf.batch, nullptr, qkv, -1);
+      if (rc != SWAM_OK) return rc;
+    }
+    if ((rc = swam_unpack(c, xp, x_full, y_full)) != SWAM_OK) return rc;
+  }
+  if (kind_out) *kind_out = kind;
+  return SWAM_OK;
+}
+
+int swam_timer_enable(swam_ctx* c, uint32_t mask, int32_t capacity) {
+  if (!c) return set_err(nullptr, SWAM_E_INVALID, "ctx is NULL");
+  if (mask && capacity < 1) return set_err(c, SWAM_E_INVALID, "capacity must be >= 1");
+  SWAM_HIP(c, hipStreamSynchronize(c->st), "synchronise");
+  for (hipEvent_t ev : c->ev) hipEventDestroy(ev);
+  c->ev.clear();
+  c->ev_cls.clear();
+  c->tmask = mask;
+  c->tcap = 0;
+  c->tused = 0;
+  if (!mask) return SWAM_OK;
+  c->ev.resize(2 * (size_t)capacity);
+  c->ev_cls.assign(capacity, -1);
+  for (auto& ev : c->ev) SWAM_HIP(c, hipEventCreate(&ev), "event create");
+  c->tcap = capacity;
+  return SWAM_OK;
+}
+
+int swam_timer_reset(swam_ctx* c) {
+  if (!c) return set_err(nullptr, SWAM_E_INVALID, "ctx is NULL");
+  SWAM_HIP(c, hipStreamSynchronize(c->st), "synchronise");
+  c->tused = 0;
+  return SWAM_OK;
+}
+
+int swam_timer_read(swam_ctx* c, int32_t cls, int64_t* launches, double* total_ms) {
+  if (!c || !launches || !total_ms) return set_err(c, SWAM_E_INVALID, "NULL argument");
+  if (cls < 0 || cls >= SWAM_T_COUNT) return set_err(c, SWAM_E_INVALID, "bad timer class");
+  SWAM_HIP(c, hipStreamSynchronize(c->st), "synchronise");
+  int64_t n = 0;
+  double ms = 0.0;
+  for (int i = 0; i < c->tused; ++i) {
+    if (c->ev_cls[i] != cls) continue;
+    float e = 0.0f;
+    SWAM_HIP(c, hipEventElapsedTime(&e, c->ev[2 * i], c->ev[2 * i + 1]), "elapsed");
+    ms += e;
+    ++n;
+  }
+  *launches = n;
+  *total_ms = ms;
+  return SWAM_OK;
+}
+
+}  // extern "C"

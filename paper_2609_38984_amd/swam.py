@@ -1,0 +1,309 @@
+"""Thin ctypes binding of libswam (include/swam.h).
+
+Argument marshalling only: tensors are checked for device, dtype, size and
+contiguity, then their device pointers are passed to the C ABI.  Every step of
+the path runs in the HIP kernels of libswam.so; if the library is missing the
+binding raises instead of computing anything itself.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+
+import torch
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libswam.so")
+
+SWAM_F32, SWAM_BF16 = 0, 1
+STATUS = {0: "SWAM_OK", -1: "SWAM_E_INVALID", -2: "SWAM_E_SHAPE", -3: "SWAM_E_DTYPE",
+          -4: "SWAM_E_STATE", -5: "SWAM_E_HIP", -6: "SWAM_E_NOMEM", -7: "SWAM_E_UNSUPPORTED"}
+FORCE_DENSE, FORCE_REFRESH = 1, 2
+KIND_DENSE, KIND_REFRESH, KIND_SPARSE = 0, 1, 2
+TIMERS = ["ADALN", "LNMOD", "GEMM_QKV", "ATTN", "GEMM_OUT", "GEMM_UP", "GEMM_DOWN", "SCORE",
+          "REDUCE", "SELECT", "PACK", "UNPACK", "COPY"]
+T = {name: i for i, name in enumerate(TIMERS)}
+
+EXPORTS = ["swam_create", "swam_destroy", "swam_set_stream", "swam_plan", "swam_status_str",
+           "swam_last_error", "swam_score", "swam_score_reduce", "swam_select",
+           "swam_set_selection", "swam_packed_rows", "swam_export", "swam_pack", "swam_unpack",
+           "swam_block", "swam_step", "swam_timer_enable", "swam_timer_reset", "swam_timer_read"]
+
+
+class SwamError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"{STATUS.get(code, code)}: {msg}")
+        self.code = code
+
+
+class Config(C.Structure):
+    _fields_ = [(n, C.c_int32) for n in (
+        "batch", "d_model", "n_heads", "head_dim", "mlp_ratio", "n_blocks", "d_temb", "n_ctx",
+        "n_frames", "frame_h", "frame_w", "n_act", "k_core", "k_anchor", "k_layer")] + [
+        ("cv_penalty", C.c_float), ("mass_threshold", C.c_float), ("reuse_R", C.c_int32),
+        ("dtype", C.c_int32)]
+
+    @classmethod
+    def from_obj(cls, o) -> "Config":
+        """Build from any object with the workload attributes (dtype 'f32'/'bf16')."""
+        c = cls()
+        for n, _ in cls._fields_:
+            if n == "dtype":
+                c.dtype = SWAM_BF16 if o.dtype == "bf16" else SWAM_F32
+            else:
+                setattr(c, n, getattr(o, n))
+        return c
+
+
+class PlanInfo(C.Structure):
+    _fields_ = [(n, C.c_int64) for n in ("n_s", "group_size", "l_full", "rows_full", "k_max",
+                                         "t_pack_fixed", "k_layer_eff", "workspace_bytes")]
+
+
+WEIGHT_NAMES = ["w_ada", "b_ada", "w_qkv", "b_qkv", "w_o", "b_o", "w_1", "b_1", "w_2", "b_2"]
+
+
+class BlockWeights(C.Structure):
+    _fields_ = [(n, C.c_void_p) for n in WEIGHT_NAMES]
+
+
+class ModelStruct(C.Structure):
+    _fields_ = [("n_blocks", C.c_int32), ("blocks", C.POINTER(BlockWeights))]
+
+
+_lib = None
+
+
+def load_library(path: str = LIB_PATH):
+    """Load libswam.so (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} is missing: build it with __graft_entry__.build() "
+                           "(the HIP library is required; there is no fallback)")
+    lib = C.CDLL(path)
+    P, I32, I64, F = C.c_void_p, C.c_int32, C.c_int64, C.c_float
+    sig = {
+        "swam_create": [C.POINTER(Config), P, C.POINTER(P)],
+        "swam_destroy": [P], "swam_set_stream": [P, P],
+        "swam_plan": [C.POINTER(Config), C.POINTER(PlanInfo)],
+        "swam_score": [P, P, I64, I64, P, I64, I64, P, P, I64, P],
+        "swam_score_reduce": [P, P, P, P, P, P],
+        "swam_select": [P, P, P, P, P, P, P, P],
+        "swam_set_selection": [P, P, P],
+        "swam_packed_rows": [P, C.POINTER(I64)],
+        "swam_export": [P, P, P, P, P, P, P, P, P, P],
+        "swam_pack": [P, P, P], "swam_unpack": [P, P, P, P],
+        "swam_block": [P, C.POINTER(BlockWeights), P, P, I64, P, I32, P, P],
+        "swam_step": [P, C.POINTER(ModelStruct), P, P, I32, P, I32, C.POINTER(I32)],
+        "swam_timer_enable": [P, C.c_uint32, I32], "swam_timer_reset": [P],
+        "swam_timer_read": [P, I32, C.POINTER(I64), C.POINTER(C.c_double)],
+    }
+    for name, args in sig.items():
+        fn = getattr(lib, name)
+        fn.argtypes = args
+        fn.restype = C.c_int
+    lib.swam_status_str.argtypes = [C.c_int]
+    lib.swam_status_str.restype = C.c_char_p
+    lib.swam_last_error.argtypes = [P]
+    lib.swam_last_error.restype = C.c_char_p
+    _lib = lib
+    return lib
+
+
+def _check(lib, ctx, rc):
+    if rc != 0:
+        raise SwamError(rc, lib.swam_last_error(ctx).decode())
+
+
+def plan(cfg) -> PlanInfo:
+    lib = load_library()
+    c = cfg if isinstance(cfg, Config) else Config.from_obj(cfg)
+    info = PlanInfo()
+    _check(lib, None, lib.swam_plan(C.byref(c), C.byref(info)))
+    return info
+
+
+def _ptr(t, dtype=None, numel=None, name="tensor"):
+    """Device pointer of a contiguous CUDA tensor (None -> NULL)."""
+    if t is None:
+        return None
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise TypeError(f"{name} must be a GPU tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if dtype is not None and t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if numel is not None and t.numel() < numel:
+        raise ValueError(f"{name} has {t.numel()} elements, needs {numel}")
+    return t.data_ptr()
+
+
+class Model:
+    """Device weights of every block, kept alive with their C descriptors."""
+
+    def __init__(self, blocks: list[dict], act_dtype: torch.dtype):
+        self.blocks = blocks
+        self._arr = (BlockWeights * len(blocks))()
+        for i, w in enumerate(blocks):
+            for n in WEIGHT_NAMES:
+                setattr(self._arr[i], n, _ptr(w[n], act_dtype, name=n))
+        self.struct = ModelStruct(len(blocks), self._arr)
+
+
+class Context:
+    """One libswam context bound to a stream (default: torch's current stream)."""
+
+    def __init__(self, cfg, stream: torch.cuda.Stream | None = None):
+        self.lib = load_library()
+        self.cfg = cfg
+        self.c_cfg = cfg if isinstance(cfg, Config) else Config.from_obj(cfg)
+        self.plan = plan(self.c_cfg)
+        self.act_dtype = torch.bfloat16 if self.c_cfg.dtype == SWAM_BF16 else torch.float32
+        self.stream = stream or torch.cuda.current_stream()
+        h = C.c_void_p()
+        _check(self.lib, None, self.lib.swam_create(C.byref(self.c_cfg),
+                                                    C.c_void_p(self.stream.cuda_stream),
+                                                    C.byref(h)))
+        self.h = h
+
+    def close(self):
+        if getattr(self, "h", None):
+            self.lib.swam_destroy(self.h)
+            self.h = None
+
+    def __del__(self):
+        self.close()
+
+    def _ok(self, rc):
+        _check(self.lib, self.h, rc)
+
+    # -- sizes -----------------------------------------------------------------
+    @property
+    def n_s(self):
+        return self.plan.n_s
+
+    @property
+    def rows_full(self):
+        return self.plan.rows_full
+
+    @property
+    def k_max(self):
+        return self.plan.k_max
+
+    # -- (1) scoring -----------------------------------------------------------
+    def score(self, q_act, q_seq, q_row, k_fut, k_seq, k_row, s_out, lse_act=None, k_all=None,
+              kall_seq=0):
+        c = self.c_cfg
+        n_s = self.n_s
+        _ptr(s_out, torch.float32, c.batch * c.n_frames * n_s, "s_out")
+        self._ok(self.lib.swam_score(
+            self.h, _ptr(q_act, self.act_dtype, name="q_act"), q_seq, q_row,
+            _ptr(k_fut, self.act_dtype, name="k_fut"), k_seq, k_row,
+            _ptr(lse_act, torch.float32, c.batch * c.n_act * c.n_heads, "lse_act"),
+            _ptr(k_all, self.act_dtype, name="k_all"), kall_seq, s_out.data_ptr()))
+
+    def score_reduce(self, s_all, v_out, a_out, q_out=None, core_out=None):
+        c = self.c_cfg
+        self._ok(self.lib.swam_score_reduce(
+            self.h, _ptr(s_all, torch.float32, c.batch * c.n_blocks * c.n_frames * self.n_s, "s_all"),
+            _ptr(q_out, torch.float32, c.batch * c.n_blocks, "q_out"),
+            _ptr(v_out, torch.float32, c.batch * c.n_frames * self.n_s, "v_out"),
+            _ptr(a_out, torch.float32, c.batch * self.n_s, "a_out"),
+            _ptr(core_out, torch.int32, c.batch * self.plan.k_layer_eff, "core_out")))
+
+    # -- (2) selection ---------------------------------------------------------
+    def select(self, v=None, a=None, keep_idx=None, keep_cnt=None, pack_pos=None, gather=None,
+               cu_seqlens=None):
+        c = self.c_cfg
+        self._ok(self.lib.swam_select(
+            self.h, _ptr(v, torch.float32, c.batch * c.n_frames * self.n_s, "v"),
+            _ptr(a, torch.float32, c.batch * self.n_s, "a"),
+            _ptr(keep_idx, torch.int32, c.batch * c.n_frames * self.k_max, "keep_idx"),
+            _ptr(keep_cnt, torch.int32, c.batch * c.n_frames, "keep_cnt"),
+            _ptr(pack_pos, torch.int32, self.rows_full, "pack_pos"),
+            _ptr(gather, torch.int32, self.rows_full, "gather"),
+            _ptr(cu_seqlens, torch.int32, c.batch + 1, "cu_seqlens")))
+
+    def set_selection(self, keep_idx, keep_cnt=None):
+        c = self.c_cfg
+        self._ok(self.lib.swam_set_selection(
+            self.h, _ptr(keep_idx, torch.int32, c.batch * c.n_frames * self.k_max, "keep_idx"),
+            _ptr(keep_cnt, torch.int32, c.batch * c.n_frames, "keep_cnt")))
+
+    def packed_rows(self) -> int:
+        r = C.c_int64()
+        self._ok(self.lib.swam_packed_rows(self.h, C.byref(r)))
+        return r.value
+
+    def export(self, s_all=None, q=None, v=None, a=None, keep_idx=None, keep_cnt=None,
+               pack_pos=None, gather=None, cu_seqlens=None):
+        c = self.c_cfg
+        n_s = self.n_s
+        self._ok(self.lib.swam_export(
+            self.h, _ptr(s_all, torch.float32, c.batch * c.n_blocks * c.n_frames * n_s, "s_all"),
+            _ptr(q, torch.float32, c.batch * c.n_blocks, "q"),
+            _ptr(v, torch.float32, c.batch * c.n_frames * n_s, "v"),
+            _ptr(a, torch.float32, c.batch * n_s, "a"),
+            _ptr(keep_idx, torch.int32, c.batch * c.n_frames * self.k_max, "keep_idx"),
+            _ptr(keep_cnt, torch.int32, c.batch * c.n_frames, "keep_cnt"),
+            _ptr(pack_pos, torch.int32, self.rows_full, "pack_pos"),
+            _ptr(gather, torch.int32, self.rows_full, "gather"),
+            _ptr(cu_seqlens, torch.int32, c.batch + 1, "cu_seqlens")))
+
+    # -- (3) pack / (5) unpack ---------------------------------------------------
+    def pack(self, x_full, x_packed):
+        d = self.c_cfg.d_model
+        self._ok(self.lib.swam_pack(self.h, _ptr(x_full, self.act_dtype, self.rows_full * d, "x_full"),
+                                    _ptr(x_packed, self.act_dtype, self.packed_rows() * d, "x_packed")))
+
+    def unpack(self, y_packed, x_full, y_full):
+        d = self.c_cfg.d_model
+        self._ok(self.lib.swam_unpack(
+            self.h, _ptr(y_packed, self.act_dtype, self.packed_rows() * d, "y_packed"),
+            _ptr(x_full, self.act_dtype, self.rows_full * d, "x_full"),
+            _ptr(y_full, self.act_dtype, self.rows_full * d, "y_full")))
+
+    # -- (4) block ---------------------------------------------------------------
+    def block(self, weights: dict, temb, x, n_rows=None, cu_seqlens=None, n_seqs=0, lse_out=None,
+              qkv_out=None):
+        c = self.c_cfg
+        d = c.d_model
+        n_rows = self.rows_full if n_rows is None else int(n_rows)
+        bw = BlockWeights()
+        for n in WEIGHT_NAMES:
+            setattr(bw, n, _ptr(weights[n], self.act_dtype, name=n))
+        self._ok(self.lib.swam_block(
+            self.h, C.byref(bw), _ptr(temb, torch.float32, c.d_temb, "temb"),
+            _ptr(x, self.act_dtype, n_rows * d, "x"), n_rows,
+            _ptr(cu_seqlens, torch.int32, None, "cu_seqlens"), n_seqs,
+            _ptr(lse_out, torch.float32, n_rows * c.n_heads, "lse_out"),
+            _ptr(qkv_out, self.act_dtype, n_rows * 3 * d, "qkv_out")))
+
+    # -- step --------------------------------------------------------------------
+    def step(self, model: Model, x_full, temb, tau: int, y_full, flags: int = 0) -> int:
+        c = self.c_cfg
+        n = self.rows_full * c.d_model
+        kind = C.c_int32(-1)
+        self._ok(self.lib.swam_step(
+            self.h, C.byref(model.struct), _ptr(x_full, self.act_dtype, n, "x_full"),
+            _ptr(temb, torch.float32, c.d_temb, "temb"), int(tau),
+            _ptr(y_full, self.act_dtype, n, "y_full"), int(flags), C.byref(kind)))
+        return kind.value
+
+    # -- timers ------------------------------------------------------------------
+    def timer_enable(self, classes, capacity=8192):
+        mask = 0
+        for cls in classes:
+            mask |= 1 << (T[cls] if isinstance(cls, str) else int(cls))
+        self._ok(self.lib.swam_timer_enable(self.h, mask, capacity))
+
+    def timer_reset(self):
+        self._ok(self.lib.swam_timer_reset(self.h))
+
+    def timer_read(self, cls) -> tuple[int, float]:
+        n, ms = C.c_int64(), C.c_double()
+        self._ok(self.lib.swam_timer_read(self.h, T[cls] if isinstance(cls, str) else int(cls),
+                                          C.byref(n), C.byref(ms)))
+        return n.value, ms.value

@@ -1,0 +1,85 @@
+"""Host-side checks of the C ABI (no GPU): exports, plan sizes, validation."""
+import ctypes as C
+import os
+import re
+
+import pytest
+
+import workload as W
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    from paper_2609_38984_amd import swam
+    if not os.path.exists(swam.LIB_PATH):
+        from paper_2609_38984_amd.build import build
+        build()
+    return swam.load_library()
+
+
+def _declared():
+    text = open(os.path.join(ROOT, "include", "swam.h")).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(swam_[a-z_]+)\s*\(", text)))
+
+
+def test_every_declared_symbol_is_exported(lib):
+    from paper_2609_38984_amd import swam
+    names = _declared()
+    assert len(names) == 19
+    assert sorted(swam.EXPORTS) == names
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def test_status_strings(lib):
+    for code, name in {0: "SWAM_OK", -1: "SWAM_E_INVALID", -4: "SWAM_E_STATE", -5: "SWAM_E_HIP"}.items():
+        assert lib.swam_status_str(code).decode() == name
+
+
+@pytest.mark.parametrize("n,want", [(1, (152, 64, 20)), (2, (1312, 660, 93)), (3, (10160, 3472, 364)),
+                                    (5, (3360, -1, 768))])
+def test_plan_sizes(lib, n, want):
+    from paper_2609_38984_amd import swam
+    cfg = W.preset(n)
+    p = swam.plan(cfg)
+    assert (p.l_full, p.t_pack_fixed, p.k_max) == want
+    assert p.rows_full == cfg.batch * cfg.l_full
+    assert p.group_size == cfg.g and p.n_s == cfg.n_s
+    assert p.k_layer_eff == min(6, cfg.n_blocks)
+    assert p.workspace_bytes > 0
+
+
+@pytest.mark.parametrize("bad,code", [
+    (dict(n_act=31), -1),              # H not divisible by F
+    (dict(k_core=60, k_anchor=8), -1),  # K_c + K_s > N_s
+    (dict(k_anchor=64), -1),           # K_s >= N_s
+    (dict(head_dim=32), -2),
+    (dict(d_model=100), -1),
+    (dict(n_blocks=0), -2),
+    (dict(reuse_R=0), -1),
+    (dict(frame_h=1, frame_w=1), -2),
+    (dict(mass_threshold=1.5), -1),
+    (dict(n_act=2 * 17, n_frames=2), -2),  # more than 16 queries per group
+])
+def test_plan_rejects_bad_configs(lib, bad, code):
+    from paper_2609_38984_amd import swam
+    base = W.preset(1)
+    cfg = swam.Config.from_obj(base)
+    for k, v in bad.items():
+        setattr(cfg, k, v)
+    info = swam.PlanInfo()
+    rc = lib.swam_plan(C.byref(cfg), C.byref(info))
+    assert rc == code
+    assert lib.swam_last_error(None).decode() != ""
+    out = C.c_void_p(123)
+    assert lib.swam_create(C.byref(cfg), None, C.byref(out)) == code   # rejected before any HIP call
+    assert out.value is None
+
+
+def test_null_context_is_rejected(lib):
+    assert lib.swam_pack(None, None, None) == -1
+    assert lib.swam_step(None, None, None, None, 0, None, 0, None) == -1
+    assert lib.swam_destroy(None) == 0

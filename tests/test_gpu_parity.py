@@ -1,0 +1,329 @@
+"""GPU parity of every C-ABI call against the CPU oracle on identical seeded inputs.
+
+Tolerances: fp32 scores 1e-5 max-relative per (sequence, frame) row; block
+outputs 1e-4 (fp32) and 2e-2 (bf16) max-relative; selection, packing
+metadata and permutations bit-exact when the GPU is fed the oracle's fp32
+scores; pruned rows bit-identical to the input.
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+import workload as W
+from helpers import act_dtype, dev, host, maxrel, model_for, rowwise_maxrel
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    torch.cuda.set_device(0)
+
+
+def _ctx(cfg):
+    from paper_2609_38984_amd import swam
+    return swam.Context(cfg)
+
+
+def _small_bf16(**kw):
+    base = dict(name="bf16-small", batch=1, d_model=256, n_heads=4, n_blocks=2, n_ctx=20,
+                n_frames=2, frame_h=8, frame_w=9, n_act=8, k_core=18, k_anchor=6, reuse_R=2,
+                n_steps=4, dtype="bf16", seed=7, blob_sigma=1.5)
+    base.update(kw)
+    return W.SwamConfig(**base)
+
+
+# ---------------------------------------------------------------------------
+# (4) block
+# ---------------------------------------------------------------------------
+def _block_case(cfg, cu, tol, lse_tol):
+    print(f"block case {cfg.name} cu={list(cu)}", flush=True)
+    blocks, dblocks, _ = model_for(cfg, 1)
+    x = W.make_inputs(cfg, blocks[0]["w_qkv"]).x(1)
+    n_rows = int(cu[-1])
+    x = x[:n_rows]
+    temb = W.timestep_embedding(cfg, 1)
+    y_ref, tr = O.block(x, blocks[0], temb, cu, cfg.n_heads, cfg.dtype)
+    ctx = _ctx(cfg)
+    xd = dev(x, act_dtype(cfg))
+    lse = torch.empty(n_rows, cfg.n_heads, dtype=torch.float32, device="cuda:0")
+    qkv = torch.empty(n_rows, 3 * cfg.d_model, dtype=act_dtype(cfg), device="cuda:0")
+    cud = dev(np.asarray(cu, np.int32))
+    ctx.block(dblocks[0], dev(temb), xd, n_rows, cud, len(cu) - 1, lse, qkv)
+    torch.cuda.synchronize()
+    e_y = maxrel(host(xd), y_ref)
+    e_q = maxrel(host(qkv), tr.qkv)
+    valid = np.zeros(n_rows, bool)
+    for a, b in zip(cu[:-1], cu[1:]):
+        valid[a:b] = True
+    e_l = float(np.abs(host(lse)[valid] - tr.lse[valid]).max())
+    print(f"  y {e_y:.2e} qkv {e_q:.2e} lse-abs {e_l:.2e}", flush=True)
+    assert e_q < tol and e_y < tol and e_l < lse_tol
+
+
+def test_block_fp32_dense():
+    cfg = W.preset(1)
+    _block_case(cfg, O.dense_cu(cfg), 1e-4, 1e-5)
+
+
+def test_block_fp32_ragged_packed():
+    cfg = W.preset(1).replace(batch=3)
+    _block_case(cfg, np.array([0, 37, 37, 190, 301]), 1e-4, 1e-5)
+
+
+def test_block_bf16_dense():
+    cfg = _small_bf16()
+    _block_case(cfg, O.dense_cu(cfg), 2e-2, 5e-2)
+
+
+def test_block_bf16_ragged_tails():
+    cfg = _small_bf16(batch=4)
+    # lengths 37, 0, 200, 129, 1: tiles cross sequence ends, an empty and a one-row sequence
+    _block_case(cfg, np.array([0, 37, 37, 237, 366, 367]), 2e-2, 5e-2)
+
+
+def test_block_bf16_wide():
+    cfg = W.preset(2).replace(n_blocks=1)
+    _block_case(cfg, O.dense_cu(cfg), 2e-2, 5e-2)
+
+
+# ---------------------------------------------------------------------------
+# (1) scoring
+# ---------------------------------------------------------------------------
+def _score_case(cfg, mode, scale=1.6):
+    print(f"score case {cfg.name} mode {mode}", flush=True)
+    rng = np.random.default_rng(cfg.seed + 100)
+    d, L, B = cfg.d_model, cfg.l_full, cfg.batch
+    qkv = (rng.standard_normal((B * L, 3 * d)) * scale).astype(np.float32)
+    if cfg.dtype == "bf16":
+        qkv = O.round_bf16(qkv).astype(np.float32)
+    act0 = cfg.n_ctx + cfg.n_fut
+    S_ref, lam_all = [], []
+    for b in range(B):
+        rows = qkv[b * L:(b + 1) * L]
+        q_act = rows[act0:, :d]
+        lam = O.lse_all_keys(q_act, rows[:, d:2 * d], cfg.n_heads)
+        lam_all.append(lam)
+        S_ref.append(O.score(q_act, rows[cfg.n_ctx:act0, d:2 * d], lam, cfg.n_frames, cfg.n_s,
+                             cfg.n_heads))
+    ctx = _ctx(cfg)
+    t = dev(qkv, act_dtype(cfg))
+    s_out = torch.empty(B * cfg.n_frames * cfg.n_s, dtype=torch.float32, device="cuda:0")
+    ld = 3 * d
+    flat = t.view(-1)
+    q_act = flat[act0 * ld:]                # action queries of sequence 0, row stride 3d
+    k_fut = flat[cfg.n_ctx * ld + d:]       # future keys inside the fused buffer
+    if mode == "A":
+        lse = dev(np.stack(lam_all).astype(np.float32))
+        ctx.score(q_act, L * ld, ld, k_fut, L * ld, ld, s_out, lse_act=lse)
+    else:
+        ctx.score(q_act, L * ld, ld, k_fut, L * ld, ld, s_out, k_all=flat[d:], kall_seq=L * ld)
+    torch.cuda.synchronize()
+    got = host(s_out).reshape(B, cfg.n_frames, cfg.n_s)
+    err = rowwise_maxrel(got, np.stack(S_ref))
+    print(f"  rowwise max-rel {err:.2e}", flush=True)
+    assert err < 1e-5
+
+
+@pytest.mark.parametrize("mode", ["A", "B"])
+def test_score_fp32(mode):
+    _score_case(W.preset(1), mode)
+
+
+@pytest.mark.parametrize("mode", ["A", "B"])
+def test_score_bf16_small(mode):
+    _score_case(_small_bf16(batch=2), mode)
+
+
+@pytest.mark.parametrize("mode", ["A", "B"])
+def test_score_bf16_wam_shape(mode):
+    # 8 frames x 1200 tokens, g = 6, 24 heads, keys inside a fused QKV buffer
+    _score_case(W.preset(3).replace(n_blocks=1), mode)
+
+
+def test_score_bf16_g16_batched():
+    cfg = _small_bf16(batch=3, n_act=32, n_frames=2, frame_h=7, frame_w=11)
+    _score_case(cfg, "A")
+
+
+# ---------------------------------------------------------------------------
+# (1 -> 2) reduce and (2) selection
+# ---------------------------------------------------------------------------
+def _random_scores(rng, B, L, F, n_s, ties=False):
+    if ties:
+        S = rng.integers(0, 4, (B, L, F, n_s)).astype(np.float64)
+    else:
+        S = rng.gamma(0.3, 1.0, (B, L, F, n_s))
+    S /= S.sum(axis=3, keepdims=True) * rng.uniform(1.0, 3.0, (B, L, F, 1))
+    S[:, :, :, :3] = 0.0
+    return O.round_f32(S).astype(np.float32)
+
+
+@pytest.mark.parametrize("n", [1, 2, 3, 5])
+def test_score_reduce(n):
+    cfg = W.preset(n)
+    print(f"reduce case {cfg.name}", flush=True)
+    rng = np.random.default_rng(40 + n)
+    S = _random_scores(rng, cfg.batch, cfg.n_blocks, cfg.n_frames, cfg.n_s)
+    ctx = _ctx(cfg)
+    V = torch.empty(cfg.batch * cfg.n_frames * cfg.n_s, dtype=torch.float32, device="cuda:0")
+    A = torch.empty(cfg.batch * cfg.n_s, dtype=torch.float32, device="cuda:0")
+    Q = torch.empty(cfg.batch * cfg.n_blocks, dtype=torch.float32, device="cuda:0")
+    core = torch.empty(cfg.batch * min(6, cfg.n_blocks), dtype=torch.int32, device="cuda:0")
+    ctx.score_reduce(dev(S), V, A, Q, core)
+    torch.cuda.synchronize()
+    for b in range(cfg.batch):
+        r = O.score_reduce(S[b], cfg.k_layer, cfg.cv_penalty)
+        k = min(6, cfg.n_blocks)
+        np.testing.assert_array_equal(host(core)[b * k:(b + 1) * k], r.L_core)
+        assert maxrel(host(Q)[b * cfg.n_blocks:(b + 1) * cfg.n_blocks], r.Q) < 1e-6
+        assert rowwise_maxrel(host(V).reshape(cfg.batch, cfg.n_frames, cfg.n_s)[b], r.V) < 1e-5
+        assert maxrel(host(A).reshape(cfg.batch, cfg.n_s)[b], r.A) < 1e-5
+
+
+def _select_case(cfg, seed, ties=False):
+    print(f"select case {cfg.name} seed {seed} ties {ties}", flush=True)
+    rng = np.random.default_rng(seed)
+    S = _random_scores(rng, cfg.batch, cfg.n_blocks, cfg.n_frames, cfg.n_s, ties)
+    Vs, As, sels = [], [], []
+    for b in range(cfg.batch):
+        r = O.score_reduce(S[b], cfg.k_layer, cfg.cv_penalty)
+        V, A = r.V.astype(np.float32), r.A.astype(np.float32)
+        if ties:
+            V = np.floor(V * 64) / 64
+            A = np.floor(A * 64) / 64
+        Vs.append(V)
+        As.append(A)
+        sels.append(O.select(V, A, cfg.k_core, cfg.k_anchor, cfg.mass_threshold))
+    pm = O.pack_map(O.keep_mask(cfg, [s.retained for s in sels]), cfg.batch)
+    ctx = _ctx(cfg)
+    kmax = ctx.k_max
+    ki = torch.empty(cfg.batch * cfg.n_frames * kmax, dtype=torch.int32, device="cuda:0")
+    kc = torch.empty(cfg.batch * cfg.n_frames, dtype=torch.int32, device="cuda:0")
+    pp = torch.empty(cfg.batch * cfg.l_full, dtype=torch.int32, device="cuda:0")
+    ga = torch.empty(cfg.batch * cfg.l_full, dtype=torch.int32, device="cuda:0")
+    cu = torch.empty(cfg.batch + 1, dtype=torch.int32, device="cuda:0")
+    ctx.select(dev(np.stack(Vs)), dev(np.stack(As)), ki, kc, pp, ga, cu)
+    torch.cuda.synchronize()
+    want_idx = np.full((cfg.batch, cfg.n_frames, kmax), -1, np.int64)
+    want_cnt = np.zeros((cfg.batch, cfg.n_frames), np.int64)
+    for b, s in enumerate(sels):
+        for f, r in enumerate(s.retained):
+            want_idx[b, f, :len(r)] = r
+            want_cnt[b, f] = len(r)
+    np.testing.assert_array_equal(ki.cpu().numpy().reshape(want_idx.shape), want_idx)
+    np.testing.assert_array_equal(kc.cpu().numpy().reshape(want_cnt.shape), want_cnt)
+    np.testing.assert_array_equal(pp.cpu().numpy(), pm.pack_pos)
+    np.testing.assert_array_equal(cu.cpu().numpy(), pm.cu_seqlens)
+    np.testing.assert_array_equal(ga.cpu().numpy()[:pm.cu_seqlens[-1]], pm.gather)
+    assert ctx.packed_rows() == pm.cu_seqlens[-1]
+
+
+@pytest.mark.parametrize("n", [1, 2, 3])
+def test_select_bitexact(n):
+    _select_case(W.preset(n), 50 + n)
+
+
+@pytest.mark.parametrize("pct", [10, 25, 50, 100])
+def test_select_bitexact_retention_sweep(pct):
+    _select_case(W.preset(4, percent=pct).replace(n_blocks=3), 60 + pct)
+
+
+def test_select_bitexact_heavy_ties():
+    _select_case(W.preset(2).replace(n_blocks=2), 71, ties=True)
+
+
+def test_select_mass_threshold_ragged():
+    _select_case(W.preset(5).replace(n_blocks=3, d_model=64, n_heads=1), 72)
+
+
+def test_select_mass_threshold_with_anchors():
+    _select_case(W.preset(5).replace(n_blocks=2, d_model=64, n_heads=1, batch=3, k_anchor=40,
+                                     mass_threshold=0.55), 73)
+
+
+# ---------------------------------------------------------------------------
+# (3) pack / (5) unpack
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("inplace", [False, True])
+def test_pack_unpack_permutation(inplace):
+    cfg = W.preset(5).replace(n_blocks=2, d_model=128, n_heads=2)
+    rng = np.random.default_rng(80)
+    S = _random_scores(rng, cfg.batch, cfg.n_blocks, cfg.n_frames, cfg.n_s)
+    V = np.stack([O.score_reduce(S[b]).V for b in range(cfg.batch)]).astype(np.float32)
+    A = np.stack([O.score_reduce(S[b]).A for b in range(cfg.batch)]).astype(np.float32)
+    sels = [O.select(V[b], A[b], cfg.k_core, cfg.k_anchor, cfg.mass_threshold) for b in range(cfg.batch)]
+    pm = O.pack_map(O.keep_mask(cfg, [s.retained for s in sels]), cfg.batch)
+    ctx = _ctx(cfg)
+    ctx.select(dev(V), dev(A))
+    T = ctx.packed_rows()
+    x = dev(rng.standard_normal((cfg.batch * cfg.l_full, cfg.d_model)).astype(np.float32), torch.bfloat16)
+    xp = torch.empty(T, cfg.d_model, dtype=torch.bfloat16, device="cuda:0")
+    ctx.pack(x, xp)
+    torch.cuda.synchronize()
+    assert torch.equal(xp.cpu(), x.cpu()[torch.from_numpy(pm.gather).long()])
+    yp = xp * 2
+    if inplace:
+        y = x.clone()
+        ctx.unpack(yp, y, y)
+    else:
+        y = torch.empty_like(x)
+        ctx.unpack(yp, x, y)
+    torch.cuda.synchronize()
+    pruned = torch.from_numpy(pm.pack_pos < 0)
+    yc, xc = y.cpu(), x.cpu()
+    assert torch.equal(yc[pruned].view(torch.int16), xc[pruned].view(torch.int16))
+    assert torch.equal(yc[~pruned], (xc * 2)[~pruned])
+
+
+# ---------------------------------------------------------------------------
+# step
+# ---------------------------------------------------------------------------
+def test_step_fp32_schedule_matches_oracle():
+    from paper_2609_38984_amd import swam
+    cfg = W.preset(1)
+    print(f"step schedule {cfg.name}", flush=True)
+    blocks, _, model = model_for(cfg)
+    inp = W.make_inputs(cfg, blocks[0]["w_qkv"])
+    ys, refr = O.run_schedule(cfg, blocks, inp.x, inp.temb)
+    ctx = _ctx(cfg)
+    kinds = []
+    for tau in range(cfg.n_steps):
+        x = dev(inp.x(tau))
+        y = torch.empty_like(x)
+        kinds.append(ctx.step(model, x, dev(inp.temb(tau)), tau, y))
+        torch.cuda.synchronize()
+        err = maxrel(host(y), ys[tau])
+        print(f"  tau {tau} kind {kinds[-1]} max-rel {err:.2e}", flush=True)
+        assert err < 1e-4
+        pruned = None
+        if tau in refr:
+            S = torch.empty(cfg.n_blocks * cfg.n_frames * cfg.n_s, dtype=torch.float32, device="cuda:0")
+            ki = torch.empty(cfg.n_frames * ctx.k_max, dtype=torch.int32, device="cuda:0")
+            ctx.export(s_all=S, keep_idx=ki)
+            torch.cuda.synchronize()
+            assert rowwise_maxrel(host(S).reshape(refr[tau].S_all.shape), refr[tau].S_all) < 1e-5
+            want = np.concatenate([np.asarray(r) for r in refr[tau].selection[0].retained])
+            np.testing.assert_array_equal(ki.cpu().numpy(), want)
+        else:
+            pm = refr[cfg.reuse_R * (tau // cfg.reuse_R)].packmap
+            pruned = pm.pack_pos < 0
+            xc = x.cpu().numpy()
+            assert y.cpu().numpy()[pruned].tobytes() == xc[pruned].tobytes()
+    assert kinds == [swam.KIND_REFRESH, swam.KIND_SPARSE] * 2
+
+
+def test_sparse_step_before_refresh_is_rejected():
+    from paper_2609_38984_amd import swam
+    cfg = W.preset(1)
+    _, _, model = model_for(cfg)
+    ctx = _ctx(cfg)
+    x = torch.zeros(cfg.l_full, cfg.d_model, device="cuda:0")
+    with pytest.raises(swam.SwamError) as e:
+        ctx.step(model, x, torch.zeros(cfg.d_temb, device="cuda:0"), 1, x)
+    assert e.value.code == -4
