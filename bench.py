@@ -1,0 +1,336 @@
+"""Benchmark of the action-guided sparse denoising step on one MI355X.
+
+A bench "step" is one denoising step of the schedule: a refresh step (dense
+forward with per-layer scoring, score reduction, selection and pack map) when
+tau mod R == 0, otherwise a sparse step (pack, blocks on the packed sequence,
+unpack).  K timed steps therefore cover every part of the hot path.
+
+value = K * batch * l_full / (timed seconds): full-latent tokens advanced per
+second over the schedule, inputs already resident in HBM.  Alongside: the
+dense, refresh and sparse step rates, the sparse/dense speedup, the score+pack
+overhead as a percentage of the dense step, per-phase times, the roofline of
+the dominant kernel (HIP events on the library's stream during the timed
+steps) and the CPU oracle timed on a bounded sample of the same workload.
+
+Default workload: the 28-block d=1536 WAM-scale DiT (8 frames x 30x40 future
+tokens, 512 context, 48 action tokens, 25% + 64 retention, R = 2).
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import statistics
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "sparse denoise-step tokens/sec vs dense at 1 MI355X; score+pack overhead %"
+PEAK_BF16_TFLOPS = 2500.0
+PEAK_FP32_TFLOPS = 157.3
+PEAK_HBM_GBS = 8000.0
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def workload_from_args(args):
+    import workload as W
+    if args.config == 4:
+        return W.preset(4, percent=args.percent, reuse_R=args.reuse or 2)
+    cfg = W.preset(args.config)
+    if args.reuse:
+        cfg = cfg.replace(reuse_R=args.reuse)
+    return cfg
+
+
+def kernel_work(cfg, cls, rows_per_seq):
+    """Algorithmic flops (GEMMs, attention) or bytes (memory-bound phases) of one
+    launch of class `cls` on sequences of the given lengths."""
+    d = cfg.d_model
+    hid = cfg.mlp_ratio * d
+    m = sum(rows_per_seq)
+    esz = 2 if cfg.dtype == "bf16" else 4
+    if cls == "GEMM_QKV":
+        return 2.0 * m * 3 * d * d
+    if cls == "GEMM_OUT":
+        return 2.0 * m * d * d
+    if cls == "GEMM_UP":
+        return 2.0 * m * hid * d
+    if cls == "GEMM_DOWN":
+        return 2.0 * m * d * hid
+    if cls == "ATTN":
+        return float(sum(4.0 * r * r * d for r in rows_per_seq))
+    if cls == "SCORE":
+        # one read of the future keys, the action queries and normalisers; S written
+        return float(cfg.batch * (cfg.n_fut * d * esz + cfg.n_act * d * esz
+                                  + cfg.n_act * cfg.n_heads * 4 + cfg.n_fut * 4))
+    if cls in ("PACK", "UNPACK"):
+        return 2.0 * m * d * esz
+    raise KeyError(cls)
+
+
+BOUND = {"GEMM_QKV": "mfma", "GEMM_OUT": "mfma", "GEMM_UP": "mfma", "GEMM_DOWN": "mfma",
+         "ATTN": "mfma", "SCORE": "hbm", "PACK": "hbm", "UNPACK": "hbm"}
+
+
+def step_flops(cfg, rows):
+    """Flop model of one block on a sequence of `rows` tokens: 24 d^2 T + 4 d T^2."""
+    d = cfg.d_model
+    return 24.0 * d * d * rows + 4.0 * d * rows * rows
+
+
+def cpu_baseline(cfg, kinds, blocks_np, inp):
+    """The oracle timed on a bounded sample of the workload: one packed block,
+    one layer's scoring and one score-reduce + selection are measured; a dense
+    block is extrapolated from the packed one by the flop model; the total is
+    scaled to the timed schedule."""
+    import oracle as O
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        cores = len(os.sched_getaffinity(0))
+    x = inp.x(0)
+    temb = inp.temb(0)
+    w = blocks_np[0]
+    rng = np.random.default_rng(0)
+    d = cfg.d_model
+    t0 = time.perf_counter()
+    for b in range(cfg.batch):
+        q = rng.standard_normal((cfg.n_act, d))
+        k = rng.standard_normal((cfg.n_fut, d))
+        O.score(q, k, np.full((cfg.n_act, cfg.n_heads), 10.0), cfg.n_frames, cfg.n_s, cfg.n_heads)
+    t_score = time.perf_counter() - t0
+    S_all = rng.random((cfg.batch, cfg.n_blocks, cfg.n_frames, cfg.n_s)) / cfg.n_s
+    t0 = time.perf_counter()
+    _, _, pm = O.selection_from_scores(cfg, S_all)
+    t_select = time.perf_counter() - t0
+    t0 = time.perf_counter()
+    O.block(O.pack(x, pm), w, temb, pm.cu_seqlens, cfg.n_heads, cfg.dtype)
+    t_sparse_block = time.perf_counter() - t0
+    packed = [int(pm.cu_seqlens[b + 1] - pm.cu_seqlens[b]) for b in range(cfg.batch)]
+    ratio = (sum(step_flops(cfg, cfg.l_full) for _ in range(cfg.batch))
+             / sum(step_flops(cfg, r) for r in packed))
+    t_dense_block = t_sparse_block * ratio
+    how = f"dense block extrapolated by the flop model (x{ratio:.2f})"
+    if t_dense_block < 25.0:   # fast host: measure the dense block as well
+        t0 = time.perf_counter()
+        O.block(x, w, temb, O.dense_cu(cfg), cfg.n_heads, cfg.dtype)
+        t_dense_block = time.perf_counter() - t0
+        how = f"one dense block ({cfg.batch * cfg.l_full} tokens) {t_dense_block:.1f}s"
+    n_ref = sum(1 for k in kinds if k == 1)
+    n_sp = len(kinds) - n_ref
+    total = (cfg.n_blocks * (n_ref * (t_dense_block + t_score) + n_sp * t_sparse_block)
+             + n_ref * t_select)
+    tokens = len(kinds) * cfg.batch * cfg.l_full
+    return {"value": round(tokens / total, 2), "unit": "tokens/s", "cores": int(cores),
+            "kind": "oracle",
+            "sample": (f"measured: one packed block ({sum(packed)} tokens) {t_sparse_block:.1f}s, "
+                       f"one layer of scoring {t_score:.2f}s, one reduce+select {t_select:.2f}s, "
+                       f"{how}; scaled to {cfg.n_blocks} blocks x {len(kinds)} steps "
+                       f"({n_ref} refresh, {n_sp} sparse)"),
+            "sample_seconds": round(t_sparse_block + t_score + t_select
+                                    + (t_dense_block if how.startswith("one") else 0.0), 2)}
+
+
+KERNEL_OF_CLASS = {"ATTN": ("attn_fwd", None), "GEMM_QKV": ("gemm", ", 0>"),
+                   "GEMM_UP": ("gemm", ", 1>"), "GEMM_OUT": ("gemm", ", 2>"),
+                   "GEMM_DOWN": ("gemm", ", 2>"), "SCORE": ("score_", None),
+                   "PACK": ("pack_rows", None), "UNPACK": ("unpack_", None)}
+
+
+def summarize_rocprof(db_path, bench_json):
+    """Per-kernel table of a rocprofv3 kernel trace of this benchmark, plus the
+    average duration of the dominant class over exactly the timed steps."""
+    import sqlite3
+    res = json.load(open(bench_json))
+    con = sqlite3.connect(db_path)
+    rows = con.execute("select name, start, end from kernels order by start").fetchall()
+    agg = {}
+    for name, a, b in rows:
+        short = name.split("(")[0].replace("void ", "")
+        n, t = agg.get(short, (0, 0))
+        agg[short] = (n + 1, t + (b - a))
+    lines = [f"{'calls':>7} {'avg_us':>10} {'total_ms':>10}  kernel"]
+    for k, (n, t) in sorted(agg.items(), key=lambda kv: -kv[1][1]):
+        lines.append(f"{n:7d} {t / n / 1e3:10.2f} {t / 1e6:10.2f}  {k}")
+    rf = res["roofline"]
+    cls = rf["kernel"]
+    sub, epi = KERNEL_OF_CLASS[cls]
+    seq = [(a, b) for name, a, b in rows if sub in name and (epi is None or epi in name)]
+    if cls in ("GEMM_OUT", "GEMM_DOWN"):
+        seq = seq[0::2] if cls == "GEMM_OUT" else seq[1::2]
+    per_step = res["config"]["n_blocks"]
+    skip = res["warmup"] * per_step
+    win = seq[skip: skip + rf["launches"]]
+    avg = sum(b - a for a, b in win) / max(len(win), 1) / 1e3
+    lines.append("")
+    lines.append(f"timed window: {cls} launches {skip}..{skip + len(win) - 1}: "
+                 f"avg {avg:.2f} us (bench live HIP-event average {rf['avg_launch_us']:.2f} us)")
+    return "\n".join(lines)
+
+
+def main():
+    if len(sys.argv) > 1 and sys.argv[1] == "--summarize":
+        print(summarize_rocprof(sys.argv[2], sys.argv[3]))
+        return
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--config", type=int, default=3)
+    ap.add_argument("--percent", type=int, default=25, help="retention for workload 4")
+    ap.add_argument("--reuse", type=int, default=0, help="override the reuse interval R")
+    ap.add_argument("--reps", type=int, default=5, help="repetitions per step kind for medians")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs on one GPU only: the step is single-GPU "
+                          "data parallel work with no collectives; run with --gpus 1"}))
+        sys.exit(2)
+
+    import torch
+    import workload as W
+    from paper_2609_38984_amd import swam
+
+    cfg = workload_from_args(args)
+    torch.cuda.set_device(0)
+    dev = torch.device("cuda:0")
+    adt = torch.bfloat16 if cfg.dtype == "bf16" else torch.float32
+    log(f"[bench] workload {cfg.name}: B={cfg.batch} L_full={cfg.l_full} d={cfg.d_model} "
+        f"blocks={cfg.n_blocks} K_c+K_s={cfg.k_core}+{cfg.k_anchor} R={cfg.reuse_R}")
+
+    t0 = time.perf_counter()
+    blocks_np, dblocks = [], []
+    for l in range(cfg.n_blocks):
+        b = W.block_weights(cfg, l)
+        if l == 0:
+            blocks_np.append(b)
+        dblocks.append({k: torch.from_numpy(v).to(dev, adt) for k, v in b.items()})
+    model = swam.Model(dblocks, adt)
+    inp = W.make_inputs(cfg, blocks_np[0]["w_qkv"])
+    n_sched = cfg.n_steps
+    xs = [torch.from_numpy(inp.x(t)).to(dev, adt) for t in range(n_sched)]
+    tembs = [torch.from_numpy(inp.temb(t)).to(dev) for t in range(n_sched)]
+    y = torch.empty_like(xs[0])
+    log(f"[bench] inputs resident in HBM ({time.perf_counter() - t0:.1f}s)")
+
+    ctx = swam.Context(cfg)
+    ctx.timer_enable(swam.TIMERS, capacity=1 << 15)
+
+    def run(tau, flags=0):
+        return ctx.step(model, xs[tau % n_sched], tembs[tau % n_sched], tau, y, flags)
+
+    # warm-up (instrumented: per-phase times pick the dominant kernel)
+    warm_kinds = [run(t) for t in range(max(args.warmup, 2))]
+    torch.cuda.synchronize()
+    phase = {}
+    for cls in swam.TIMERS:
+        n, ms = ctx.timer_read(cls)
+        phase[cls] = (n, ms)
+    dominant = max(BOUND, key=lambda c: phase[c][1])
+    log(f"[bench] warm-up kinds {warm_kinds}; dominant kernel class {dominant}")
+
+    # timed region: exactly K steps, only the dominant class bracketed by events
+    ctx.timer_enable([dominant], capacity=max(64, args.steps * cfg.n_blocks * 2))
+    torch.cuda.synchronize()
+    t_start = time.perf_counter()
+    kinds = [run(t) for t in range(args.steps)]
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t_start
+    n_dom, ms_dom = ctx.timer_read(dominant)
+    packed = ctx.packed_rows()
+    log(f"[bench] timed {args.steps} steps in {elapsed * 1e3:.2f} ms; kinds {kinds}")
+
+    # algorithmic work of the dominant class over the timed launches
+    full_rows = [cfg.l_full] * cfg.batch
+    cu = torch.empty(cfg.batch + 1, dtype=torch.int32, device=dev)
+    ctx.export(cu_seqlens=cu)
+    cuh = cu.cpu().numpy()
+    packed_rows = [int(cuh[b + 1] - cuh[b]) for b in range(cfg.batch)]
+    per_kind_rows = {swam.KIND_REFRESH: full_rows, swam.KIND_DENSE: full_rows,
+                     swam.KIND_SPARSE: packed_rows}
+    if dominant in ("SCORE",):
+        work = sum(kernel_work(cfg, dominant, full_rows) * cfg.n_blocks
+                   for k in kinds if k == swam.KIND_REFRESH)
+    elif dominant in ("PACK", "UNPACK"):
+        work = sum(kernel_work(cfg, dominant, packed_rows) for k in kinds if k == swam.KIND_SPARSE)
+    else:
+        work = sum(kernel_work(cfg, dominant, per_kind_rows[k]) * cfg.n_blocks for k in kinds)
+    bound = BOUND[dominant]
+    if bound == "mfma":
+        achieved = work / (ms_dom * 1e-3) / 1e12
+        peak = PEAK_BF16_TFLOPS if cfg.dtype == "bf16" else PEAK_FP32_TFLOPS
+        unit = "TFLOP/s"
+    else:
+        achieved = work / (ms_dom * 1e-3) / 1e9
+        peak = PEAK_HBM_GBS
+        unit = "GB/s"
+    roofline = {"kernel": dominant, "bound": bound, "achieved": round(achieved, 2), "peak": peak,
+                "unit": unit, "frac": round(achieved / peak, 4), "traffic": None,
+                "launches": n_dom, "avg_launch_us": round(ms_dom * 1e3 / max(n_dom, 1), 2)}
+
+    # step medians per kind and per-phase breakdown over one schedule
+    def median_ms(flags, tau, reps):
+        ts = []
+        for _ in range(reps):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            run(tau, flags)
+            e1.record()
+            torch.cuda.synchronize()
+            ts.append(e0.elapsed_time(e1))
+        return statistics.median(ts)
+
+    ctx.timer_enable([], 1)
+    t_dense = median_ms(swam.FORCE_DENSE, 0, args.reps)
+    t_refresh = median_ms(swam.FORCE_REFRESH, 0, args.reps)
+    t_sparse = median_ms(0, 1 if cfg.reuse_R > 1 else 0, args.reps) if cfg.reuse_R > 1 else float("nan")
+    ctx.timer_enable(swam.TIMERS, capacity=1 << 15)
+    sched = [run(t) for t in range(n_sched)]
+    torch.cuda.synchronize()
+    phase_ms = {cls: round(ctx.timer_read(cls)[1] / n_sched, 4) for cls in swam.TIMERS}
+    ctx.timer_enable([], 1)
+    over = (phase_ms["SCORE"] + phase_ms["REDUCE"] + phase_ms["SELECT"] + phase_ms["PACK"]
+            + phase_ms["UNPACK"])
+    tok = cfg.batch * cfg.l_full
+    value = args.steps * tok / elapsed
+    out = {
+        "metric": METRIC, "value": round(value, 1), "unit": "tokens/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": max(args.warmup, 2),
+        "ms_per_step": round(elapsed * 1e3 / args.steps, 4), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": cfg.dtype, "data": "synthetic",
+        "config": {"workload": cfg.name, "batch": cfg.batch, "l_full": cfg.l_full,
+                   "d_model": cfg.d_model, "n_blocks": cfg.n_blocks,
+                   "frames": f"{cfg.n_frames}x{cfg.frame_h}x{cfg.frame_w}",
+                   "n_ctx": cfg.n_ctx, "n_act": cfg.n_act,
+                   "k_core": cfg.k_core, "k_anchor": cfg.k_anchor,
+                   "mass_threshold": cfg.mass_threshold, "reuse_R": cfg.reuse_R,
+                   "packed_rows": packed, "schedule_kinds": kinds},
+        "dense_step_ms": round(t_dense, 4), "refresh_step_ms": round(t_refresh, 4),
+        "sparse_step_ms": round(t_sparse, 4),
+        "dense_tokens_per_s": round(tok / t_dense * 1e3, 1),
+        "sparse_tokens_per_s": round(tok / t_sparse * 1e3, 1),
+        "refresh_tokens_per_s": round(tok / t_refresh * 1e3, 1),
+        "speedup_sparse_vs_dense": round(t_dense / t_sparse, 3),
+        "speedup_schedule_vs_dense": round(t_dense / (elapsed * 1e3 / args.steps), 3),
+        "overhead_pct_of_dense": round(100.0 * over / t_dense, 3),
+        "phase_ms_per_step": phase_ms,
+        "roofline": roofline,
+    }
+    if not args.no_cpu_baseline:
+        log("[bench] timing the CPU oracle on a bounded sample")
+        out["cpu_baseline"] = cpu_baseline(cfg, kinds, blocks_np, inp)
+    else:
+        out["cpu_baseline"] = None
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()
