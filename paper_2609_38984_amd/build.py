@@ -22,6 +22,13 @@ HIPCC_FLAGS = [
 ]
 
 
+# per-source code-generation flags: attention keeps its MFMA accumulators in VGPRs so the
+# softmax can rescale them without AGPR round trips
+EXTRA_DEVICE_FLAGS = {
+    "k_attn.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"],
+}
+
+
 def _hipcc() -> str:
     for cand in (shutil.which("hipcc"), "/opt/rocm/bin/hipcc"):
         if cand and os.path.exists(cand):
@@ -31,7 +38,8 @@ def _hipcc() -> str:
 
 def _compile(src: str) -> str:
     obj = os.path.join(OBJ, os.path.basename(src) + ".o")
-    cmd = [_hipcc(), *HIPCC_FLAGS, "-c", src, "-o", obj]
+    extra = EXTRA_DEVICE_FLAGS.get(os.path.basename(src), [])
+    cmd = [_hipcc(), *HIPCC_FLAGS, *extra, "-c", src, "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"hipcc failed for {src}:\n{r.stderr}")

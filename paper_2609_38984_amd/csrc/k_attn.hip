@@ -93,6 +93,9 @@ attn_fwd_bf16(const bf16_t* __restrict__ qkv, bf16_t* __restrict__ out, float* _
 #pragma unroll
     for (int r = 0; r < 16; ++r) o[t][r] = 0.0f;
   float m_run = -1e30f, l_run = 0.0f;
+  bf16x2 ones2;
+  ones2[0] = (__bf16)1.0f;
+  ones2[1] = (__bf16)1.0f;
   const float sc = 1.4426950408889634f * 0.125f;      // log2(e) / sqrt(64)
 
   const int nkt = (s1 - s0 + ATT_BK - 1) / ATT_BK;
@@ -118,40 +121,57 @@ attn_fwd_bf16(const bf16_t* __restrict__ qkv, bf16_t* __restrict__ out, float* _
         st[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[s], st[t], 0, 0, 0);
       }
     }
-    // mask keys beyond the sequence (last tile only)
+    // keys beyond the sequence exist only in the last tile (wave-uniform branch)
     const int nvalid = s1 - kb;
-    float mx = -1e30f;
+    if (nvalid < ATT_BK) {
 #pragma unroll
-    for (int t = 0; t < 2; ++t)
+      for (int t = 0; t < 2; ++t)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int key = 32 * t + 8 * (r >> 2) + 4 * g + (r & 3);
-        float v = st[t][r] * sc;
-        v = key < nvalid ? v : -INFINITY;
-        st[t][r] = v;
-        mx = fmaxf(mx, v);
-      }
-    mx = fmaxf(mx, __shfl_xor(mx, 32));
-    const float m_new = fmaxf(m_run, mx);
-    const float corr = __builtin_amdgcn_exp2f(m_run - m_new);
-    m_run = m_new;
-    float psum = 0.0f;
-    bf16x8 pf[2][2];
-#pragma unroll
-    for (int t = 0; t < 2; ++t)
-#pragma unroll
-      for (int u = 0; u < 2; ++u)
-#pragma unroll
-        for (int mm = 0; mm < 8; ++mm) {
-          const float p = __builtin_amdgcn_exp2f(st[t][8 * u + mm] - m_new);
-          psum += p;
-          pf[t][u][mm] = (__bf16)p;
+        for (int r = 0; r < 16; ++r) {
+          const int key = 32 * t + 8 * (r >> 2) + 4 * g + (r & 3);
+          if (key >= nvalid) st[t][r] = -INFINITY;
         }
-    l_run = l_run * corr + psum;
+    }
+    // row max of the raw logits: 16 keys in-lane per half tile, the rest in lane ^ 32
+    float mx = st[0][0];
 #pragma unroll
     for (int t = 0; t < 2; ++t)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) o[t][r] *= corr;
+      for (int r = 0; r < 16; ++r) mx = fmaxf(mx, st[t][r]);
+    mx = fmaxf(mx, __shfl_xor(mx, 32));
+    // lazy rescaling: the running max (log2 units) is only raised when some row of
+    // the wave grew by more than 2^8; otherwise p <= 256 against the stale max
+    const float m_tile = mx * sc;
+    if (__any(m_tile > m_run + 8.0f)) {
+      const float m_new = fmaxf(m_run, m_tile);
+      const float corr = __builtin_amdgcn_exp2f(m_run - m_new);
+      m_run = m_new;
+      l_run *= corr;
+#pragma unroll
+      for (int t = 0; t < 2; ++t)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) o[t][r] *= corr;
+    }
+    // p = exp2(s * sc - m); P^T packed to bf16 pairs; row sum from the same bf16 values
+    bf16x8 pf[2][2];
+    float psum = 0.0f;
+#pragma unroll
+    for (int t = 0; t < 2; ++t)
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+#pragma unroll
+        for (int mm = 0; mm < 8; mm += 2) {
+          const float p0 = __builtin_amdgcn_exp2f(fmaf(st[t][8 * u + mm], sc, -m_run));
+          const float p1 = __builtin_amdgcn_exp2f(fmaf(st[t][8 * u + mm + 1], sc, -m_run));
+          bf16x2 pp;
+          pp[0] = (__bf16)p0;
+          pp[1] = (__bf16)p1;
+          pf[t][u][mm] = pp[0];
+          pf[t][u][mm + 1] = pp[1];
+          psum = __builtin_amdgcn_fdot2_f32_bf16(pp, ones2, psum, false);
+        }
+      }
+    l_run += psum;
 
     // O^T += V^T P^T; k-substep (t, u) covers keys 32t + 16u + {4g..4g+3, 8+4g..8+4g+3}
 #pragma unroll

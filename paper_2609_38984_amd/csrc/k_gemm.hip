@@ -14,9 +14,12 @@
 namespace swam {
 
 __device__ __forceinline__ float gelu_tanh(float u) {
-  // 0.5 u (1 + tanh(z)) = u / (1 + exp(-2 z)), z = sqrt(2/pi) (u + 0.044715 u^3)
-  const float z = 0.7978845608028654f * (u + 0.044715f * u * u * u);
-  return u / (1.0f + expf(-2.0f * z));
+  // 0.5 u (1 + tanh(z)) = u / (1 + exp(-2 z)), z = sqrt(2/pi) (u + 0.044715 u^3);
+  // exp(-2z) = exp2(-2 log2(e) z) on the hardware exp2, then the hardware reciprocal
+  // (both about 1 ulp: far below the bf16 rounding of the stored result)
+  const float z2 = -2.0f * 1.4426950408889634f * 0.7978845608028654f *
+                   (u + 0.044715f * u * u * u);
+  return u * __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(z2));
 }
 
 template <int EPI>
@@ -46,42 +49,75 @@ __device__ __forceinline__ void tile_of(int pid, int nwg, int tiles_m, int tiles
   tn = (id % in_group) / gsz;
 }
 
+typedef __attribute__((address_space(3))) void lds_void_t;
+typedef __attribute__((address_space(1))) void glb_void_t;
+
+// one k-stage (64) of MFMAs from a staged A/B tile pair
+template <int BM, int BN, int TM, int TN, int FM, int FN>
+__device__ __forceinline__ void mma_stage(const uint4* __restrict__ as, const uint4* __restrict__ bs,
+                                          int wm, int wn, int lane, f32x16 (&acc)[FM][FN]) {
+  const int khalf = lane >> 5, r31 = lane & 31;
+#pragma unroll
+  for (int s = 0; s < GEMM_BK / 16; ++s) {
+    const int chunk = 2 * s + khalf;
+    bf16x8 af[FM], bfr[FN];
+#pragma unroll
+    for (int i = 0; i < FM; ++i) {
+      const int row = wm * TM + i * 32 + r31;
+      af[i] = __builtin_bit_cast(bf16x8, as[row * 8 + (chunk ^ (row & 7))]);
+    }
+#pragma unroll
+    for (int j = 0; j < FN; ++j) {
+      const int row = wn * TN + j * 32 + r31;
+      bfr[j] = __builtin_bit_cast(bf16x8, bs[row * 8 + (chunk ^ (row & 7))]);
+    }
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+      for (int j = 0; j < FN; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
+  }
+}
+
+// Stage loads go global -> LDS directly (no registers): each instruction moves
+// 8 rows x 128 bytes; lane i lands at slot i of the 1 KB slab, i.e. row
+// lane >> 3 and physical chunk lane & 7, so it fetches logical chunk
+// (lane & 7) ^ (row & 7) -- the swizzle is applied on the global side.
 template <int BM, int BN, int WM, int WN, int EPI>
 __global__ void __launch_bounds__(WM * WN * 64)
 gemm_bf16_nt(const bf16_t* __restrict__ A, int64_t lda, const bf16_t* __restrict__ B,
              int64_t ldb, const bf16_t* __restrict__ bias, const float* __restrict__ gate,
              bf16_t* C, int64_t ldc, int M, int N, int K, int tiles_m, int tiles_n) {
-  constexpr int NT = WM * WN * 64;
+  constexpr int NW = WM * WN;
   constexpr int TM = BM / WM, TN = BN / WN;
   constexpr int FM = TM / 32, FN = TN / 32;
-  constexpr int A_LD = BM * 8 / NT;   // 16-byte chunks per thread per stage
-  constexpr int B_LD = BN * 8 / NT;
-  static_assert(A_LD * NT == BM * 8 && B_LD * NT == BN * 8, "tile/threads mismatch");
-  extern __shared__ uint4 lds[];
-  uint4* As = lds;                    // [2][BM*8]
-  uint4* Bs = lds + 2 * BM * 8;       // [2][BN*8]
+  constexpr int A_INS = BM / 8 / NW, B_INS = BN / 8 / NW;
+  static_assert(A_INS * 8 * NW == BM && B_INS * 8 * NW == BN, "tile/waves mismatch");
+  __shared__ uint4 lds[2 * (BM + BN) * 8];   // [stage][A rows | B rows][8 chunks]
 
   int tm, tn;
   tile_of(blockIdx.x, gridDim.x, tiles_m, tiles_n, tm, tn);
   const int m0 = tm * BM, n0 = tn * BN;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave / WN, wn = wave % WN;
+  const int lrow = lane >> 3, lchunk = (lane & 7) ^ lrow;
 
-  // global -> register staging: thread owns chunk (tid & 7) of rows (tid >> 3) + i * NT / 8
-  const int lc = tid & 7, lr = tid >> 3;
-  const bf16_t* a_base = A + lc * 8;
-  const bf16_t* b_base = B + lc * 8;
-  auto a_ptr = [&](int i) {
-    return a_base + (int64_t)min(m0 + lr + i * (NT / 8), M - 1) * lda;
+  auto a_src = [&](int j) {
+    return A + (int64_t)min(m0 + (wave * A_INS + j) * 8 + lrow, M - 1) * lda + 8 * lchunk;
   };
-  auto b_ptr = [&](int i) {
-    return b_base + (int64_t)min(n0 + lr + i * (NT / 8), N - 1) * ldb;
+  auto b_src = [&](int j) {
+    return B + (int64_t)min(n0 + (wave * B_INS + j) * 8 + lrow, N - 1) * ldb + 8 * lchunk;
   };
-  auto lds_slot = [&](int i) {
-    const int row = lr + i * (NT / 8);
-    return row * 8 + (lc ^ (row & 7));
+  auto issue = [&](uint4* as, uint4* bs, int k0) {
+#pragma unroll
+    for (int j = 0; j < A_INS; ++j)
+      __builtin_amdgcn_global_load_lds((glb_void_t*)(a_src(j) + k0),
+                                       (lds_void_t*)(as + (wave * A_INS + j) * 64), 16, 0, 0);
+#pragma unroll
+    for (int j = 0; j < B_INS; ++j)
+      __builtin_amdgcn_global_load_lds((glb_void_t*)(b_src(j) + k0),
+                                       (lds_void_t*)(bs + (wave * B_INS + j) * 64), 16, 0, 0);
   };
-  uint4 ra[A_LD], rb[B_LD];
 
   f32x16 acc[FM][FN];
 #pragma unroll
@@ -91,89 +127,74 @@ gemm_bf16_nt(const bf16_t* __restrict__ A, int64_t lda, const bf16_t* __restrict
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
 
+  constexpr int STAGE = (BM + BN) * 8;
   const int KT = K / GEMM_BK;
-#pragma unroll
-  for (int i = 0; i < A_LD; ++i) ra[i] = *(const uint4*)a_ptr(i);
-#pragma unroll
-  for (int i = 0; i < B_LD; ++i) rb[i] = *(const uint4*)b_ptr(i);
-#pragma unroll
-  for (int i = 0; i < A_LD; ++i) As[lds_slot(i)] = ra[i];
-#pragma unroll
-  for (int i = 0; i < B_LD; ++i) Bs[lds_slot(i)] = rb[i];
+  issue(lds, lds + BM * 8, 0);
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   __syncthreads();
-
-  // per-lane operand row offsets inside the stage (rows are fixed per lane)
-  int a_row[FM], b_row[FN];
-#pragma unroll
-  for (int i = 0; i < FM; ++i) a_row[i] = wm * TM + i * 32 + (lane & 31);
-#pragma unroll
-  for (int j = 0; j < FN; ++j) b_row[j] = wn * TN + j * 32 + (lane & 31);
-  const int khalf = lane >> 5;
-
   for (int kt = 0; kt < KT; ++kt) {
-    const int cur = kt & 1;
-    {
-      // prefetch the next stage (the last iteration re-reads a valid stage; unused)
-      const int off = min(kt + 1, KT - 1) * GEMM_BK;
-#pragma unroll
-      for (int i = 0; i < A_LD; ++i) ra[i] = *(const uint4*)(a_ptr(i) + off);
-#pragma unroll
-      for (int i = 0; i < B_LD; ++i) rb[i] = *(const uint4*)(b_ptr(i) + off);
-    }
-    const uint4* as = As + cur * BM * 8;
-    const uint4* bs = Bs + cur * BN * 8;
-#pragma unroll
-    for (int s = 0; s < GEMM_BK / 16; ++s) {
-      const int chunk = 2 * s + khalf;
-      bf16x8 af[FM], bfr[FN];
-#pragma unroll
-      for (int i = 0; i < FM; ++i) {
-        uint4 v = as[a_row[i] * 8 + (chunk ^ (a_row[i] & 7))];
-        af[i] = __builtin_bit_cast(bf16x8, v);
-      }
-#pragma unroll
-      for (int j = 0; j < FN; ++j) {
-        uint4 v = bs[b_row[j] * 8 + (chunk ^ (b_row[j] & 7))];
-        bfr[j] = __builtin_bit_cast(bf16x8, v);
-      }
-#pragma unroll
-      for (int i = 0; i < FM; ++i)
-#pragma unroll
-        for (int j = 0; j < FN; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
-    }
-    {
-      // the other stage was released by the barrier of the previous iteration
-      uint4* an = As + (cur ^ 1) * BM * 8;
-      uint4* bn = Bs + (cur ^ 1) * BN * 8;
-#pragma unroll
-      for (int i = 0; i < A_LD; ++i) an[lds_slot(i)] = ra[i];
-#pragma unroll
-      for (int i = 0; i < B_LD; ++i) bn[lds_slot(i)] = rb[i];
-    }
+    uint4* cur = lds + (kt & 1) * STAGE;
+    uint4* nxt = lds + ((kt + 1) & 1) * STAGE;
+    // prefetch stage kt + 1 into the other buffer (released by the previous barrier)
+    if (kt + 1 < KT) issue(nxt, nxt + BM * 8, (kt + 1) * GEMM_BK);
+    mma_stage<BM, BN, TM, TN, FM, FN>(cur, cur + BM * 8, wm, wn, lane, acc);
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
   }
 
-  // epilogue: lane holds column (lane & 31) of rows 8*(r/4) + 4*(lane/32) + r%4
+  // Epilogue through LDS (the stage buffers are free after the last barrier):
+  // each wave parks one 32-row slice of its tile as fp32, then every lane
+  // handles 8 consecutive columns with 16-byte loads (bias, gate, residual) and
+  // a 16-byte store, so each 8 lanes write one contiguous 128-byte row run.
+  constexpr int EP_LD = TN + 4;                       // fp32 row pitch of the staging slice
+  static_assert(NW * 32 * EP_LD * 4 <= (int)sizeof(lds), "epilogue staging exceeds LDS");
+  float* stage = reinterpret_cast<float*>(lds) + wave * 32 * EP_LD;
+  const int col0 = n0 + wn * TN;
 #pragma unroll
-  for (int j = 0; j < FN; ++j) {
-    const int col = n0 + wn * TN + j * 32 + (lane & 31);
-    if (col >= N) continue;
-    const float bv = bf16_to_f32(bias[col]);
-    const float gv = (EPI == EPI_BIAS_GATED_RESIDUAL) ? gate[col] : 0.0f;
+  for (int i = 0; i < FM; ++i) {
 #pragma unroll
-    for (int i = 0; i < FM; ++i) {
-      const int rbase = m0 + wm * TM + i * 32 + 4 * (lane >> 5);
+    for (int j = 0; j < FN; ++j)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int row = rbase + 8 * (r >> 2) + (r & 3);
-        if (row < M) {
-          bf16_t* p = C + (int64_t)row * ldc + col;
-          const float resid = (EPI == EPI_BIAS_GATED_RESIDUAL) ? bf16_to_f32(*p) : 0.0f;
-          *p = f32_to_bf16(epi_value<EPI>(acc[i][j][r], bv, gv, resid));
+      for (int r = 0; r < 16; ++r)
+        stage[(8 * (r >> 2) + 4 * (lane >> 5) + (r & 3)) * EP_LD + j * 32 + (lane & 31)] =
+            acc[i][j][r];
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_s_waitcnt(0xc07f);                 // lgkmcnt(0): slice visible to the wave
+    __builtin_amdgcn_wave_barrier();
+    const int row0 = m0 + wm * TM + i * 32;
+#pragma unroll
+    for (int c = lane; c < 32 * TN / 8; c += 64) {
+      const int rl = c / (TN / 8), cl = (c % (TN / 8)) * 8;
+      const int row = row0 + rl, col = col0 + cl;
+      if (row < M && col < N) {
+        const float4 v0 = *reinterpret_cast<const float4*>(stage + rl * EP_LD + cl);
+        const float4 v1 = *reinterpret_cast<const float4*>(stage + rl * EP_LD + cl + 4);
+        const float v[8] = {v0.x, v0.y, v0.z, v0.w, v1.x, v1.y, v1.z, v1.w};
+        const uint4 bw = *reinterpret_cast<const uint4*>(bias + col);
+        const uint32_t bb[4] = {bw.x, bw.y, bw.z, bw.w};
+        bf16_t* p = C + (int64_t)row * ldc + col;
+        uint32_t rr[4] = {0u, 0u, 0u, 0u};
+        float gg[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+        if (EPI == EPI_BIAS_GATED_RESIDUAL) {
+          const uint4 rw = *reinterpret_cast<const uint4*>(p);
+          rr[0] = rw.x; rr[1] = rw.y; rr[2] = rw.z; rr[3] = rw.w;
+          const float4 g0 = *reinterpret_cast<const float4*>(gate + col);
+          const float4 g1 = *reinterpret_cast<const float4*>(gate + col + 4);
+          gg[0] = g0.x; gg[1] = g0.y; gg[2] = g0.z; gg[3] = g0.w;
+          gg[4] = g1.x; gg[5] = g1.y; gg[6] = g1.z; gg[7] = g1.w;
         }
+        uint32_t out[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const float b0 = __uint_as_float(bb[e] << 16), b1 = __uint_as_float(bb[e] & 0xFFFF0000u);
+          const float x0 = __uint_as_float(rr[e] << 16), x1 = __uint_as_float(rr[e] & 0xFFFF0000u);
+          out[e] = pack_bf16x2(epi_value<EPI>(v[2 * e], b0, gg[2 * e], x0),
+                               epi_value<EPI>(v[2 * e + 1], b1, gg[2 * e + 1], x1));
+        }
+        *reinterpret_cast<uint4*>(p) = make_uint4(out[0], out[1], out[2], out[3]);
       }
     }
+    __builtin_amdgcn_wave_barrier();
   }
 }
 
@@ -236,22 +257,16 @@ static hipError_t run_bf16(const void* A, int64_t lda, const void* B, int64_t ld
                            const void* bias, const float* gate, void* C, int64_t ldc, int M,
                            int N, int K, hipStream_t st) {
   const int tiles_m = (M + BM - 1) / BM, tiles_n = (N + BN - 1) / BN;
-  const size_t lds = (size_t)2 * (BM + BN) * 8 * sizeof(uint4);
   auto kern = gemm_bf16_nt<BM, BN, WM, WN, EPI>;
-  static bool attr_set = false;  // per instantiation
-  if (!attr_set) {
-    hipError_t e = hipFuncSetAttribute((const void*)kern,
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-    if (e != hipSuccess) return e;
-    attr_set = true;
-  }
-  hipLaunchKernelGGL(kern, dim3(tiles_m * tiles_n), dim3(WM * WN * 64), lds, st,
+  hipLaunchKernelGGL(kern, dim3(tiles_m * tiles_n), dim3(WM * WN * 64), 0, st,
                      (const bf16_t*)A, lda, (const bf16_t*)B, ldb, (const bf16_t*)bias, gate,
                      (bf16_t*)C, ldc, M, N, K, tiles_m, tiles_n);
   return hipGetLastError();
 }
 
-// Tile choice: fewest "rounds" of 256 CUs, weighted by per-tile efficiency.
+// Tile choice: time ~ rounds * (per-CU work of one round / efficiency), where a
+// round places `per_cu` workgroups on each of the 256 CUs (LDS-limited) and the
+// efficiencies are the measured per-tile MFMA rates of the three kernels.
 static int choose_tile(int64_t M, int64_t N) {
   static int forced = -2;
   if (forced == -2) {
@@ -259,15 +274,15 @@ static int choose_tile(int64_t M, int64_t N) {
     forced = e ? atoi(e) : -1;
   }
   if (forced >= 0 && forced <= 2) return forced;
-  struct Cand { int bm, bn; double eff; };
-  const Cand c[3] = {{256, 256, 1.0}, {256, 128, 0.85}, {128, 128, 0.7}};
+  struct Cand { int bm, bn, per_cu; double eff; };
+  const Cand c[3] = {{256, 256, 1, 1.0}, {256, 128, 1, 0.85}, {128, 128, 2, 0.75}};
   int best = 0;
   double best_t = 1e30;
   for (int i = 0; i < 3; ++i) {
-    if (N % c[i].bn) continue;
     const int64_t tiles = ((M + c[i].bm - 1) / c[i].bm) * ((N + c[i].bn - 1) / c[i].bn);
-    const int64_t rounds = (tiles + 255) / 256;
-    const double t = (double)rounds * c[i].bm * c[i].bn / c[i].eff;
+    const int64_t slots = 256ll * c[i].per_cu;
+    const int64_t rounds = (tiles + slots - 1) / slots;
+    const double t = (double)rounds * c[i].bm * c[i].bn * c[i].per_cu / c[i].eff;
     if (t < best_t) { best_t = t; best = i; }
   }
   return best;
@@ -278,8 +293,8 @@ static hipError_t dispatch_bf16(const void* A, int64_t lda, const void* B, int64
                                 const void* bias, const float* gate, void* C, int64_t ldc,
                                 int M, int N, int K, hipStream_t st) {
   switch (choose_tile(M, N)) {
-    case 0: return run_bf16<256, 256, 2, 2, EPI>(A, lda, B, ldb, bias, gate, C, ldc, M, N, K, st);
-    case 1: return run_bf16<256, 128, 2, 2, EPI>(A, lda, B, ldb, bias, gate, C, ldc, M, N, K, st);
+    case 0: return run_bf16<256, 256, 2, 4, EPI>(A, lda, B, ldb, bias, gate, C, ldc, M, N, K, st);
+    case 1: return run_bf16<256, 128, 4, 2, EPI>(A, lda, B, ldb, bias, gate, C, ldc, M, N, K, st);
     default: return run_bf16<128, 128, 2, 2, EPI>(A, lda, B, ldb, bias, gate, C, ldc, M, N, K, st);
   }
 }
