@@ -163,6 +163,50 @@ def block(x, w, temb, cu_seqlens, n_heads, dtype):
     return y, BlockTrace(qkv=qkv, lse=round_f32(lse), x_mid=x1)
 
 
+def block_rows(x, w, temb, cu_seqlens, rows, n_heads, dtype):
+    """The block output of selected rows only (same arithmetic as ``block``).
+
+    Keys and values need every row of the sampled rows' sequences; queries,
+    the attention output, the projections and the MLP are formed for the
+    sampled rows alone, so large workloads can be checked one row at a time.
+    Returns ([len(rows)][d] outputs, [len(rows)][N_h] normalisers).
+    """
+    st = storage_round(dtype)
+    x = np.asarray(x, np.float64)
+    d = x.shape[1]
+    hd = d // n_heads
+    rows = np.asarray(rows, np.int64)
+    sh1, sc1, g1, sh2, sc2, g2 = modulation(w["w_ada"], w["b_ada"], temb)
+    W = {k: np.asarray(v, np.float64) for k, v in w.items()}
+    cu = np.asarray(cu_seqlens, np.int64)
+    out = np.zeros((len(rows), d))
+    lam = np.zeros((len(rows), n_heads))
+    for b in range(len(cu) - 1):
+        s0, s1 = int(cu[b]), int(cu[b + 1])
+        sel = np.nonzero((rows >= s0) & (rows < s1))[0]
+        if len(sel) == 0:
+            continue
+        h = st(layer_norm(x[s0:s1]) * (1.0 + sc1) + sh1)
+        kv = st(h @ W["w_qkv"][d:].T + W["b_qkv"][d:])
+        k, v = kv[:, :d], kv[:, d:]
+        r = rows[sel]
+        q = st(h[r - s0] @ W["w_qkv"][:d].T + W["b_qkv"][:d])
+        o = np.zeros((len(r), d))
+        for hh in range(n_heads):
+            cols = slice(hh * hd, (hh + 1) * hd)
+            logits = q[:, cols] @ k[:, cols].T / math.sqrt(hd)
+            mx = logits.max(axis=1, keepdims=True)
+            lm = mx[:, 0] + np.log(np.exp(logits - mx).sum(axis=1))
+            o[:, cols] = np.exp(logits - lm[:, None]) @ v[:, cols]
+            lam[sel, hh] = lm
+        o = st(o)
+        x1 = st(x[r] + g1 * (o @ W["w_o"].T + W["b_o"]))
+        h2 = st(layer_norm(x1) * (1.0 + sc2) + sh2)
+        u = st(gelu_tanh(h2 @ W["w_1"].T + W["b_1"]))
+        out[sel] = st(x1 + g2 * (u @ W["w_2"].T + W["b_2"]))
+    return out, round_f32(lam)
+
+
 # ---------------------------------------------------------------------------
 # action-to-future scoring (Sec. 4.1 frame-aligned score; App. A.1, A.2)
 # ---------------------------------------------------------------------------

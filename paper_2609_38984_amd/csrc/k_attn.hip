@@ -93,9 +93,6 @@ attn_fwd_bf16(const bf16_t* __restrict__ qkv, bf16_t* __restrict__ out, float* _
 #pragma unroll
     for (int r = 0; r < 16; ++r) o[t][r] = 0.0f;
   float m_run = -1e30f, l_run = 0.0f;
-  bf16x2 ones2;
-  ones2[0] = (__bf16)1.0f;
-  ones2[1] = (__bf16)1.0f;
   const float sc = 1.4426950408889634f * 0.125f;      // log2(e) / sqrt(64)
 
   const int nkt = (s1 - s0 + ATT_BK - 1) / ATT_BK;
@@ -152,9 +149,10 @@ attn_fwd_bf16(const bf16_t* __restrict__ qkv, bf16_t* __restrict__ out, float* _
 #pragma unroll
         for (int r = 0; r < 16; ++r) o[t][r] *= corr;
     }
-    // p = exp2(s * sc - m); P^T packed to bf16 pairs; row sum from the same bf16 values
+    // p = exp2(s * sc - m); P^T packed to bf16 pairs for the PV MFMA; the row sum
+    // (and so lambda, which the scorer reuses) is accumulated from the fp32 values
     bf16x8 pf[2][2];
-    float psum = 0.0f;
+    float psum0 = 0.0f, psum1 = 0.0f;
 #pragma unroll
     for (int t = 0; t < 2; ++t)
 #pragma unroll
@@ -163,14 +161,13 @@ attn_fwd_bf16(const bf16_t* __restrict__ qkv, bf16_t* __restrict__ out, float* _
         for (int mm = 0; mm < 8; mm += 2) {
           const float p0 = __builtin_amdgcn_exp2f(fmaf(st[t][8 * u + mm], sc, -m_run));
           const float p1 = __builtin_amdgcn_exp2f(fmaf(st[t][8 * u + mm + 1], sc, -m_run));
-          bf16x2 pp;
-          pp[0] = (__bf16)p0;
-          pp[1] = (__bf16)p1;
-          pf[t][u][mm] = pp[0];
-          pf[t][u][mm + 1] = pp[1];
-          psum = __builtin_amdgcn_fdot2_f32_bf16(pp, ones2, psum, false);
+          psum0 += p0;
+          psum1 += p1;
+          pf[t][u][mm] = (__bf16)p0;
+          pf[t][u][mm + 1] = (__bf16)p1;
         }
       }
+    const float psum = psum0 + psum1;
     l_run += psum;
 
     // O^T += V^T P^T; k-substep (t, u) covers keys 32t + 16u + {4g..4g+3, 8+4g..8+4g+3}

@@ -493,3 +493,18 @@ def test_anchor_statistics_use_all_layers():
     np.testing.assert_allclose(red.Q, [0.5, 0.2], rtol=1e-7)
     np.testing.assert_allclose(red.V, S_all[0], rtol=1e-7)
     np.testing.assert_allclose(red.A, [0.25 / 0.7, 0.04 / 0.7, 0.0, 0.0], rtol=1e-6)
+
+
+@pytest.mark.parametrize("dtype", ["f64", "bf16"])
+def test_block_rows_equals_full_block(dtype):
+    """The row-sampled block gives exactly the rows of the full block."""
+    cfg = W.preset(1).replace(batch=2)
+    w = W.block_weights(cfg, 0)
+    x = W.make_inputs(cfg).x(2)
+    temb = W.timestep_embedding(cfg, 2)
+    cu = np.array([0, 100, cfg.batch * cfg.l_full])
+    y, tr = O.block(x, w, temb, cu, cfg.n_heads, dtype)
+    rows = np.array([0, 5, 99, 100, 101, 250, 303])
+    yr, lr = O.block_rows(x, w, temb, cu, rows, cfg.n_heads, dtype)
+    np.testing.assert_allclose(yr, y[rows], rtol=1e-12, atol=1e-12)
+    np.testing.assert_allclose(lr, tr.lse[rows], rtol=1e-6)
