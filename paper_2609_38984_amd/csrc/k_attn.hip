@@ -35,14 +35,25 @@ __device__ __forceinline__ bool find_tile(const int32_t* cu, int n_seqs, int n_r
   return false;
 }
 
-__global__ void __launch_bounds__(256)
+// WPE = minimum waves per SIMD the register allocation must allow: 4 caps the
+// kernel at 128 VGPRs (no spills), which pays when enough workgroups exist to
+// keep 4 waves on every SIMD; otherwise the unconstrained build (3) is used.
+template <int WPE>
+__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(WPE, 8)))
 attn_fwd_bf16(const bf16_t* __restrict__ qkv, bf16_t* __restrict__ out, float* __restrict__ lse,
               const int32_t* __restrict__ cu, int n_seqs, int n_heads, int n_rows) {
   __shared__ uint4 Ks[2][ATT_BK * 8];                 // [key][8 chunks], swizzled
   __shared__ uint32_t Vt[2][64 * VT_PITCH / 2];       // [hd][keys] bf16 pairs
+  // XCD-aware order: dispatch deals workgroup ids round-robin over the 8 XCDs;
+  // renumber so each XCD walks a contiguous run of (head, query tile) pairs and
+  // its L2 holds the K/V of one or two heads at a time.
+  const int nwg = gridDim.x, pid = blockIdx.x;
+  const int xcd = pid & 7, per = nwg >> 3, rem = nwg & 7;
+  const int id = xcd * per + min(xcd, rem) + (pid >> 3);
+  const int slots = nwg / n_heads;
+  const int h = id / slots;
   int s0, s1, q0;
-  if (!find_tile(cu, n_seqs, n_rows, blockIdx.x, ATT_BQ, s0, s1, q0)) return;
-  const int h = blockIdx.y;
+  if (!find_tile(cu, n_seqs, n_rows, id - h * slots, ATT_BQ, s0, s1, q0)) return;
   const int d = n_heads * 64;
   const int64_t ld = 3 * (int64_t)d;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -63,28 +74,30 @@ attn_fwd_bf16(const bf16_t* __restrict__ qkv, bf16_t* __restrict__ out, float* _
   const bf16_t* kbase = qkv + d + h * 64 + 8 * c;
   const bf16_t* vbase = qkv + 2 * d + h * 64 + 8 * c;
   uint4 rk0, rk1, rv0, rv1;
-#define SWAM_ATT_LOAD(kb_)                                                        \
+#define SWAM_ATT_LOAD(t_)                                                         \
   {                                                                               \
-    const int64_t k0_ = min((kb_) + 2 * kp, s1 - 1), k1_ = min((kb_) + 2 * kp + 1, s1 - 1); \
+    const int r0_ = s0 + (t_) * ATT_BK + 2 * kp;                                  \
+    const int64_t k0_ = min(r0_, s1 - 1), k1_ = min(r0_ + 1, s1 - 1);            \
     rk0 = *(const uint4*)(kbase + k0_ * ld);                                      \
     rk1 = *(const uint4*)(kbase + k1_ * ld);                                      \
     rv0 = *(const uint4*)(vbase + k0_ * ld);                                      \
     rv1 = *(const uint4*)(vbase + k1_ * ld);                                      \
   }
-  // K rows swizzled by 16-byte chunk; V transposed: Vt[8c + e][2kp .. 2kp+1]
+  // K rows swizzled by 16-byte chunk; V transposed: Vt[8c + e][2kp .. 2kp+1], the
+  // (key 2kp, key 2kp+1) pair of one head-dim column packed with one byte permute
 #define SWAM_ATT_STORE(buf_)                                                      \
   {                                                                               \
     Ks[buf_][(2 * kp) * 8 + (c ^ ((2 * kp) & 7))] = rk0;                          \
     Ks[buf_][(2 * kp + 1) * 8 + (c ^ ((2 * kp + 1) & 7))] = rk1;                  \
     uint32_t* vt_ = &Vt[buf_][(8 * c) * (VT_PITCH / 2) + kp];                      \
-    vt_[0 * (VT_PITCH / 2)] = (rv0.x & 0xFFFFu) | (rv1.x << 16);                  \
-    vt_[1 * (VT_PITCH / 2)] = (rv0.x >> 16) | (rv1.x & 0xFFFF0000u);              \
-    vt_[2 * (VT_PITCH / 2)] = (rv0.y & 0xFFFFu) | (rv1.y << 16);                  \
-    vt_[3 * (VT_PITCH / 2)] = (rv0.y >> 16) | (rv1.y & 0xFFFF0000u);              \
-    vt_[4 * (VT_PITCH / 2)] = (rv0.z & 0xFFFFu) | (rv1.z << 16);                  \
-    vt_[5 * (VT_PITCH / 2)] = (rv0.z >> 16) | (rv1.z & 0xFFFF0000u);              \
-    vt_[6 * (VT_PITCH / 2)] = (rv0.w & 0xFFFFu) | (rv1.w << 16);                  \
-    vt_[7 * (VT_PITCH / 2)] = (rv0.w >> 16) | (rv1.w & 0xFFFF0000u);              \
+    vt_[0 * (VT_PITCH / 2)] = __builtin_amdgcn_perm(rv1.x, rv0.x, 0x05040100u);   \
+    vt_[1 * (VT_PITCH / 2)] = __builtin_amdgcn_perm(rv1.x, rv0.x, 0x07060302u);   \
+    vt_[2 * (VT_PITCH / 2)] = __builtin_amdgcn_perm(rv1.y, rv0.y, 0x05040100u);   \
+    vt_[3 * (VT_PITCH / 2)] = __builtin_amdgcn_perm(rv1.y, rv0.y, 0x07060302u);   \
+    vt_[4 * (VT_PITCH / 2)] = __builtin_amdgcn_perm(rv1.z, rv0.z, 0x05040100u);   \
+    vt_[5 * (VT_PITCH / 2)] = __builtin_amdgcn_perm(rv1.z, rv0.z, 0x07060302u);   \
+    vt_[6 * (VT_PITCH / 2)] = __builtin_amdgcn_perm(rv1.w, rv0.w, 0x05040100u);   \
+    vt_[7 * (VT_PITCH / 2)] = __builtin_amdgcn_perm(rv1.w, rv0.w, 0x07060302u);   \
   }
 
   f32x16 o[2];
@@ -96,13 +109,13 @@ attn_fwd_bf16(const bf16_t* __restrict__ qkv, bf16_t* __restrict__ out, float* _
   const float sc = 1.4426950408889634f * 0.125f;      // log2(e) / sqrt(64)
 
   const int nkt = (s1 - s0 + ATT_BK - 1) / ATT_BK;
-  SWAM_ATT_LOAD(s0);
+  SWAM_ATT_LOAD(0);
   SWAM_ATT_STORE(0);
   __syncthreads();
   for (int kt = 0; kt < nkt; ++kt) {
     const int cur = kt & 1;
     const int kb = s0 + kt * ATT_BK;
-    SWAM_ATT_LOAD(kt + 1 < nkt ? kb + ATT_BK : kb);   // last iteration: harmless re-read
+    SWAM_ATT_LOAD(kt + 1 < nkt ? kt + 1 : kt);        // last iteration: harmless re-read
 
     // S^T tile: two 32-key halves
     f32x16 st[2];
@@ -247,9 +260,15 @@ hipError_t launch_attention(int dtype, const void* qkv, void* o, float* lse,
   if (n_rows <= 0) return hipSuccess;
   if (dtype == 1) {
     const int slots = (int)((n_rows + ATT_BQ - 1) / ATT_BQ) + n_seqs;
-    hipLaunchKernelGGL(attn_fwd_bf16, dim3(slots, n_heads), dim3(256), 0, st,
-                       (const bf16_t*)qkv, (bf16_t*)o, lse, cu_seqlens, n_seqs, n_heads,
-                       (int)n_rows);
+    const bool dense_grid = (int64_t)(slots - n_seqs) * n_heads >= 3 * 256;
+    if (dense_grid)
+      hipLaunchKernelGGL(attn_fwd_bf16<4>, dim3(slots * n_heads), dim3(256), 0, st,
+                         (const bf16_t*)qkv, (bf16_t*)o, lse, cu_seqlens, n_seqs, n_heads,
+                         (int)n_rows);
+    else
+      hipLaunchKernelGGL(attn_fwd_bf16<1>, dim3(slots * n_heads), dim3(256), 0, st,
+                         (const bf16_t*)qkv, (bf16_t*)o, lse, cu_seqlens, n_seqs, n_heads,
+                         (int)n_rows);
   } else {
     hipLaunchKernelGGL(attn_fwd_f32, dim3((unsigned)n_rows, n_heads), dim3(64), 0, st,
                        (const float*)qkv, (float*)o, lse, cu_seqlens, n_seqs, n_heads, n_rows);
