@@ -284,6 +284,47 @@ def measure(cfg, model, xs, tembs, steps, warmup, reps):
     }
 
 
+def measure_graph(cfg, model, xs, tembs, steps, reps):
+    """Schedule and per-kind step times through swam_step_graph (captured once,
+    replayed), on a dedicated stream."""
+    import torch
+    from paper_2609_38984_amd import swam
+    n_sched = len(xs)
+    stream = torch.cuda.Stream()
+    with torch.cuda.stream(stream):
+        y = torch.empty_like(xs[0])
+        ctx = swam.Context(cfg, stream=stream)
+
+        def run(tau, flags=0):
+            return ctx.step_graph(model, xs[tau % n_sched], tembs[tau % n_sched], tau, y, flags)
+
+        for t in range(max(n_sched, steps)):        # capture every (kind, input) pair once
+            run(t)
+        stream.synchronize()
+        t0 = time.perf_counter()
+        for t in range(steps):
+            run(t)
+        stream.synchronize()
+        elapsed = time.perf_counter() - t0
+
+        def median_ms(flags, tau):
+            ts = []
+            for _ in range(reps):
+                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                e0.record(stream)
+                run(tau, flags)
+                e1.record(stream)
+                stream.synchronize()
+                ts.append(e0.elapsed_time(e1))
+            return statistics.median(ts)
+
+        t_dense = median_ms(swam.FORCE_DENSE, 0)
+        run(0)
+        t_sparse = median_ms(0, 1) if cfg.reuse_R > 1 else float("nan")
+    return {"schedule_step_ms": elapsed * 1e3 / steps, "dense_step_ms": t_dense,
+            "sparse_step_ms": t_sparse}
+
+
 def inputs_for(cfg, blocks_np, dev, adt):
     import torch
     import workload as W
@@ -302,16 +343,18 @@ def sweep(args):
     rows = []
     head = ("| workload | retention | R | packed rows | dense ms | refresh ms | sparse ms | "
             "schedule ms/step | sparse/dense | schedule/dense | score+pack % of dense | "
-            "dominant kernel | MFMA frac |")
+            "dominant kernel | MFMA frac | graph dense ms | graph sparse ms | graph schedule ms/step |")
     print(head)
-    print("|" + "---|" * 13)
+    print("|" + "---|" * 16)
 
-    def emit(cfg, ret, m):
+    def emit(cfg, ret, m, model, xs, tembs):
+        g = measure_graph(cfg, model, xs, tembs, cfg.n_steps, args.reps)
         rf = m["roofline"]
         line = (f"| {cfg.name} | {ret} | {cfg.reuse_R} | {m['packed_rows']} | {m['dense_step_ms']:.2f} | "
                 f"{m['refresh_step_ms']:.2f} | {m['sparse_step_ms']:.2f} | {m['schedule_step_ms']:.2f} | "
                 f"{m['speedup_sparse_vs_dense']} | {m['speedup_schedule_vs_dense']} | "
-                f"{m['overhead_pct_of_dense']:.3f} | {rf['kernel']} | {rf['frac']:.3f} |")
+                f"{m['overhead_pct_of_dense']:.3f} | {rf['kernel']} | {rf['frac']:.3f} | "
+                f"{g['dense_step_ms']:.3f} | {g['sparse_step_ms']:.3f} | {g['schedule_step_ms']:.3f} |")
         print(line, flush=True)
 
     for n in (1, 2, 3):
@@ -320,7 +363,7 @@ def sweep(args):
         blocks_np, model = load_model(cfg, dev, adt)
         _, xs, tembs = inputs_for(cfg, blocks_np, dev, adt)
         emit(cfg, f"{cfg.k_core}+{cfg.k_anchor} of {cfg.n_s}",
-             measure(cfg, model, xs, tembs, cfg.n_steps, 2, args.reps))
+             measure(cfg, model, xs, tembs, cfg.n_steps, 2, args.reps), model, xs, tembs)
         del model, xs
         torch.cuda.empty_cache()
     base = W.preset(4, percent=25)
@@ -330,13 +373,14 @@ def sweep(args):
         for R in (1, 2, 4):
             cfg = W.preset(4, percent=pct, reuse_R=R)
             emit(cfg, f"{pct}% ({cfg.k_core}+{cfg.k_anchor})",
-                 measure(cfg, model, xs, tembs, cfg.n_steps, 2, args.reps))
+                 measure(cfg, model, xs, tembs, cfg.n_steps, 2, args.reps), model, xs, tembs)
     del model, xs
     torch.cuda.empty_cache()
     cfg = W.preset(5)
     blocks_np, model = load_model(cfg, dev, torch.bfloat16)
     _, xs, tembs = inputs_for(cfg, blocks_np, dev, torch.bfloat16)
-    emit(cfg, "mass 0.8", measure(cfg, model, xs, tembs, cfg.n_steps, 2, args.reps))
+    emit(cfg, "mass 0.8", measure(cfg, model, xs, tembs, cfg.n_steps, 2, args.reps), model, xs,
+         tembs)
 
 
 KERNEL_SOURCES = {"ATTN": ["k_attn.hip"], "GEMM_QKV": ["k_gemm.hip"], "GEMM_OUT": ["k_gemm.hip"],

@@ -267,6 +267,21 @@ int swam_step(swam_ctx* ctx, const swam_model* model, const void* x_full,
               const float* temb, int32_t tau, void* y_full, int32_t flags,
               int32_t* kind_out);
 
+/* As swam_step, but every distinct step -- same kind, x_full, y_full, temb,
+ * weight pointers and packed length -- is captured once into a HIP graph on
+ * the context stream and replayed afterwards, so the fixed-length step costs
+ * one launch on the host (the paper's engine gains most from graph capture of
+ * its fixed-length sparse step; Sec. 5 and App. B.4).  Needs a non-default
+ * stream (SWAM_E_STATE otherwise).  Mass-threshold refresh steps read their
+ * packed lengths back and run eagerly.  Graphs are cached (at most 64, oldest
+ * evicted); the buffers they reference must stay valid while cached.  Timers
+ * do not bracket captured work. */
+int swam_step_graph(swam_ctx* ctx, const swam_model* model, const void* x_full,
+                    const float* temb, int32_t tau, void* y_full, int32_t flags,
+                    int32_t* kind_out);
+/* Synchronise and free every cached graph of ctx. */
+int swam_graph_clear(swam_ctx* ctx);
+
 /* --------------------------------------------------------- timers */
 
 /* Kernel / phase classes for on-stream timing with HIP events. */

@@ -161,6 +161,18 @@ struct swam_ctx {
   int tcap = 0, tused = 0;
   std::vector<hipEvent_t> ev;   // 2 per slot
   std::vector<int> ev_cls;
+  // captured steps (swam_step_graph)
+  struct GraphEntry {
+    int kind;
+    const void* x;
+    const void* y;
+    const float* temb;
+    uint64_t wsig;
+    int64_t packed;
+    hipGraphExec_t exec;
+  };
+  std::vector<GraphEntry> graphs;
+  bool capturing = false;
 
   template <typename T> T* ptr(size_t off) { return (T*)(arena + off); }
 };
@@ -188,7 +200,7 @@ struct Timed {
   swam_ctx* c;
   int slot = -1;
   Timed(swam_ctx* ctx, int cls) : c(ctx) {
-    if (((c->tmask >> cls) & 1u) && c->tused < c->tcap) {
+    if (!c->capturing && ((c->tmask >> cls) & 1u) && c->tused < c->tcap) {
       slot = c->tused++;
       c->ev_cls[slot] = cls;
       hipEventRecord(c->ev[2 * slot], c->st);
@@ -459,6 +471,8 @@ int swam_create(const swam_config* cfg, void* stream, swam_ctx** out) {
 
 int swam_destroy(swam_ctx* c) {
   if (!c) return SWAM_OK;
+  if (c->st || c->arena) hipStreamSynchronize(c->st);
+  for (auto& g : c->graphs) hipGraphExecDestroy(g.exec);
   for (hipEvent_t ev : c->ev) hipEventDestroy(ev);
   if (c->arena) hipFree(c->arena);
   if (c->host_cu) hipHostFree(c->host_cu);
@@ -634,9 +648,12 @@ int swam_block(swam_ctx* c, const swam_block_weights* w, const float* temb, void
   return run_block(c, w, c->ptr<float>(c->lay.mod), x, n_rows, cu, n_seqs, lse_out, qkv, -1);
 }
 
-int swam_step(swam_ctx* c, const swam_model* model, const void* x_full, const float* temb,
-              int32_t tau, void* y_full, int32_t flags, int32_t* kind_out) {
-  if (!c) return set_err(nullptr, SWAM_E_INVALID, "ctx is NULL");
+}  // extern "C"
+
+namespace {
+
+int check_step(swam_ctx* c, const swam_model* model, const void* x_full, const float* temb,
+               int32_t tau, void* y_full, int32_t flags, int* kind) {
   const swam_config& cf = c->cfg;
   if (!model || !model->blocks || model->n_blocks != cf.n_blocks)
     return set_err(c, SWAM_E_INVALID, "model must have config.n_blocks blocks");
@@ -644,12 +661,18 @@ int swam_step(swam_ctx* c, const swam_model* model, const void* x_full, const fl
     if (any_null_block(&model->blocks[l])) return set_err(c, SWAM_E_INVALID, "NULL block weight");
   if (!x_full || !y_full || !temb) return set_err(c, SWAM_E_INVALID, "NULL tensor");
   if (tau < 0) return set_err(c, SWAM_E_INVALID, "tau < 0");
-  int kind;
-  if (flags & SWAM_STEP_FORCE_DENSE) kind = SWAM_KIND_DENSE;
-  else if ((flags & SWAM_STEP_FORCE_REFRESH) || tau % cf.reuse_R == 0) kind = SWAM_KIND_REFRESH;
-  else kind = SWAM_KIND_SPARSE;
-  if (kind == SWAM_KIND_SPARSE && !c->sel_valid)
+  if (flags & SWAM_STEP_FORCE_DENSE) *kind = SWAM_KIND_DENSE;
+  else if ((flags & SWAM_STEP_FORCE_REFRESH) || tau % cf.reuse_R == 0) *kind = SWAM_KIND_REFRESH;
+  else *kind = SWAM_KIND_SPARSE;
+  if (*kind == SWAM_KIND_SPARSE && !c->sel_valid)
     return set_err(c, SWAM_E_STATE, "sparse step before any selection (run a refresh first)");
+  return SWAM_OK;
+}
+
+// every launch of one step, in order, on the context stream
+int enqueue_step(swam_ctx* c, const swam_model* model, const void* x_full, const float* temb,
+                 int kind, void* y_full) {
+  const swam_config& cf = c->cfg;
   int rc = run_adaln(c, model->blocks, cf.n_blocks, temb);
   if (rc != SWAM_OK) return rc;
   const int64_t d = c->dv.d;
@@ -683,7 +706,105 @@ int swam_step(swam_ctx* c, const swam_model* model, const void* x_full, const fl
     }
     if ((rc = swam_unpack(c, xp, x_full, y_full)) != SWAM_OK) return rc;
   }
+  return SWAM_OK;
+}
+
+uint64_t weight_signature(const swam_model* m) {
+  uint64_t h = 1469598103934665603ull;   // FNV-1a over every weight pointer
+  for (int l = 0; l < m->n_blocks; ++l) {
+    const void* const* p = (const void* const*)&m->blocks[l];
+    for (size_t i = 0; i < sizeof(swam_block_weights) / sizeof(void*); ++i) {
+      uint64_t v = (uint64_t)(uintptr_t)p[i];
+      for (int k = 0; k < 8; ++k) {
+        h ^= (v >> (8 * k)) & 0xFF;
+        h *= 1099511628211ull;
+      }
+    }
+  }
+  return h;
+}
+
+constexpr size_t MAX_GRAPHS = 64;
+
+}  // namespace
+
+extern "C" {
+
+int swam_step(swam_ctx* c, const swam_model* model, const void* x_full, const float* temb,
+              int32_t tau, void* y_full, int32_t flags, int32_t* kind_out) {
+  if (!c) return set_err(nullptr, SWAM_E_INVALID, "ctx is NULL");
+  int kind;
+  int rc = check_step(c, model, x_full, temb, tau, y_full, flags, &kind);
+  if (rc != SWAM_OK) return rc;
+  if ((rc = enqueue_step(c, model, x_full, temb, kind, y_full)) != SWAM_OK) return rc;
   if (kind_out) *kind_out = kind;
+  return SWAM_OK;
+}
+
+int swam_step_graph(swam_ctx* c, const swam_model* model, const void* x_full,
+                    const float* temb, int32_t tau, void* y_full, int32_t flags,
+                    int32_t* kind_out) {
+  if (!c) return set_err(nullptr, SWAM_E_INVALID, "ctx is NULL");
+  int kind;
+  int rc = check_step(c, model, x_full, temb, tau, y_full, flags, &kind);
+  if (rc != SWAM_OK) return rc;
+  if (kind == SWAM_KIND_REFRESH && c->dv.mass_den > 0) {
+    // the ragged refresh reads its packed lengths back to the host: run it eagerly
+    if ((rc = enqueue_step(c, model, x_full, temb, kind, y_full)) != SWAM_OK) return rc;
+    if (kind_out) *kind_out = kind;
+    return SWAM_OK;
+  }
+  if (c->st == nullptr)
+    return set_err(c, SWAM_E_STATE, "graph capture needs a non-default stream");
+  const uint64_t wsig = weight_signature(model);
+  const int64_t packed = kind == SWAM_KIND_SPARSE ? c->packed_rows : -1;
+  hipGraphExec_t exec = nullptr;
+  for (auto& g : c->graphs)
+    if (g.kind == kind && g.x == x_full && g.y == y_full && g.temb == temb && g.wsig == wsig &&
+        g.packed == packed) {
+      exec = g.exec;
+      break;
+    }
+  if (!exec) {
+    c->capturing = true;
+    hipError_t e = hipStreamBeginCapture(c->st, hipStreamCaptureModeThreadLocal);
+    if (e != hipSuccess) {
+      c->capturing = false;
+      return hip_check(c, e, "begin capture");
+    }
+    rc = enqueue_step(c, model, x_full, temb, kind, y_full);
+    hipGraph_t graph = nullptr;
+    e = hipStreamEndCapture(c->st, &graph);
+    c->capturing = false;
+    if (rc != SWAM_OK) {
+      if (graph) hipGraphDestroy(graph);
+      return rc;
+    }
+    if (e != hipSuccess) return hip_check(c, e, "end capture");
+    e = hipGraphInstantiate(&exec, graph, nullptr, nullptr, 0);
+    hipGraphDestroy(graph);
+    if (e != hipSuccess) return hip_check(c, e, "graph instantiate");
+    if (c->graphs.size() >= MAX_GRAPHS) {
+      hipGraphExecDestroy(c->graphs.front().exec);
+      c->graphs.erase(c->graphs.begin());
+    }
+    c->graphs.push_back({kind, x_full, y_full, temb, wsig, packed, exec});
+  }
+  SWAM_HIP(c, hipGraphLaunch(exec, c->st), "graph launch");
+  if (kind == SWAM_KIND_REFRESH) {   // host-side effects of a replayed refresh
+    c->scores_valid = true;
+    c->sel_valid = true;
+    c->packed_rows = (int64_t)c->cfg.batch * c->dv.t_pack_fixed;
+  }
+  if (kind_out) *kind_out = kind;
+  return SWAM_OK;
+}
+
+int swam_graph_clear(swam_ctx* c) {
+  if (!c) return set_err(nullptr, SWAM_E_INVALID, "ctx is NULL");
+  SWAM_HIP(c, hipStreamSynchronize(c->st), "synchronise");
+  for (auto& g : c->graphs) hipGraphExecDestroy(g.exec);
+  c->graphs.clear();
   return SWAM_OK;
 }
 

@@ -27,7 +27,8 @@ T = {name: i for i, name in enumerate(TIMERS)}
 EXPORTS = ["swam_create", "swam_destroy", "swam_set_stream", "swam_plan", "swam_status_str",
            "swam_last_error", "swam_score", "swam_score_reduce", "swam_select",
            "swam_set_selection", "swam_packed_rows", "swam_export", "swam_pack", "swam_unpack",
-           "swam_block", "swam_step", "swam_timer_enable", "swam_timer_reset", "swam_timer_read"]
+           "swam_block", "swam_step", "swam_step_graph", "swam_graph_clear", "swam_timer_enable",
+           "swam_timer_reset", "swam_timer_read"]
 
 
 class SwamError(RuntimeError):
@@ -97,6 +98,8 @@ def load_library(path: str = LIB_PATH):
         "swam_pack": [P, P, P], "swam_unpack": [P, P, P, P],
         "swam_block": [P, C.POINTER(BlockWeights), P, P, I64, P, I32, P, P],
         "swam_step": [P, C.POINTER(ModelStruct), P, P, I32, P, I32, C.POINTER(I32)],
+        "swam_step_graph": [P, C.POINTER(ModelStruct), P, P, I32, P, I32, C.POINTER(I32)],
+        "swam_graph_clear": [P],
         "swam_timer_enable": [P, C.c_uint32, I32], "swam_timer_reset": [P],
         "swam_timer_read": [P, I32, C.POINTER(I64), C.POINTER(C.c_double)],
     }
@@ -291,6 +294,20 @@ class Context:
             _ptr(temb, torch.float32, c.d_temb, "temb"), int(tau),
             _ptr(y_full, self.act_dtype, n, "y_full"), int(flags), C.byref(kind)))
         return kind.value
+
+    def step_graph(self, model: Model, x_full, temb, tau: int, y_full, flags: int = 0) -> int:
+        """swam_step through cached HIP graphs (needs a non-default stream)."""
+        c = self.c_cfg
+        n = self.rows_full * c.d_model
+        kind = C.c_int32(-1)
+        self._ok(self.lib.swam_step_graph(
+            self.h, C.byref(model.struct), _ptr(x_full, self.act_dtype, n, "x_full"),
+            _ptr(temb, torch.float32, c.d_temb, "temb"), int(tau),
+            _ptr(y_full, self.act_dtype, n, "y_full"), int(flags), C.byref(kind)))
+        return kind.value
+
+    def graph_clear(self):
+        self._ok(self.lib.swam_graph_clear(self.h))
 
     # -- timers ------------------------------------------------------------------
     def timer_enable(self, classes, capacity=8192):
