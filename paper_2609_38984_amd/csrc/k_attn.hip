@@ -2,122 +2,109 @@
 // sequence, writing O and the natural-log normaliser lambda of every query
 // row and head (the normaliser the scorer reuses).
 //
-// bf16 path, one head per workgroup, 4 waves x 32 query rows:
+// bf16 path, one head per workgroup, 4 or 8 waves x 32 query rows:
 //   S^T = K Q^T with 32x32x16 MFMA: K (64-key tile, LDS) is the A operand and
 //   the wave's 32 query rows are the B operand held in registers, so the C
 //   layout gives each lane ONE query (lane & 31) and 16 of every 32 keys;
 //   the other 16 sit in lane ^ 32.  Row max / sum are in-lane plus one swap.
 //   O^T = V^T P^T: P^T straight from the S^T accumulators is the B operand
-//   (no shuffle); V is staged transposed in LDS so the A operand reads are
-//   8-byte row reads.  Online softmax in the log2 domain with the 1/8 scale
-//   folded into the exponent.  K/V tiles are double-buffered.
+//   (no shuffle); the V^T operand comes from transposed LDS reads of the
+//   row-major V tile.  K and V tiles are DMA'd global -> LDS (no register
+//   staging), double-buffered.  Online softmax in the log2 domain with the
+//   1/8 scale folded into one FMA, tail-only masking and lazy rescaling.
 // fp32 path: one wave per (query row, head), online softmax with shuffles.
 #include "common.h"
 
 namespace swam {
 
-constexpr int ATT_BQ = 128;     // query rows per workgroup
 constexpr int ATT_BK = 64;      // keys per tile
-constexpr int VT_PITCH = 68;    // V^T row pitch in bf16 (64 keys + 4 pad) = 136 bytes
 
+template <int BQ>
 __device__ __forceinline__ bool find_tile(const int32_t* cu, int n_seqs, int n_rows, int t,
-                                          int bq, int& s0, int& s1, int& q0) {
+                                          int& s0, int& s1, int& q0) {
   for (int b = 0; b < n_seqs; ++b) {
     const int e = min(max(cu[b + 1], 0), n_rows);
     const int a = min(max(cu[b], 0), e);
-    const int nt = (e - a + bq - 1) / bq;
-    if (t < nt) {
-      s0 = a; s1 = e; q0 = a + t * bq;
-      return true;
-    }
+    const int nt = (e - a + BQ - 1) / BQ;
+    if (t < nt) { s0 = a; s1 = e; q0 = a + t * BQ; return true; }
     t -= nt;
   }
   return false;
 }
 
-// WPE = minimum waves per SIMD the register allocation must allow: 4 caps the
-// kernel at 128 VGPRs (no spills), which pays when enough workgroups exist to
-// keep 4 waves on every SIMD; otherwise the unconstrained build (3) is used.
-template <int WPE>
-__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(WPE, 8)))
+typedef __attribute__((address_space(3))) void lds_void_t;
+typedef __attribute__((address_space(1))) void glb_void_t;
+typedef short v4i16 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) v4i16 lds_v4i16;
+
+// NW waves x 32 query rows per workgroup; WPE = minimum waves per SIMD the
+// register allocation must allow (4 caps it at 128 VGPRs without spills).
+template <int NW, int WPE>
+__global__ void __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(WPE, 8)))
 attn_fwd_bf16(const bf16_t* __restrict__ qkv, bf16_t* __restrict__ out, float* __restrict__ lse,
-              const int32_t* __restrict__ cu, int n_seqs, int n_heads, int n_rows) {
-  __shared__ uint4 Ks[2][ATT_BK * 8];                 // [key][8 chunks], swizzled
-  __shared__ uint32_t Vt[2][64 * VT_PITCH / 2];       // [hd][keys] bf16 pairs
-  // XCD-aware order: dispatch deals workgroup ids round-robin over the 8 XCDs;
-  // renumber so each XCD walks a contiguous run of (head, query tile) pairs and
-  // its L2 holds the K/V of one or two heads at a time.
+     const int32_t* __restrict__ cu, int n_seqs, int n_heads, int n_rows) {
+  constexpr int S = 2;                           // LDS stages (K and V tiles)
+  __shared__ uint4 Ks[S][ATT_BK * 8];             // [key][8 chunks], chunk ^ (key & 7)
+  __shared__ uint4 Vs[S][ATT_BK * 8];
   const int nwg = gridDim.x, pid = blockIdx.x;
   const int xcd = pid & 7, per = nwg >> 3, rem = nwg & 7;
   const int id = xcd * per + min(xcd, rem) + (pid >> 3);
   const int slots = nwg / n_heads;
   const int h = id / slots;
   int s0, s1, q0;
-  if (!find_tile(cu, n_seqs, n_rows, id - h * slots, ATT_BQ, s0, s1, q0)) return;
+  constexpr int BQ = 32 * NW;
+  if (!find_tile<BQ>(cu, n_seqs, n_rows, id - h * slots, s0, s1, q0)) return;
   const int d = n_heads * 64;
   const int64_t ld = 3 * (int64_t)d;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int g = lane >> 5;                            // half-wave
+  const int g = lane >> 5;
   const int qrow = q0 + wave * 32 + (lane & 31);
   const bool qvalid = qrow < s1;
-
-  // Q^T B-operand fragments: query (lane & 31), hd chunk 2s + g
   bf16x8 qf[4];
   {
     const bf16_t* qp = qkv + (int64_t)min(qrow, s1 - 1) * ld + h * 64;
 #pragma unroll
     for (int s = 0; s < 4; ++s) qf[s] = __builtin_bit_cast(bf16x8, *(const uint4*)(qp + 8 * (2 * s + g)));
   }
-
-  // K / V staging: thread -> (chunk c, key pair kp)
-  const int c = tid & 7, kp = tid >> 3;               // kp 0..31
-  const bf16_t* kbase = qkv + d + h * 64 + 8 * c;
-  const bf16_t* vbase = qkv + 2 * d + h * 64 + 8 * c;
-  uint4 rk0, rk1, rv0, rv1;
-#define SWAM_ATT_LOAD(t_)                                                         \
-  {                                                                               \
-    const int r0_ = s0 + (t_) * ATT_BK + 2 * kp;                                  \
-    const int64_t k0_ = min(r0_, s1 - 1), k1_ = min(r0_ + 1, s1 - 1);            \
-    rk0 = *(const uint4*)(kbase + k0_ * ld);                                      \
-    rk1 = *(const uint4*)(kbase + k1_ * ld);                                      \
-    rv0 = *(const uint4*)(vbase + k0_ * ld);                                      \
-    rv1 = *(const uint4*)(vbase + k1_ * ld);                                      \
-  }
-  // K rows swizzled by 16-byte chunk; V transposed: Vt[8c + e][2kp .. 2kp+1], the
-  // (key 2kp, key 2kp+1) pair of one head-dim column packed with one byte permute
-#define SWAM_ATT_STORE(buf_)                                                      \
-  {                                                                               \
-    Ks[buf_][(2 * kp) * 8 + (c ^ ((2 * kp) & 7))] = rk0;                          \
-    Ks[buf_][(2 * kp + 1) * 8 + (c ^ ((2 * kp + 1) & 7))] = rk1;                  \
-    uint32_t* vt_ = &Vt[buf_][(8 * c) * (VT_PITCH / 2) + kp];                      \
-    vt_[0 * (VT_PITCH / 2)] = __builtin_amdgcn_perm(rv1.x, rv0.x, 0x05040100u);   \
-    vt_[1 * (VT_PITCH / 2)] = __builtin_amdgcn_perm(rv1.x, rv0.x, 0x07060302u);   \
-    vt_[2 * (VT_PITCH / 2)] = __builtin_amdgcn_perm(rv1.y, rv0.y, 0x05040100u);   \
-    vt_[3 * (VT_PITCH / 2)] = __builtin_amdgcn_perm(rv1.y, rv0.y, 0x07060302u);   \
-    vt_[4 * (VT_PITCH / 2)] = __builtin_amdgcn_perm(rv1.z, rv0.z, 0x05040100u);   \
-    vt_[5 * (VT_PITCH / 2)] = __builtin_amdgcn_perm(rv1.z, rv0.z, 0x07060302u);   \
-    vt_[6 * (VT_PITCH / 2)] = __builtin_amdgcn_perm(rv1.w, rv0.w, 0x05040100u);   \
-    vt_[7 * (VT_PITCH / 2)] = __builtin_amdgcn_perm(rv1.w, rv0.w, 0x07060302u);   \
-  }
-
+  // K and V tiles go global -> LDS directly, row-major with the chunk swizzle
+  // applied on the global side: each instruction moves an 8-row slab (1 KB),
+  // lane i landing in row i >> 3, physical chunk i & 7.
+  const int lrow = lane >> 3, lchunk = (lane & 7) ^ lrow;
+  const bf16_t* kbase = qkv + d + h * 64 + 8 * lchunk;
+  const bf16_t* vbase = qkv + 2 * d + h * 64 + 8 * lchunk;
+  auto issue = [&](int buf, int kb) {
+#pragma unroll
+    for (int j = 0; j < 8 / NW; ++j) {
+      const int r0 = (64 / NW) * wave + 8 * j;
+      const int64_t key = min(kb + r0 + lrow, s1 - 1);
+      __builtin_amdgcn_global_load_lds((glb_void_t*)(kbase + key * ld), (lds_void_t*)(&Ks[buf][r0 * 8]), 16, 0, 0);
+      __builtin_amdgcn_global_load_lds((glb_void_t*)(vbase + key * ld), (lds_void_t*)(&Vs[buf][r0 * 8]), 16, 0, 0);
+    }
+  };
+  // PV operand (V^T fragment) from transposed LDS reads: within each 16-lane
+  // group, lane a addresses V[key0 + (a >> 2)][hd0 + 4 (a & 3)] and lane i
+  // receives V[key0 .. key0+3][hd0 + i], i.e. four consecutive keys of one
+  // head-dim column (the k order the P^T accumulators provide).
+  const int a16 = lane & 15, G = lane >> 4;
   f32x16 o[2];
 #pragma unroll
   for (int t = 0; t < 2; ++t)
 #pragma unroll
     for (int r = 0; r < 16; ++r) o[t][r] = 0.0f;
   float m_run = -1e30f, l_run = 0.0f;
-  const float sc = 1.4426950408889634f * 0.125f;      // log2(e) / sqrt(64)
-
+  const float sc = 1.4426950408889634f * 0.125f;
   const int nkt = (s1 - s0 + ATT_BK - 1) / ATT_BK;
-  SWAM_ATT_LOAD(0);
-  SWAM_ATT_STORE(0);
-  __syncthreads();
+#pragma unroll
+  for (int p = 0; p < S - 1; ++p)
+    if (p < nkt) issue(p, s0 + p * ATT_BK);
   for (int kt = 0; kt < nkt; ++kt) {
-    const int cur = kt & 1;
+    const int cur = kt % S;
     const int kb = s0 + kt * ATT_BK;
-    SWAM_ATT_LOAD(kt + 1 < nkt ? kt + 1 : kt);        // last iteration: harmless re-read
-
-    // S^T tile: two 32-key halves
+    // tile kt has landed (own DMA done, then everyone's via the barrier); the
+    // barrier also releases the stage the next prefetch overwrites
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();
+    if (kt + S - 1 < nkt) issue((kt + S - 1) % S, kb + (S - 1) * ATT_BK);
     f32x16 st[2];
 #pragma unroll
     for (int t = 0; t < 2; ++t) {
@@ -131,7 +118,6 @@ attn_fwd_bf16(const bf16_t* __restrict__ qkv, bf16_t* __restrict__ out, float* _
         st[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[s], st[t], 0, 0, 0);
       }
     }
-    // keys beyond the sequence exist only in the last tile (wave-uniform branch)
     const int nvalid = s1 - kb;
     if (nvalid < ATT_BK) {
 #pragma unroll
@@ -142,15 +128,12 @@ attn_fwd_bf16(const bf16_t* __restrict__ qkv, bf16_t* __restrict__ out, float* _
           if (key >= nvalid) st[t][r] = -INFINITY;
         }
     }
-    // row max of the raw logits: 16 keys in-lane per half tile, the rest in lane ^ 32
     float mx = st[0][0];
 #pragma unroll
     for (int t = 0; t < 2; ++t)
 #pragma unroll
       for (int r = 0; r < 16; ++r) mx = fmaxf(mx, st[t][r]);
     mx = fmaxf(mx, __shfl_xor(mx, 32));
-    // lazy rescaling: the running max (log2 units) is only raised when some row of
-    // the wave grew by more than 2^8; otherwise p <= 256 against the stale max
     const float m_tile = mx * sc;
     if (__any(m_tile > m_run + 8.0f)) {
       const float m_new = fmaxf(m_run, m_tile);
@@ -162,48 +145,40 @@ attn_fwd_bf16(const bf16_t* __restrict__ qkv, bf16_t* __restrict__ out, float* _
 #pragma unroll
         for (int r = 0; r < 16; ++r) o[t][r] *= corr;
     }
-    // p = exp2(s * sc - m); P^T packed to bf16 pairs for the PV MFMA; the row sum
-    // (and so lambda, which the scorer reuses) is accumulated from the fp32 values
     bf16x8 pf[2][2];
     float psum0 = 0.0f, psum1 = 0.0f;
 #pragma unroll
     for (int t = 0; t < 2; ++t)
 #pragma unroll
-      for (int u = 0; u < 2; ++u) {
+      for (int u = 0; u < 2; ++u)
 #pragma unroll
         for (int mm = 0; mm < 8; mm += 2) {
           const float p0 = __builtin_amdgcn_exp2f(fmaf(st[t][8 * u + mm], sc, -m_run));
           const float p1 = __builtin_amdgcn_exp2f(fmaf(st[t][8 * u + mm + 1], sc, -m_run));
-          psum0 += p0;
-          psum1 += p1;
-          pf[t][u][mm] = (__bf16)p0;
-          pf[t][u][mm + 1] = (__bf16)p1;
+          psum0 += p0; psum1 += p1;
+          pf[t][u][mm] = (__bf16)p0; pf[t][u][mm + 1] = (__bf16)p1;
         }
-      }
-    const float psum = psum0 + psum1;
-    l_run += psum;
-
-    // O^T += V^T P^T; k-substep (t, u) covers keys 32t + 16u + {4g..4g+3, 8+4g..8+4g+3}
+    l_run += psum0 + psum1;
+    const unsigned short* vs = reinterpret_cast<const unsigned short*>(&Vs[cur][0]);
 #pragma unroll
     for (int ht = 0; ht < 2; ++ht) {
-      const int hd = 32 * ht + (lane & 31);
-      const uint32_t* vrow = &Vt[cur][hd * (VT_PITCH / 2)];
+      const int hd = 32 * ht + 16 * (G & 1) + 4 * (a16 & 3);
 #pragma unroll
       for (int t = 0; t < 2; ++t)
 #pragma unroll
         for (int u = 0; u < 2; ++u) {
-          const int kb0 = 32 * t + 16 * u + 4 * g;          // keys kb0..kb0+3 and kb0+8..+11
-          uint2 lo = *(const uint2*)(vrow + kb0 / 2);
-          uint2 hi = *(const uint2*)(vrow + (kb0 + 8) / 2);
-          uint4 w = make_uint4(lo.x, lo.y, hi.x, hi.y);
-          bf16x8 vf = __builtin_bit_cast(bf16x8, w);
+          const int r1 = 32 * t + 16 * u + 4 * g + (a16 >> 2);
+          const int r2 = r1 + 8;
+          const int e1 = r1 * 64 + 8 * ((hd >> 3) ^ (r1 & 7)) + (hd & 7);
+          const int e2 = r2 * 64 + 8 * ((hd >> 3) ^ (r2 & 7)) + (hd & 7);
+          const v4i16 x1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)(vs + e1));
+          const v4i16 x2 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)(vs + e2));
+          const uint2 w1 = __builtin_bit_cast(uint2, x1), w2 = __builtin_bit_cast(uint2, x2);
+          const bf16x8 vf = __builtin_bit_cast(bf16x8, make_uint4(w1.x, w1.y, w2.x, w2.y));
           o[ht] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[t][u], o[ht], 0, 0, 0);
         }
     }
-    SWAM_ATT_STORE(cur ^ 1);                   // other stage released by the last barrier
-    __syncthreads();
   }
-
   const float l_tot = l_run + __shfl_xor(l_run, 32);
   if (!qvalid) return;
   const float inv = 1.0f / l_tot;
@@ -220,8 +195,6 @@ attn_fwd_bf16(const bf16_t* __restrict__ qkv, bf16_t* __restrict__ out, float* _
     }
   if (lse != nullptr && g == 0)
     lse[(int64_t)qrow * n_heads + h] = (m_run + log2f(l_tot)) * 0.6931471805599453f;
-#undef SWAM_ATT_LOAD
-#undef SWAM_ATT_STORE
 }
 
 // fp32: one wave per (query row, head); lane = head-dim element.
@@ -259,14 +232,21 @@ hipError_t launch_attention(int dtype, const void* qkv, void* o, float* lse,
                             int n_heads, hipStream_t st) {
   if (n_rows <= 0) return hipSuccess;
   if (dtype == 1) {
-    const int slots = (int)((n_rows + ATT_BQ - 1) / ATT_BQ) + n_seqs;
-    const bool dense_grid = (int64_t)(slots - n_seqs) * n_heads >= 3 * 256;
-    if (dense_grid)
-      hipLaunchKernelGGL(attn_fwd_bf16<4>, dim3(slots * n_heads), dim3(256), 0, st,
+    // 8 waves (256 query rows) share each K/V tile when the grid still gives
+    // every CU two such workgroups; otherwise 4 waves, with the 4-waves/SIMD
+    // register cap only when enough workgroups exist to use it.
+    const int slots8 = (int)((n_rows + 255) / 256) + n_seqs;
+    const int slots4 = (int)((n_rows + 127) / 128) + n_seqs;
+    if ((int64_t)(slots8 - n_seqs) * n_heads >= 2 * 256)
+      hipLaunchKernelGGL((attn_fwd_bf16<8, 4>), dim3(slots8 * n_heads), dim3(512), 0, st,
+                         (const bf16_t*)qkv, (bf16_t*)o, lse, cu_seqlens, n_seqs, n_heads,
+                         (int)n_rows);
+    else if ((int64_t)(slots4 - n_seqs) * n_heads >= 3 * 256)
+      hipLaunchKernelGGL((attn_fwd_bf16<4, 4>), dim3(slots4 * n_heads), dim3(256), 0, st,
                          (const bf16_t*)qkv, (bf16_t*)o, lse, cu_seqlens, n_seqs, n_heads,
                          (int)n_rows);
     else
-      hipLaunchKernelGGL(attn_fwd_bf16<1>, dim3(slots * n_heads), dim3(256), 0, st,
+      hipLaunchKernelGGL((attn_fwd_bf16<4, 1>), dim3(slots4 * n_heads), dim3(256), 0, st,
                          (const bf16_t*)qkv, (bf16_t*)o, lse, cu_seqlens, n_seqs, n_heads,
                          (int)n_rows);
   } else {
