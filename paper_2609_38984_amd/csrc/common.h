@@ -95,6 +95,8 @@ struct ScoreArgs {
   int64_t s_seq;
   const float* alpha;         // [g] device
   int B, F, n_s, H, n_heads;
+  int n_layers;               // layers scored by one launch (>= 1)
+  int64_t q_lay, k_lay, lse_lay, s_lay;   // element strides between layers
 };
 hipError_t launch_score(int dtype, const ScoreArgs& a, hipStream_t st);
 hipError_t launch_lse_all(int dtype, const void* q, int64_t q_seq, int64_t q_row,

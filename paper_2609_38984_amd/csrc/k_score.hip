@@ -5,6 +5,9 @@
 // against a stream of keys), so it is bound by the single read of the future
 // keys; MFMA only keeps the dot products off the VALU.
 //
+// One launch may score several layers (the refresh step scores all of them
+// after its last block, from per-layer q/k/lambda kept resident in HBM).
+//
 // bf16: workgroup = 4 waves on 16 keys of one frame.  Each wave takes every
 // 4th head: two 16x16x32 MFMAs per head with the keys as the A operand
 // (lane -> key lane&15, 8 hd at 8*(lane>>4)) and the group's queries as the
@@ -27,12 +30,21 @@ __global__ void __launch_bounds__(256)
 score_bf16(const bf16_t* __restrict__ q, int64_t q_seq, int64_t q_row,
            const bf16_t* __restrict__ k, int64_t k_seq, int64_t k_row,
            const float* __restrict__ lse, int64_t lse_seq, float* __restrict__ s_out,
-           int64_t s_seq, const float* __restrict__ alpha, int F, int n_s, int H, int n_heads) {
+           int64_t s_seq, const float* __restrict__ alpha, int B, int F, int n_s, int H,
+           int n_heads, int64_t q_lay, int64_t k_lay, int64_t lse_lay, int64_t s_lay) {
   __shared__ float part[4][16];
   const int ktiles = (n_s + 15) >> 4;
-  const int kt = blockIdx.x % ktiles;
-  const int f = (blockIdx.x / ktiles) % F;
-  const int b = blockIdx.x / (ktiles * F);
+  int bid = blockIdx.x;
+  const int kt = bid % ktiles;
+  bid /= ktiles;
+  const int f = bid % F;
+  bid /= F;
+  const int b = bid % B;
+  const int layer = bid / B;
+  q += layer * q_lay;
+  k += layer * k_lay;
+  lse += layer * lse_lay;
+  s_out += layer * s_lay;
   const int g = H / F;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int j0 = kt * 16;
@@ -88,10 +100,16 @@ score_f32(const float* __restrict__ q, int64_t q_seq, int64_t q_row,
           const float* __restrict__ k, int64_t k_seq, int64_t k_row,
           const float* __restrict__ lse, int64_t lse_seq, float* __restrict__ s_out,
           int64_t s_seq, const float* __restrict__ alpha, int B, int F, int n_s, int H,
-          int n_heads) {
+          int n_heads, int n_layers, int64_t q_lay, int64_t k_lay, int64_t lse_lay,
+          int64_t s_lay) {
   const int64_t id = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (id >= (int64_t)B * F * n_s) return;
-  const int j = id % n_s, f = (id / n_s) % F, b = id / ((int64_t)n_s * F);
+  if (id >= (int64_t)n_layers * B * F * n_s) return;
+  const int j = id % n_s, f = (id / n_s) % F, b = (id / ((int64_t)n_s * F)) % B;
+  const int layer = (int)(id / ((int64_t)n_s * F * B));
+  q += layer * q_lay;
+  k += layer * k_lay;
+  lse += layer * lse_lay;
+  s_out += layer * s_lay;
   const int g = H / F;
   const float* kr = k + b * k_seq + (int64_t)(f * n_s + j) * k_row;
   float s = 0.0f;
@@ -168,18 +186,19 @@ __global__ void lse_combine(const float* __restrict__ part, int chunks, int B, i
 }
 
 hipError_t launch_score(int dtype, const ScoreArgs& a, hipStream_t st) {
+  const int nl = a.n_layers < 1 ? 1 : a.n_layers;
   if (dtype == 1) {
     const int ktiles = (a.n_s + 15) / 16;
-    hipLaunchKernelGGL(score_bf16, dim3(a.B * a.F * ktiles), dim3(256), 0, st,
+    hipLaunchKernelGGL(score_bf16, dim3(nl * a.B * a.F * ktiles), dim3(256), 0, st,
                        (const bf16_t*)a.q, a.q_seq, a.q_row, (const bf16_t*)a.k, a.k_seq,
-                       a.k_row, a.lse, a.lse_seq, a.s_out, a.s_seq, a.alpha, a.F, a.n_s, a.H,
-                       a.n_heads);
+                       a.k_row, a.lse, a.lse_seq, a.s_out, a.s_seq, a.alpha, a.B, a.F, a.n_s,
+                       a.H, a.n_heads, a.q_lay, a.k_lay, a.lse_lay, a.s_lay);
   } else {
-    const int64_t n = (int64_t)a.B * a.F * a.n_s;
+    const int64_t n = (int64_t)nl * a.B * a.F * a.n_s;
     hipLaunchKernelGGL(score_f32, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st,
                        (const float*)a.q, a.q_seq, a.q_row, (const float*)a.k, a.k_seq,
                        a.k_row, a.lse, a.lse_seq, a.s_out, a.s_seq, a.alpha, a.B, a.F, a.n_s,
-                       a.H, a.n_heads);
+                       a.H, a.n_heads, nl, a.q_lay, a.k_lay, a.lse_lay, a.s_lay);
   }
   return hipGetLastError();
 }

@@ -112,12 +112,14 @@ Layout layout_for(const swam_config* c, const Derived& dv) {
   };
   const int64_t R = dv.rows_full, B = c->batch, F = c->n_frames, Lb = c->n_blocks;
   const int64_t chunks = (dv.l_full + 255) / 256;
-  L.qkv = take(R * 3 * dv.d * dv.esz);
+  // one QKV / lambda slot per block: a refresh keeps every layer's projections
+  // resident and scores all layers in one launch after the last block
+  L.qkv = take(Lb * R * 3 * dv.d * dv.esz);
   L.h = take(R * dv.d * dv.esz);
   L.o = take(R * dv.d * dv.esz);
   L.u = take(R * dv.hidden * dv.esz);
   L.xp = take(R * dv.d * dv.esz);
-  L.lse = take(R * c->n_heads * 4);
+  L.lse = take(Lb * R * c->n_heads * 4);
   L.mod = take(Lb * 6 * dv.d * 4);
   L.alpha = take(16 * 4);
   L.lse_act = take(B * c->n_act * c->n_heads * 4);
@@ -218,8 +220,7 @@ bool any_null_block(const swam_block_weights* w) {
 
 // one block in place on x [n_rows][d]; mod = this block's [6][d] modulation
 int run_block(swam_ctx* c, const swam_block_weights* w, const float* mod, void* x,
-              int64_t n_rows, const int32_t* cu, int n_seqs, float* lse_out, void* qkv,
-              int layer_for_score /* -1: no scoring */) {
+              int64_t n_rows, const int32_t* cu, int n_seqs, float* lse_out, void* qkv) {
   const int dt = c->cfg.dtype;
   const int64_t d = c->dv.d, hid = c->dv.hidden;
   void* h = c->ptr<char>(c->lay.h);
@@ -242,31 +243,6 @@ int run_block(swam_ctx* c, const swam_block_weights* w, const float* mod, void* 
     Timed t(c, SWAM_T_ATTN);
     SWAM_HIP(c, launch_attention(dt, qkv, o, lse_out, cu, n_seqs, n_rows, c->cfg.n_heads, st),
              "attention");
-  }
-  if (layer_for_score >= 0) {
-    // scores of this layer from the dense forward's q, k and normalisers
-    Timed t(c, SWAM_T_SCORE);
-    const swam_config& cf = c->cfg;
-    const int64_t ld = 3 * d, es = c->dv.esz;
-    ScoreArgs a{};
-    const int64_t act0 = cf.n_ctx + (int64_t)cf.n_frames * c->dv.n_s;
-    a.q = (const char*)qkv + act0 * ld * es;
-    a.q_seq = c->dv.l_full * ld;
-    a.q_row = ld;
-    a.k = (const char*)qkv + (cf.n_ctx * ld + d) * es;
-    a.k_seq = c->dv.l_full * ld;
-    a.k_row = ld;
-    a.lse = lse_out + act0 * cf.n_heads;
-    a.lse_seq = c->dv.l_full * cf.n_heads;
-    a.s_out = c->ptr<float>(c->lay.s_all) + (int64_t)layer_for_score * cf.n_frames * c->dv.n_s;
-    a.s_seq = (int64_t)cf.n_blocks * cf.n_frames * c->dv.n_s;
-    a.alpha = c->ptr<float>(c->lay.alpha);
-    a.B = cf.batch;
-    a.F = cf.n_frames;
-    a.n_s = (int)c->dv.n_s;
-    a.H = cf.n_act;
-    a.n_heads = cf.n_heads;
-    SWAM_HIP(c, launch_score(dt, a, st), "score");
   }
   {
     Timed t(c, SWAM_T_GEMM_OUT);
@@ -516,6 +492,7 @@ int swam_score(swam_ctx* c, const void* q_act, int64_t q_seq_stride, int64_t q_r
   a.alpha = c->ptr<float>(c->lay.alpha);
   a.B = cf.batch; a.F = cf.n_frames; a.n_s = (int)c->dv.n_s; a.H = cf.n_act;
   a.n_heads = cf.n_heads;
+  a.n_layers = 1;
   Timed t(c, SWAM_T_SCORE);
   SWAM_HIP(c, launch_score(cf.dtype, a, c->st), "score");
   return SWAM_OK;
@@ -645,7 +622,7 @@ int swam_block(swam_ctx* c, const swam_block_weights* w, const float* temb, void
   int rc = run_adaln(c, w, 1, temb);
   if (rc != SWAM_OK) return rc;
   void* qkv = qkv_out ? qkv_out : c->ptr<char>(c->lay.qkv);
-  return run_block(c, w, c->ptr<float>(c->lay.mod), x, n_rows, cu, n_seqs, lse_out, qkv, -1);
+  return run_block(c, w, c->ptr<float>(c->lay.mod), x, n_rows, cu, n_seqs, lse_out, qkv);
 }
 
 }  // extern "C"
@@ -684,11 +661,43 @@ int enqueue_step(swam_ctx* c, const swam_model* model, const void* x_full, const
       SWAM_HIP(c, launch_copy(x_full, y_full, c->dv.rows_full * d * c->dv.esz, c->st), "copy");
     }
     const bool score = kind == SWAM_KIND_REFRESH;
+    const int64_t qkv_slot = c->dv.rows_full * 3 * d * c->dv.esz;      // bytes per layer
+    const int64_t lse_slot = c->dv.rows_full * cf.n_heads;             // floats per layer
     for (int l = 0; l < cf.n_blocks; ++l) {
       rc = run_block(c, &model->blocks[l], mod + (int64_t)l * 6 * d, y_full, c->dv.rows_full,
                      c->ptr<int32_t>(c->lay.cu_dense), cf.batch,
-                     score ? c->ptr<float>(c->lay.lse) : nullptr, qkv, score ? l : -1);
+                     score ? c->ptr<float>(c->lay.lse) + l * lse_slot : nullptr,
+                     score ? (void*)((char*)qkv + l * qkv_slot) : qkv);
       if (rc != SWAM_OK) return rc;
+    }
+    if (score) {
+      // every layer's action-to-future scores from its stored q, k and lambda
+      Timed t(c, SWAM_T_SCORE);
+      const int64_t ld = 3 * d, es = c->dv.esz;
+      const int64_t act0 = cf.n_ctx + (int64_t)cf.n_frames * c->dv.n_s;
+      ScoreArgs a{};
+      a.q = (const char*)qkv + act0 * ld * es;
+      a.q_seq = c->dv.l_full * ld;
+      a.q_row = ld;
+      a.k = (const char*)qkv + (cf.n_ctx * ld + d) * es;
+      a.k_seq = c->dv.l_full * ld;
+      a.k_row = ld;
+      a.lse = c->ptr<float>(c->lay.lse) + act0 * cf.n_heads;
+      a.lse_seq = c->dv.l_full * cf.n_heads;
+      a.s_out = c->ptr<float>(c->lay.s_all);
+      a.s_seq = (int64_t)cf.n_blocks * cf.n_frames * c->dv.n_s;
+      a.alpha = c->ptr<float>(c->lay.alpha);
+      a.B = cf.batch;
+      a.F = cf.n_frames;
+      a.n_s = (int)c->dv.n_s;
+      a.H = cf.n_act;
+      a.n_heads = cf.n_heads;
+      a.n_layers = cf.n_blocks;
+      a.q_lay = c->dv.rows_full * ld;
+      a.k_lay = c->dv.rows_full * ld;
+      a.lse_lay = lse_slot;
+      a.s_lay = (int64_t)cf.n_frames * c->dv.n_s;
+      SWAM_HIP(c, launch_score(cf.dtype, a, c->st), "score");
     }
     if (score) {
       c->scores_valid = true;
@@ -701,7 +710,7 @@ int enqueue_step(swam_ctx* c, const swam_model* model, const void* x_full, const
     if ((rc = swam_pack(c, x_full, xp)) != SWAM_OK) return rc;
     for (int l = 0; l < cf.n_blocks; ++l) {
       rc = run_block(c, &model->blocks[l], mod + (int64_t)l * 6 * d, xp, c->packed_rows,
-                     c->ptr<int32_t>(c->lay.cu_packed), cf.batch, nullptr, qkv, -1);
+                     c->ptr<int32_t>(c->lay.cu_packed), cf.batch, nullptr, qkv);
       if (rc != SWAM_OK) return rc;
     }
     if ((rc = swam_unpack(c, xp, x_full, y_full)) != SWAM_OK) return rc;
