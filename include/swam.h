@@ -59,6 +59,9 @@ extern "C" {
 #define SWAM_MAX_FRAMES 64   /* future frames per sequence */
 #define SWAM_MAX_NS 4096     /* spatial tokens per frame */
 #define SWAM_MAX_BATCH 64    /* sequences per call */
+/* Also: batch * L_full < 2^30 rows, and in bf16 batch * L_full * 3 * d_model
+ * < 2^31 elements (32-bit offsets into the QKV buffer); swam_create rejects
+ * larger configurations with SWAM_E_SHAPE. */
 
 typedef enum { SWAM_F32 = 0, SWAM_BF16 = 1 } swam_dtype;
 

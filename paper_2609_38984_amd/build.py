@@ -25,7 +25,7 @@ HIPCC_FLAGS = [
 # per-source code-generation flags: attention keeps its MFMA accumulators in VGPRs so the
 # softmax can rescale them without AGPR round trips
 EXTRA_DEVICE_FLAGS = {
-    "k_attn.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"],
+    "k_attn.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form", "-fno-honor-nans"],
 }
 
 

@@ -30,6 +30,16 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
   return (uint32_t)f32_to_bf16(lo) | ((uint32_t)f32_to_bf16(hi) << 16);
 }
 
+// Physical 16-byte chunk of logical chunk c in row r of an LDS tile with
+// 128-byte rows is c ^ lds_swz(r).  The LDS serves a ds_read_b128 in phases
+// of 16 lanes and a 64-bit read in phases of 32 lanes over 64 four-byte banks;
+// with this swizzle 16 consecutive rows at one logical chunk (the MFMA operand
+// reads) and the transposed 64-bit reads of 8 rows x 64 bytes both hit every
+// bank once per phase.  Only row bits 1..3 matter.
+__device__ __forceinline__ int lds_swz(int r) {
+  return ((r >> 1) & 3) | ((((r >> 1) ^ (r >> 3)) & 1) << 2);
+}
+
 template <typename T> struct Elem;
 template <> struct Elem<float> {
   __device__ __forceinline__ static float load(const float* p) { return *p; }

@@ -15,6 +15,8 @@
 // fp32 path: one wave per (query row, head), online softmax with shuffles.
 #include "common.h"
 
+#include <type_traits>
+
 namespace swam {
 
 constexpr int ATT_BK = 64;      // keys per tile
@@ -44,7 +46,7 @@ __global__ void __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(WP
 attn_fwd_bf16(const bf16_t* __restrict__ qkv, bf16_t* __restrict__ out, float* __restrict__ lse,
      const int32_t* __restrict__ cu, int n_seqs, int n_heads, int n_rows) {
   constexpr int S = 2;                           // LDS stages (K and V tiles)
-  __shared__ uint4 Ks[S][ATT_BK * 8];             // [key][8 chunks], chunk ^ (key & 7)
+  __shared__ uint4 Ks[S][ATT_BK * 8];             // [key][8 chunks], chunk ^ lds_swz(key)
   __shared__ uint4 Vs[S][ATT_BK * 8];
   const int nwg = gridDim.x, pid = blockIdx.x;
   const int xcd = pid & 7, per = nwg >> 3, rem = nwg & 7;
@@ -69,16 +71,24 @@ attn_fwd_bf16(const bf16_t* __restrict__ qkv, bf16_t* __restrict__ out, float* _
   // K and V tiles go global -> LDS directly, row-major with the chunk swizzle
   // applied on the global side: each instruction moves an 8-row slab (1 KB),
   // lane i landing in row i >> 3, physical chunk i & 7.
-  const int lrow = lane >> 3, lchunk = (lane & 7) ^ lrow;
-  const bf16_t* kbase = qkv + d + h * 64 + 8 * lchunk;
-  const bf16_t* vbase = qkv + 2 * d + h * 64 + 8 * lchunk;
+  // (element offsets stay below 2^31: the launcher checks n_rows * 3d)
+  const int lrow = lane >> 3;
+  const int ld32 = 3 * d;
+  const bf16_t* kbase = qkv + d + h * 64;
+  const bf16_t* vbase = qkv + 2 * d + h * 64;
+  int lofs[8 / NW];
+#pragma unroll
+  for (int j = 0; j < 8 / NW; ++j) {
+    const int r0 = (64 / NW) * wave + 8 * j;
+    lofs[j] = 8 * ((lane & 7) ^ lds_swz((r0 & 8) + lrow));
+  }
   auto issue = [&](int buf, int kb) {
 #pragma unroll
     for (int j = 0; j < 8 / NW; ++j) {
       const int r0 = (64 / NW) * wave + 8 * j;
-      const int64_t key = min(kb + r0 + lrow, s1 - 1);
-      __builtin_amdgcn_global_load_lds((glb_void_t*)(kbase + key * ld), (lds_void_t*)(&Ks[buf][r0 * 8]), 16, 0, 0);
-      __builtin_amdgcn_global_load_lds((glb_void_t*)(vbase + key * ld), (lds_void_t*)(&Vs[buf][r0 * 8]), 16, 0, 0);
+      const int e = min(kb + r0 + lrow, s1 - 1) * ld32 + lofs[j];
+      __builtin_amdgcn_global_load_lds((glb_void_t*)(kbase + e), (lds_void_t*)(&Ks[buf][r0 * 8]), 16, 0, 0);
+      __builtin_amdgcn_global_load_lds((glb_void_t*)(vbase + e), (lds_void_t*)(&Vs[buf][r0 * 8]), 16, 0, 0);
     }
   };
   // PV operand (V^T fragment) from transposed LDS reads: within each 16-lane
@@ -86,6 +96,19 @@ attn_fwd_bf16(const bf16_t* __restrict__ qkv, bf16_t* __restrict__ out, float* _
   // receives V[key0 .. key0+3][hd0 + i], i.e. four consecutive keys of one
   // head-dim column (the k order the P^T accumulators provide).
   const int a16 = lane & 15, G = lane >> 4;
+  // loop-invariant part of those addresses: key 32t + 16u + rlo (+ 8 for the
+  // second read), column hd = 32ht + 16 (G & 1) + 4 (a16 & 3); the swizzle
+  // sees only key bits 1..3, i.e. rlo and the +8
+  const int rlo = 4 * g + (a16 >> 2);
+  int vofs[2][2];
+#pragma unroll
+  for (int ht = 0; ht < 2; ++ht)
+#pragma unroll
+    for (int hf = 0; hf < 2; ++hf) {
+      const int r = rlo + 8 * hf;
+      const int hd = 32 * ht + 16 * (G & 1) + 4 * (a16 & 3);
+      vofs[ht][hf] = r * 64 + 8 * ((hd >> 3) ^ lds_swz(r)) + (hd & 7);
+    }
   f32x16 o[2];
 #pragma unroll
   for (int t = 0; t < 2; ++t)
@@ -97,7 +120,9 @@ attn_fwd_bf16(const bf16_t* __restrict__ qkv, bf16_t* __restrict__ out, float* _
 #pragma unroll
   for (int p = 0; p < S - 1; ++p)
     if (p < nkt) issue(p, s0 + p * ATT_BK);
-  for (int kt = 0; kt < nkt; ++kt) {
+  // full tiles carry no masking code; the ragged last tile, if any, runs a
+  // second copy of the body with the key mask
+  auto tile = [&](int kt, auto masked) {
     const int cur = kt % S;
     const int kb = s0 + kt * ATT_BK;
     // tile kt has landed (own DMA done, then everyone's via the barrier); the
@@ -114,12 +139,12 @@ attn_fwd_bf16(const bf16_t* __restrict__ qkv, bf16_t* __restrict__ out, float* _
 #pragma unroll
       for (int s = 0; s < 4; ++s) {
         const int ch = 2 * s + g;
-        bf16x8 kf = __builtin_bit_cast(bf16x8, Ks[cur][key * 8 + (ch ^ (key & 7))]);
+        bf16x8 kf = __builtin_bit_cast(bf16x8, Ks[cur][key * 8 + (ch ^ lds_swz(key))]);
         st[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[s], st[t], 0, 0, 0);
       }
     }
-    const int nvalid = s1 - kb;
-    if (nvalid < ATT_BK) {
+    if constexpr (decltype(masked)::value) {
+      const int nvalid = s1 - kb;
 #pragma unroll
       for (int t = 0; t < 2; ++t)
 #pragma unroll
@@ -155,6 +180,7 @@ attn_fwd_bf16(const bf16_t* __restrict__ qkv, bf16_t* __restrict__ out, float* _
         for (int mm = 0; mm < 8; mm += 2) {
           const float p0 = __builtin_amdgcn_exp2f(fmaf(st[t][8 * u + mm], sc, -m_run));
           const float p1 = __builtin_amdgcn_exp2f(fmaf(st[t][8 * u + mm + 1], sc, -m_run));
+          // row sums from the fp32 probabilities (the exported normaliser)
           psum0 += p0; psum1 += p1;
           pf[t][u][mm] = (__bf16)p0; pf[t][u][mm + 1] = (__bf16)p1;
         }
@@ -162,15 +188,12 @@ attn_fwd_bf16(const bf16_t* __restrict__ qkv, bf16_t* __restrict__ out, float* _
     const unsigned short* vs = reinterpret_cast<const unsigned short*>(&Vs[cur][0]);
 #pragma unroll
     for (int ht = 0; ht < 2; ++ht) {
-      const int hd = 32 * ht + 16 * (G & 1) + 4 * (a16 & 3);
 #pragma unroll
       for (int t = 0; t < 2; ++t)
 #pragma unroll
         for (int u = 0; u < 2; ++u) {
-          const int r1 = 32 * t + 16 * u + 4 * g + (a16 >> 2);
-          const int r2 = r1 + 8;
-          const int e1 = r1 * 64 + 8 * ((hd >> 3) ^ (r1 & 7)) + (hd & 7);
-          const int e2 = r2 * 64 + 8 * ((hd >> 3) ^ (r2 & 7)) + (hd & 7);
+          const int e1 = vofs[ht][0] + (32 * t + 16 * u) * 64;
+          const int e2 = vofs[ht][1] + (32 * t + 16 * u) * 64;
           const v4i16 x1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)(vs + e1));
           const v4i16 x2 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)(vs + e2));
           const uint2 w1 = __builtin_bit_cast(uint2, x1), w2 = __builtin_bit_cast(uint2, x2);
@@ -178,7 +201,10 @@ attn_fwd_bf16(const bf16_t* __restrict__ qkv, bf16_t* __restrict__ out, float* _
           o[ht] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[t][u], o[ht], 0, 0, 0);
         }
     }
-  }
+  };
+  const int nfull = (s1 - s0) / ATT_BK;
+  for (int kt = 0; kt < nfull; ++kt) tile(kt, std::false_type{});
+  if (nfull < nkt) tile(nfull, std::true_type{});
   const float l_tot = l_run + __shfl_xor(l_run, 32);
   if (!qvalid) return;
   const float inv = 1.0f / l_tot;
@@ -232,23 +258,25 @@ hipError_t launch_attention(int dtype, const void* qkv, void* o, float* lse,
                             int n_heads, hipStream_t st) {
   if (n_rows <= 0) return hipSuccess;
   if (dtype == 1) {
+    if (n_rows * 3 * (int64_t)n_heads * 64 >= ((int64_t)1 << 31)) return hipErrorInvalidValue;
     // 8 waves (256 query rows) share each K/V tile when the grid still gives
     // every CU two such workgroups; otherwise 4 waves, with the 4-waves/SIMD
     // register cap only when enough workgroups exist to use it.
     const int slots8 = (int)((n_rows + 255) / 256) + n_seqs;
     const int slots4 = (int)((n_rows + 127) / 128) + n_seqs;
+    const bf16_t* a = (const bf16_t*)qkv;
+    bf16_t* ob = (bf16_t*)o;
+    const int ni = (int)n_rows;
+#define SWAM_ATT(NW_, WPE_, SL_)                                                          \
+  hipLaunchKernelGGL((attn_fwd_bf16<NW_, WPE_>), dim3((SL_) * n_heads), dim3(NW_ * 64), 0, st, \
+                     a, ob, lse, cu_seqlens, n_seqs, n_heads, ni)
     if ((int64_t)(slots8 - n_seqs) * n_heads >= 2 * 256)
-      hipLaunchKernelGGL((attn_fwd_bf16<8, 4>), dim3(slots8 * n_heads), dim3(512), 0, st,
-                         (const bf16_t*)qkv, (bf16_t*)o, lse, cu_seqlens, n_seqs, n_heads,
-                         (int)n_rows);
+      SWAM_ATT(8, 4, slots8);
     else if ((int64_t)(slots4 - n_seqs) * n_heads >= 3 * 256)
-      hipLaunchKernelGGL((attn_fwd_bf16<4, 4>), dim3(slots4 * n_heads), dim3(256), 0, st,
-                         (const bf16_t*)qkv, (bf16_t*)o, lse, cu_seqlens, n_seqs, n_heads,
-                         (int)n_rows);
+      SWAM_ATT(4, 4, slots4);
     else
-      hipLaunchKernelGGL((attn_fwd_bf16<4, 1>), dim3(slots4 * n_heads), dim3(256), 0, st,
-                         (const bf16_t*)qkv, (bf16_t*)o, lse, cu_seqlens, n_seqs, n_heads,
-                         (int)n_rows);
+      SWAM_ATT(4, 1, slots4);
+#undef SWAM_ATT
   } else {
     hipLaunchKernelGGL(attn_fwd_f32, dim3((unsigned)n_rows, n_heads), dim3(64), 0, st,
                        (const float*)qkv, (float*)o, lse, cu_seqlens, n_seqs, n_heads, n_rows);

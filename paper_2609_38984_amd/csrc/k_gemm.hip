@@ -4,7 +4,7 @@
 // MFMA operand is eight consecutive bf16 of one row.  bf16 path: workgroup
 // tile BM x BN x 64, waves arranged WM x WN, each wave a grid of 32x32x16
 // MFMA tiles with fp32 accumulators; A/B tiles double-buffered in LDS with a
-// 16-byte-chunk XOR swizzle (chunk ^ (row & 7)) so the column reads of the
+// 16-byte-chunk XOR swizzle (chunk ^ lds_swz(row)) so the column reads of the
 // MFMA operand layout are spread over all banks.  Workgroup ids are remapped
 // so that each XCD (dispatch round-robins over 8) receives a contiguous run
 // of tiles, grouped GROUP_M tile-rows deep, to share its L2.
@@ -57,19 +57,20 @@ template <int BM, int BN, int TM, int TN, int FM, int FN>
 __device__ __forceinline__ void mma_stage(const uint4* __restrict__ as, const uint4* __restrict__ bs,
                                           int wm, int wn, int lane, f32x16 (&acc)[FM][FN]) {
   const int khalf = lane >> 5, r31 = lane & 31;
+  const int sw = lds_swz(r31);   // rows differ from r31 by multiples of 32
 #pragma unroll
   for (int s = 0; s < GEMM_BK / 16; ++s) {
-    const int chunk = 2 * s + khalf;
+    const int chunk = (2 * s + khalf) ^ sw;
     bf16x8 af[FM], bfr[FN];
 #pragma unroll
     for (int i = 0; i < FM; ++i) {
       const int row = wm * TM + i * 32 + r31;
-      af[i] = __builtin_bit_cast(bf16x8, as[row * 8 + (chunk ^ (row & 7))]);
+      af[i] = __builtin_bit_cast(bf16x8, as[row * 8 + chunk]);
     }
 #pragma unroll
     for (int j = 0; j < FN; ++j) {
       const int row = wn * TN + j * 32 + r31;
-      bfr[j] = __builtin_bit_cast(bf16x8, bs[row * 8 + (chunk ^ (row & 7))]);
+      bfr[j] = __builtin_bit_cast(bf16x8, bs[row * 8 + chunk]);
     }
 #pragma unroll
     for (int i = 0; i < FM; ++i)
@@ -82,7 +83,7 @@ __device__ __forceinline__ void mma_stage(const uint4* __restrict__ as, const ui
 // Stage loads go global -> LDS directly (no registers): each instruction moves
 // 8 rows x 128 bytes; lane i lands at slot i of the 1 KB slab, i.e. row
 // lane >> 3 and physical chunk lane & 7, so it fetches logical chunk
-// (lane & 7) ^ (row & 7) -- the swizzle is applied on the global side.
+// (lane & 7) ^ lds_swz(row) -- the swizzle is applied on the global side.
 template <int BM, int BN, int WM, int WN, int EPI>
 __global__ void __launch_bounds__(WM * WN * 64)
 gemm_bf16_nt(const bf16_t* __restrict__ A, int64_t lda, const bf16_t* __restrict__ B,
@@ -100,13 +101,18 @@ gemm_bf16_nt(const bf16_t* __restrict__ A, int64_t lda, const bf16_t* __restrict
   const int m0 = tm * BM, n0 = tn * BN;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave / WN, wn = wave % WN;
-  const int lrow = lane >> 3, lchunk = (lane & 7) ^ lrow;
+  const int lrow = lane >> 3;
+  // logical chunk fetched by this lane for an 8-row slab starting at row8
+  // (a multiple of 8): only bit 3 of the row beyond lrow enters the swizzle
+  auto lchunk = [&](int row8) { return (lane & 7) ^ lds_swz(row8 + lrow); };
 
   auto a_src = [&](int j) {
-    return A + (int64_t)min(m0 + (wave * A_INS + j) * 8 + lrow, M - 1) * lda + 8 * lchunk;
+    const int r = (wave * A_INS + j) * 8;
+    return A + (int64_t)min(m0 + r + lrow, M - 1) * lda + 8 * lchunk(r & 8);
   };
   auto b_src = [&](int j) {
-    return B + (int64_t)min(n0 + (wave * B_INS + j) * 8 + lrow, N - 1) * ldb + 8 * lchunk;
+    const int r = (wave * B_INS + j) * 8;
+    return B + (int64_t)min(n0 + r + lrow, N - 1) * ldb + 8 * lchunk(r & 8);
   };
   auto issue = [&](uint4* as, uint4* bs, int k0) {
 #pragma unroll

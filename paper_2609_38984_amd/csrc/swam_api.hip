@@ -77,6 +77,9 @@ int derive(const swam_config* c, Derived* dv, std::string* err) {
   const int64_t l_full = c->n_ctx + (int64_t)c->n_frames * n_s + c->n_act;
   const int64_t rows = (int64_t)c->batch * l_full;
   if (rows >= (1ll << 30)) return fail(err, SWAM_E_SHAPE, "batch * tokens exceeds 2^30");
+  // the bf16 attention addresses the QKV buffer with 32-bit element offsets
+  if (c->dtype == SWAM_BF16 && rows * 3 * d >= (1ll << 31))
+    return fail(err, SWAM_E_SHAPE, "batch * tokens * 3 * d_model must stay below 2^31");
   dv->n_s = n_s;
   dv->g = g;
   dv->l_full = l_full;

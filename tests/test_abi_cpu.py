@@ -63,6 +63,9 @@ def test_plan_sizes(lib, n, want):
     (dict(frame_h=1, frame_w=1), -2),
     (dict(mass_threshold=1.5), -1),
     (dict(n_act=2 * 17, n_frames=2), -2),  # more than 16 queries per group
+    # bf16 QKV buffer beyond 2^31 elements: 64 x 4112 rows x 3 x 4096
+    (dict(dtype=1, batch=64, n_heads=64, d_model=4096, n_frames=1, frame_h=64, frame_w=64,
+          n_act=16, n_ctx=0, k_core=100, k_anchor=10), -2),
 ])
 def test_plan_rejects_bad_configs(lib, bad, code):
     from paper_2609_38984_amd import swam
