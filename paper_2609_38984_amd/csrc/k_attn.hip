@@ -40,14 +40,16 @@ typedef short v4i16 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) v4i16 lds_v4i16;
 
 // NW waves x 32 query rows per workgroup; WPE = minimum waves per SIMD the
-// register allocation must allow (4 caps it at 128 VGPRs without spills).
-template <int NW, int WPE>
+// register allocation must allow (4 caps it at 128 VGPRs); SUB 64-key tiles
+// share one LDS stage, i.e. one barrier and one DMA wait.
+template <int NW, int WPE, int SUB>
 __global__ void __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(WPE, 8)))
 attn_fwd_bf16(const bf16_t* __restrict__ qkv, bf16_t* __restrict__ out, float* __restrict__ lse,
      const int32_t* __restrict__ cu, int n_seqs, int n_heads, int n_rows) {
   constexpr int S = 2;                           // LDS stages (K and V tiles)
-  __shared__ uint4 Ks[S][ATT_BK * 8];             // [key][8 chunks], chunk ^ lds_swz(key)
-  __shared__ uint4 Vs[S][ATT_BK * 8];
+  constexpr int SK = SUB * ATT_BK;               // keys per stage: SUB tiles per barrier
+  __shared__ uint4 Ks[S][SK * 8];                 // [key][8 chunks], chunk ^ lds_swz(key)
+  __shared__ uint4 Vs[S][SK * 8];
   const int nwg = gridDim.x, pid = blockIdx.x;
   const int xcd = pid & 7, per = nwg >> 3, rem = nwg & 7;
   const int id = xcd * per + min(xcd, rem) + (pid >> 3);
@@ -76,16 +78,17 @@ attn_fwd_bf16(const bf16_t* __restrict__ qkv, bf16_t* __restrict__ out, float* _
   const int ld32 = 3 * d;
   const bf16_t* kbase = qkv + d + h * 64;
   const bf16_t* vbase = qkv + 2 * d + h * 64;
-  int lofs[8 / NW];
+  constexpr int SLABS = SK / 8 / NW;             // 8-row slabs per wave and stage
+  int lofs[SLABS];
 #pragma unroll
-  for (int j = 0; j < 8 / NW; ++j) {
-    const int r0 = (64 / NW) * wave + 8 * j;
+  for (int j = 0; j < SLABS; ++j) {
+    const int r0 = (SK / NW) * wave + 8 * j;
     lofs[j] = 8 * ((lane & 7) ^ lds_swz((r0 & 8) + lrow));
   }
   auto issue = [&](int buf, int kb) {
 #pragma unroll
-    for (int j = 0; j < 8 / NW; ++j) {
-      const int r0 = (64 / NW) * wave + 8 * j;
+    for (int j = 0; j < SLABS; ++j) {
+      const int r0 = (SK / NW) * wave + 8 * j;
       const int e = min(kb + r0 + lrow, s1 - 1) * ld32 + lofs[j];
       __builtin_amdgcn_global_load_lds((glb_void_t*)(kbase + e), (lds_void_t*)(&Ks[buf][r0 * 8]), 16, 0, 0);
       __builtin_amdgcn_global_load_lds((glb_void_t*)(vbase + e), (lds_void_t*)(&Vs[buf][r0 * 8]), 16, 0, 0);
@@ -116,20 +119,14 @@ attn_fwd_bf16(const bf16_t* __restrict__ qkv, bf16_t* __restrict__ out, float* _
     for (int r = 0; r < 16; ++r) o[t][r] = 0.0f;
   float m_run = -1e30f, l_run = 0.0f;
   const float sc = 1.4426950408889634f * 0.125f;
-  const int nkt = (s1 - s0 + ATT_BK - 1) / ATT_BK;
+  const int nkt = (s1 - s0 + SK - 1) / SK;       // stages
 #pragma unroll
   for (int p = 0; p < S - 1; ++p)
-    if (p < nkt) issue(p, s0 + p * ATT_BK);
-  // full tiles carry no masking code; the ragged last tile, if any, runs a
-  // second copy of the body with the key mask
-  auto tile = [&](int kt, auto masked) {
-    const int cur = kt % S;
-    const int kb = s0 + kt * ATT_BK;
-    // tile kt has landed (own DMA done, then everyone's via the barrier); the
-    // barrier also releases the stage the next prefetch overwrites
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-    __syncthreads();
-    if (kt + S - 1 < nkt) issue((kt + S - 1) % S, kb + (S - 1) * ATT_BK);
+    if (p < nkt) issue(p, s0 + p * SK);
+  // one 64-key tile of stage buffer `cur` at key offset sub * 64; full tiles
+  // carry no masking code, the ragged last one runs a copy with the key mask
+  auto tile = [&](int cur, int sub, int kb, auto masked) {
+    const uint4* Kt = &Ks[cur][sub * ATT_BK * 8];
     f32x16 st[2];
 #pragma unroll
     for (int t = 0; t < 2; ++t) {
@@ -139,7 +136,7 @@ attn_fwd_bf16(const bf16_t* __restrict__ qkv, bf16_t* __restrict__ out, float* _
 #pragma unroll
       for (int s = 0; s < 4; ++s) {
         const int ch = 2 * s + g;
-        bf16x8 kf = __builtin_bit_cast(bf16x8, Ks[cur][key * 8 + (ch ^ lds_swz(key))]);
+        bf16x8 kf = __builtin_bit_cast(bf16x8, Kt[key * 8 + (ch ^ lds_swz(key))]);
         st[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[s], st[t], 0, 0, 0);
       }
     }
@@ -185,7 +182,7 @@ attn_fwd_bf16(const bf16_t* __restrict__ qkv, bf16_t* __restrict__ out, float* _
           pf[t][u][mm] = (__bf16)p0; pf[t][u][mm + 1] = (__bf16)p1;
         }
     l_run += psum0 + psum1;
-    const unsigned short* vs = reinterpret_cast<const unsigned short*>(&Vs[cur][0]);
+    const unsigned short* vs = reinterpret_cast<const unsigned short*>(&Vs[cur][sub * ATT_BK * 8]);
 #pragma unroll
     for (int ht = 0; ht < 2; ++ht) {
 #pragma unroll
@@ -202,9 +199,27 @@ attn_fwd_bf16(const bf16_t* __restrict__ qkv, bf16_t* __restrict__ out, float* _
         }
     }
   };
-  const int nfull = (s1 - s0) / ATT_BK;
-  for (int kt = 0; kt < nfull; ++kt) tile(kt, std::false_type{});
-  if (nfull < nkt) tile(nfull, std::true_type{});
+  auto stage = [&](int kt, auto masked) {
+    const int cur = kt % S;
+    const int kb = s0 + kt * SK;
+    // stage kt has landed (own DMA done, then everyone's via the barrier); the
+    // barrier also releases the stage the next prefetch overwrites
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();
+    if (kt + S - 1 < nkt) issue((kt + S - 1) % S, kb + (S - 1) * SK);
+#pragma unroll
+    for (int sub = 0; sub < SUB; ++sub) {
+      const int kbs = kb + sub * ATT_BK;
+      if constexpr (decltype(masked)::value) {
+        if (s1 > kbs) tile(cur, sub, kbs, std::true_type{});   // a no-op mask when full
+      } else {
+        tile(cur, sub, kbs, std::false_type{});
+      }
+    }
+  };
+  const int nfull = (s1 - s0) / SK;
+  for (int kt = 0; kt < nfull; ++kt) stage(kt, std::false_type{});
+  if (nfull < nkt) stage(nfull, std::true_type{});
   const float l_tot = l_run + __shfl_xor(l_run, 32);
   if (!qvalid) return;
   const float inv = 1.0f / l_tot;
@@ -267,15 +282,17 @@ hipError_t launch_attention(int dtype, const void* qkv, void* o, float* lse,
     const bf16_t* a = (const bf16_t*)qkv;
     bf16_t* ob = (bf16_t*)o;
     const int ni = (int)n_rows;
-#define SWAM_ATT(NW_, WPE_, SL_)                                                          \
-  hipLaunchKernelGGL((attn_fwd_bf16<NW_, WPE_>), dim3((SL_) * n_heads), dim3(NW_ * 64), 0, st, \
-                     a, ob, lse, cu_seqlens, n_seqs, n_heads, ni)
+#define SWAM_ATT(NW_, WPE_, SUB_, SL_)                                                       \
+  hipLaunchKernelGGL((attn_fwd_bf16<NW_, WPE_, SUB_>), dim3((SL_) * n_heads), dim3(NW_ * 64), 0, \
+                     st, a, ob, lse, cu_seqlens, n_seqs, n_heads, ni)
+    // the 8-wave kernel stages 128 keys per barrier (64 KB of LDS, two
+    // workgroups per CU); the 4-wave ones keep 64 so four fit on a CU
     if ((int64_t)(slots8 - n_seqs) * n_heads >= 2 * 256)
-      SWAM_ATT(8, 4, slots8);
+      SWAM_ATT(8, 4, 2, slots8);
     else if ((int64_t)(slots4 - n_seqs) * n_heads >= 3 * 256)
-      SWAM_ATT(4, 4, slots4);
+      SWAM_ATT(4, 4, 1, slots4);
     else
-      SWAM_ATT(4, 1, slots4);
+      SWAM_ATT(4, 1, 1, slots4);
 #undef SWAM_ATT
   } else {
     hipLaunchKernelGGL(attn_fwd_f32, dim3((unsigned)n_rows, n_heads), dim3(64), 0, st,
