@@ -244,6 +244,9 @@ def measure(cfg, model, xs, tembs, steps, warmup, reps):
                 "launches": n_dom, "avg_launch_us": round(ms_dom * 1e3 / max(n_dom, 1), 2)}
 
     def median_ms(flags, tau):
+        # the paper's protocol: 5 untimed runs, then `reps` timed ones, median
+        for _ in range(5):
+            run(tau, flags)
         ts = []
         for _ in range(reps):
             e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -308,6 +311,8 @@ def measure_graph(cfg, model, xs, tembs, steps, reps):
         elapsed = time.perf_counter() - t0
 
         def median_ms(flags, tau):
+            for _ in range(5):
+                run(tau, flags)
             ts = []
             for _ in range(reps):
                 e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -348,7 +353,7 @@ def sweep(args):
     print("|" + "---|" * 16)
 
     def emit(cfg, ret, m, model, xs, tembs):
-        g = measure_graph(cfg, model, xs, tembs, cfg.n_steps, args.reps)
+        g = measure_graph(cfg, model, xs, tembs, cfg.n_steps, args.sweep_reps)
         rf = m["roofline"]
         line = (f"| {cfg.name} | {ret} | {cfg.reuse_R} | {m['packed_rows']} | {m['dense_step_ms']:.2f} | "
                 f"{m['refresh_step_ms']:.2f} | {m['sparse_step_ms']:.2f} | {m['schedule_step_ms']:.2f} | "
@@ -363,7 +368,7 @@ def sweep(args):
         blocks_np, model = load_model(cfg, dev, adt)
         _, xs, tembs = inputs_for(cfg, blocks_np, dev, adt)
         emit(cfg, f"{cfg.k_core}+{cfg.k_anchor} of {cfg.n_s}",
-             measure(cfg, model, xs, tembs, cfg.n_steps, 2, args.reps), model, xs, tembs)
+             measure(cfg, model, xs, tembs, cfg.n_steps, 2, args.sweep_reps), model, xs, tembs)
         del model, xs
         torch.cuda.empty_cache()
     base = W.preset(4, percent=25)
@@ -373,13 +378,13 @@ def sweep(args):
         for R in (1, 2, 4):
             cfg = W.preset(4, percent=pct, reuse_R=R)
             emit(cfg, f"{pct}% ({cfg.k_core}+{cfg.k_anchor})",
-                 measure(cfg, model, xs, tembs, cfg.n_steps, 2, args.reps), model, xs, tembs)
+                 measure(cfg, model, xs, tembs, cfg.n_steps, 2, args.sweep_reps), model, xs, tembs)
     del model, xs
     torch.cuda.empty_cache()
     cfg = W.preset(5)
     blocks_np, model = load_model(cfg, dev, torch.bfloat16)
     _, xs, tembs = inputs_for(cfg, blocks_np, dev, torch.bfloat16)
-    emit(cfg, "mass 0.8", measure(cfg, model, xs, tembs, cfg.n_steps, 2, args.reps), model, xs,
+    emit(cfg, "mass 0.8", measure(cfg, model, xs, tembs, cfg.n_steps, 2, args.sweep_reps), model, xs,
          tembs)
 
 
@@ -468,7 +473,75 @@ def read_traffic(cls, workload):
         return None
 
 
+def summarize_mfma(db_path, bench_json):
+    """MFMA-busy share per MFMA kernel class over the timed steps, from one
+    `rocprofv3 --kernel-trace --pmc SQ_VALU_MFMA_BUSY_CYCLES SQ_BUSY_CYCLES
+    GRBM_GUI_ACTIVE SQ_INSTS_VALU_MFMA_MOPS_BF16` run of this benchmark.
+    SQ_VALU_MFMA_BUSY_CYCLES counts SIMD-cycles with the matrix core busy; it
+    is divided by the launch time x 2.4 GHz x 1024 SIMDs (the clock of the
+    2.5 PFLOP/s peak).  SQ_INSTS_VALU_MFMA_MOPS_BF16 x 512 is the flops the
+    matrix cores executed (padding of ragged tiles included).  GRBM_GUI_ACTIVE
+    / 8 XCDs / launch time is shown as the clock the GPU ran at (approximate
+    for short launches, whose counts include dispatch overhead)."""
+    import sqlite3
+    res = json.load(open(bench_json))
+    cfgj = res["config"]
+    con = sqlite3.connect(db_path)
+    rows = con.execute("select dispatch_id, name, counter_name, sum(counter_value) from pmc_events "
+                       "group by dispatch_id, counter_name").fetchall()
+    cnt, names = {}, {}
+    for did, name, c, v in rows:
+        cnt.setdefault(did, {})[c] = v
+        names[did] = name
+    dur = {did: b - a for did, a, b in con.execute("select dispatch_id, start, end from kernels")}
+    cfg = workload_from_json(cfgj)
+    packed = cfgj["packed_rows"]
+    lines = [f"{'class':10s} {'launches':>8s} {'avg_us':>8s} {'MFMA_busy_%':>11s} {'alg_TFLOP/s':>11s} "
+             f"{'%_of_2.5PF':>10s} {'exec/alg_flops':>14s} {'GRBM_clock_GHz':>14s}"]
+    skip = res["warmup"] * cfgj["n_blocks"]
+    for cls in ("ATTN", "GEMM_QKV", "GEMM_OUT", "GEMM_UP", "GEMM_DOWN"):
+        sub, epi = KERNEL_OF_CLASS[cls]
+        seq = [did for did in sorted(cnt) if sub in names[did] and (epi is None or epi in names[did])]
+        if cls in ("GEMM_OUT", "GEMM_DOWN"):
+            seq = seq[0::2] if cls == "GEMM_OUT" else seq[1::2]
+        win = seq[skip: skip + len(res["config"]["schedule_kinds"]) * cfgj["n_blocks"]]
+        if not win:
+            continue
+        kinds = res["config"]["schedule_kinds"]
+        alg = 0.0
+        for i, _ in enumerate(win):
+            k = kinds[i // cfgj["n_blocks"]]
+            rows_k = [cfgj["l_full"]] * cfgj["batch"] if k != 2 else [packed]
+            alg += kernel_work(cfg, cls, rows_k)
+        t = sum(dur.get(d, 0) for d in win) * 1e-9
+        gui = sum(cnt[d].get("GRBM_GUI_ACTIVE", 0) for d in win) / 8.0
+        busy = sum(cnt[d].get("SQ_VALU_MFMA_BUSY_CYCLES", 0) for d in win)
+        mops = sum(cnt[d].get("SQ_INSTS_VALU_MFMA_MOPS_BF16", 0) for d in win)
+        lines.append(f"{cls:10s} {len(win):8d} {t / len(win) * 1e6:8.1f} "
+                     f"{100.0 * busy / (t * 2.4e9 * 1024):11.1f} {alg / t / 1e12:11.1f} "
+                     f"{100.0 * alg / t / 1e12 / PEAK_BF16_TFLOPS:10.1f} {mops * 512 / alg:14.3f} "
+                     f"{gui / t / 1e9:14.2f}")
+    return "\n".join(lines)
+
+
+def workload_from_json(cj):
+    import workload as W
+    for n in (1, 2, 3, 5):
+        c = W.preset(n)
+        if c.name == cj["workload"]:
+            return c
+    for pct in (10, 25, 50, 100):
+        for R in (1, 2, 4):
+            c = W.preset(4, percent=pct, reuse_R=R)
+            if c.name == cj["workload"]:
+                return c
+    raise KeyError(cj["workload"])
+
+
 def main():
+    if len(sys.argv) > 1 and sys.argv[1] == "--mfma":
+        print(summarize_mfma(sys.argv[2], sys.argv[3]))
+        return
     if len(sys.argv) > 1 and sys.argv[1] == "--summarize":
         print(summarize_rocprof(sys.argv[2], sys.argv[3]))
         return
@@ -482,7 +555,9 @@ def main():
     ap.add_argument("--config", type=int, default=3)
     ap.add_argument("--percent", type=int, default=25, help="retention for workload 4")
     ap.add_argument("--reuse", type=int, default=0, help="override the reuse interval R")
-    ap.add_argument("--reps", type=int, default=5, help="repetitions per step kind for medians")
+    ap.add_argument("--reps", type=int, default=30,
+                    help="timed repetitions per step kind for the medians (after 5 untimed)")
+    ap.add_argument("--sweep-reps", type=int, default=5, help="the same, per sweep workload")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--sweep", action="store_true", help="markdown table over all workloads")
     args = ap.parse_args()
