@@ -24,6 +24,7 @@ import numpy as np
 __all__ = [
     "SwamConfig", "preset", "PRESETS", "budgets", "rng_for", "block_weights",
     "timestep_embedding", "StepInputs", "make_inputs", "blob_direction",
+    "time_embedding", "latent_io_weights", "SamplerInputs", "make_sampler_inputs",
 ]
 
 
@@ -216,6 +217,14 @@ def block_weights(cfg: SwamConfig, layer: int) -> dict:
     return {k: _storage(cfg, v) for k, v in w.items()}
 
 
+def time_embedding(cfg: SwamConfig, t: float) -> np.ndarray:
+    """Sinusoidal embedding of a model time t, layout [cos | sin]."""
+    half = cfg.d_temb // 2
+    freqs = np.exp(-math.log(10000.0) * np.arange(half, dtype=np.float64) / half)
+    arg = float(t) * freqs
+    return np.concatenate([np.cos(arg), np.sin(arg)]).astype(np.float32)
+
+
 def timestep_embedding(cfg: SwamConfig, tau: int) -> np.ndarray:
     """Sinusoidal embedding of t = 1000 (N - tau) / N, layout [cos | sin]."""
     t = 1000.0 * (cfg.n_steps - tau) / cfg.n_steps
@@ -330,3 +339,40 @@ def make_inputs(cfg: SwamConfig, w_qkv0: np.ndarray | None = None) -> StepInputs
         inp.blobs.append(blobs)
         inp.direction.append(blob_direction(cfg, w_qkv0, act))
     return inp
+
+
+# ---------------------------------------------------------------------------
+# closed-loop sampling: latent embedding / velocity read-out and initial noise
+# ---------------------------------------------------------------------------
+_STREAM_LATENT_W = 5
+_STREAM_LATENT_Z = 6
+
+
+def latent_io_weights(cfg: SwamConfig, d_latent: int = 16) -> dict:
+    """Latent embedding w_in [d][c], b_in [d] (std 1/sqrt(c), so unit-variance
+    latents give unit-variance tokens) and velocity head w_v [c][d], b_v [c]
+    (std 1/sqrt(d)), on the storage grid of the configuration."""
+    d, c = cfg.d_model, d_latent
+    rng = rng_for(cfg, _STREAM_LATENT_W)
+    w = {"w_in": _normal(rng, (d, c), 1.0 / math.sqrt(c)),
+         "b_in": _normal(rng, (d,), 1.0 / math.sqrt(c)),
+         "w_v": _normal(rng, (c, d), 1.0 / math.sqrt(d)),
+         "b_v": _normal(rng, (c,), 1.0 / math.sqrt(d))}
+    return {k: _storage(cfg, v) for k, v in w.items()}
+
+
+@dataclass
+class SamplerInputs:
+    """Context tokens per sequence ([B][n_ctx][d], storage grid) and the
+    initial latent noise z0 ([B * (F*N_s + H)][c] float32, future then action
+    tokens of each sequence)."""
+    ctx: np.ndarray
+    z0: np.ndarray
+
+
+def make_sampler_inputs(cfg: SwamConfig, d_latent: int = 16) -> SamplerInputs:
+    base = make_inputs(cfg)
+    ctx = np.stack([b[:cfg.n_ctx] for b in base.base]).astype(np.float32)
+    rng = rng_for(cfg, _STREAM_LATENT_Z)
+    z0 = rng.standard_normal((cfg.batch * (cfg.l_full - cfg.n_ctx), d_latent), dtype=np.float32)
+    return SamplerInputs(ctx=_storage(cfg, ctx), z0=z0)
