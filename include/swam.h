@@ -285,13 +285,62 @@ int swam_step_graph(swam_ctx* ctx, const swam_model* model, const void* x_full,
 /* Synchronise and free every cached graph of ctx. */
 int swam_graph_clear(swam_ctx* ctx);
 
+/* ------------------------------------------ sampling update (Sec. 4.2) */
+
+/* Latent read-in and read-out of the backbone (c = d_latent channels per
+ * token, 1..64; matrices [out_features][in_features] row-major in the config
+ * dtype).  Latent tensors -- z, velocities v, the velocity cache -- are float
+ * [B][L_lat][c] with L_lat = F*N_s + H: the future tokens of each sequence
+ * (frame-major, row-major in a frame) followed by its action tokens, i.e. the
+ * full-layout rows n_ctx .. l_full-1 of every sequence. */
+typedef struct {
+  int32_t d_latent;
+  const void* w_in;  const void* b_in;     /* [d][c], [d]: token = z W_in^T + b_in */
+  const void* w_v;   const void* b_v;      /* [c][d], [c]: v = LN(y) W_v^T + b_v   */
+} swam_latent_io;
+
+/* Tokens of the latent rows of x_full [B*l_full][d] from z (stored in the
+ * config dtype); context rows are not touched. */
+int swam_embed(swam_ctx* ctx, const swam_latent_io* io, const float* z, void* x_full);
+
+/* Velocity read-out v = LN(y) W_v^T + b_v (LayerNorm without affine, eps
+ * 1e-6) of the latent rows of y_full.  retained_only != 0: only the rows of
+ * the cached selection (retained future tokens and all action tokens; other
+ * rows of v are left as they are; SWAM_E_STATE without a selection). */
+int swam_velocity(swam_ctx* ctx, const swam_latent_io* io, const void* y_full,
+                  int32_t retained_only, float* v);
+
+/* One sampler update of z in place (c = d_latent channels), z <- z + dsigma * v~, where v~ is
+ *   kind SWAM_KIND_DENSE  : v;
+ *   kind SWAM_KIND_REFRESH: v, and the future-token rows of v are stored in
+ *                           v_cache (the full step caches the visual velocity);
+ *   kind SWAM_KIND_SPARSE : the paper's merge M v + (1 - M) v_cache over the
+ *                           future tokens, M = the cached selection (Sec. 4.2,
+ *                           cached visual prediction eq.); action rows take v.
+ * (fp32 FMA per element.)  v_cache may be NULL for SWAM_KIND_DENSE. */
+int swam_sample_update(swam_ctx* ctx, int32_t d_latent, const float* v, float* v_cache,
+                       float* z, float dsigma, int32_t kind);
+
+/* One closed-loop sampling step: swam_embed(z -> x_full), swam_step(x_full ->
+ * y_full), swam_velocity (all latent rows after a full step, the retained
+ * rows after a sparse one) and swam_sample_update with the step's kind.
+ * x_full must hold the context tokens in its context rows and must not
+ * alias y_full (the context rows stay the conditioning of the next step).
+ * dsigma = sigma_{tau+1} - sigma_tau of the caller's schedule (the paper's
+ * backbones use a flow schedule with shift 5.0, App. B.2); temb encodes the
+ * model time of step tau. */
+int swam_sample_step(swam_ctx* ctx, const swam_model* model, const swam_latent_io* io,
+                     float* z, float* v, float* v_cache, void* x_full, void* y_full,
+                     const float* temb, int32_t tau, float dsigma, int32_t flags,
+                     int32_t* kind_out);
+
 /* --------------------------------------------------------- timers */
 
 /* Kernel / phase classes for on-stream timing with HIP events. */
 enum {
   SWAM_T_ADALN = 0, SWAM_T_LNMOD, SWAM_T_GEMM_QKV, SWAM_T_ATTN, SWAM_T_GEMM_OUT,
   SWAM_T_GEMM_UP, SWAM_T_GEMM_DOWN, SWAM_T_SCORE, SWAM_T_REDUCE, SWAM_T_SELECT,
-  SWAM_T_PACK, SWAM_T_UNPACK, SWAM_T_COPY, SWAM_T_COUNT
+  SWAM_T_PACK, SWAM_T_UNPACK, SWAM_T_COPY, SWAM_T_SAMPLE, SWAM_T_COUNT
 };
 
 /* Bracket every launch (phase) of the classes in `mask` (bit i = class i)

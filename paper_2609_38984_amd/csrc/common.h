@@ -157,6 +157,16 @@ hipError_t launch_unpack_scatter(const void* y_packed, void* y_full, const int32
 hipError_t launch_unpack_merge(const void* y_packed, const void* x_full, void* y_full,
                                const int32_t* pack_pos, int64_t rows, int64_t row_bytes,
                                hipStream_t st);
+// sampling update (k_sampler.hip)
+hipError_t launch_embed(int dtype, const float* z, const void* w_in, const void* b_in, void* x,
+                        int64_t n_lat_rows, int l_lat, int l_full, int n_ctx, int c, int d,
+                        hipStream_t st);
+hipError_t launch_velocity(int dtype, const void* y, const int32_t* gather, int64_t n_items,
+                           const void* w_v, const void* b_v, float* v, int l_lat, int l_full,
+                           int n_ctx, int c, int d, hipStream_t st);
+hipError_t launch_sample_update(const float* v, float* v_cache, float* z, const int32_t* pack_pos,
+                                float dsigma, int kind, int64_t n_lat_rows, int l_lat, int l_full,
+                                int n_ctx, int n_fut, int c, hipStream_t st);
 hipError_t launch_copy(const void* src, void* dst, int64_t bytes, hipStream_t st);
 
 }  // namespace swam

@@ -14,6 +14,8 @@
 #include "../../include/swam.h"
 #include "common.h"
 
+#include <cmath>
+
 using namespace swam;
 
 namespace {
@@ -749,6 +751,93 @@ int swam_step(swam_ctx* c, const swam_model* model, const void* x_full, const fl
   int rc = check_step(c, model, x_full, temb, tau, y_full, flags, &kind);
   if (rc != SWAM_OK) return rc;
   if ((rc = enqueue_step(c, model, x_full, temb, kind, y_full)) != SWAM_OK) return rc;
+  if (kind_out) *kind_out = kind;
+  return SWAM_OK;
+}
+
+// ------------------------------------------------------------- sampler
+
+static int check_io(swam_ctx* c, const swam_latent_io* io) {
+  if (!io) return set_err(c, SWAM_E_INVALID, "latent io is NULL");
+  if (io->d_latent < 1 || io->d_latent > 64)
+    return set_err(c, SWAM_E_SHAPE, "d_latent must be in [1, 64]");
+  if (!io->w_in || !io->b_in || !io->w_v || !io->b_v)
+    return set_err(c, SWAM_E_INVALID, "NULL latent io weight");
+  return SWAM_OK;
+}
+
+int swam_embed(swam_ctx* c, const swam_latent_io* io, const float* z, void* x_full) {
+  if (!c) return set_err(nullptr, SWAM_E_INVALID, "ctx is NULL");
+  int rc = check_io(c, io);
+  if (rc != SWAM_OK) return rc;
+  if (!z || !x_full) return set_err(c, SWAM_E_INVALID, "NULL tensor");
+  const swam_config& cf = c->cfg;
+  const int l_lat = (int)(c->dv.l_full - cf.n_ctx);
+  Timed t(c, SWAM_T_SAMPLE);
+  SWAM_HIP(c, launch_embed(cf.dtype, z, io->w_in, io->b_in, x_full, (int64_t)cf.batch * l_lat, l_lat,
+                           (int)c->dv.l_full, cf.n_ctx, io->d_latent, (int)c->dv.d, c->st),
+           "embed");
+  return SWAM_OK;
+}
+
+int swam_velocity(swam_ctx* c, const swam_latent_io* io, const void* y_full, int32_t retained_only,
+                  float* v) {
+  if (!c) return set_err(nullptr, SWAM_E_INVALID, "ctx is NULL");
+  int rc = check_io(c, io);
+  if (rc != SWAM_OK) return rc;
+  if (!y_full || !v) return set_err(c, SWAM_E_INVALID, "NULL tensor");
+  if (retained_only && !c->sel_valid) return set_err(c, SWAM_E_STATE, "no selection cached");
+  const swam_config& cf = c->cfg;
+  const int l_lat = (int)(c->dv.l_full - cf.n_ctx);
+  const int32_t* gather = retained_only ? c->ptr<int32_t>(c->lay.gather) : nullptr;
+  const int64_t items = retained_only ? c->packed_rows : (int64_t)cf.batch * l_lat;
+  Timed t(c, SWAM_T_SAMPLE);
+  SWAM_HIP(c, launch_velocity(cf.dtype, y_full, gather, items, io->w_v, io->b_v, v, l_lat,
+                              (int)c->dv.l_full, cf.n_ctx, io->d_latent, (int)c->dv.d, c->st),
+           "velocity");
+  return SWAM_OK;
+}
+
+static int sample_update(swam_ctx* c, int c_lat, const float* v, float* v_cache, float* z,
+                         float dsigma, int32_t kind) {
+  if (!v || !z) return set_err(c, SWAM_E_INVALID, "NULL tensor");
+  if (kind != SWAM_KIND_DENSE && kind != SWAM_KIND_REFRESH && kind != SWAM_KIND_SPARSE)
+    return set_err(c, SWAM_E_INVALID, "bad step kind");
+  if (kind != SWAM_KIND_DENSE && !v_cache) return set_err(c, SWAM_E_INVALID, "NULL velocity cache");
+  if (kind == SWAM_KIND_SPARSE && !c->sel_valid) return set_err(c, SWAM_E_STATE, "no selection cached");
+  if (!std::isfinite(dsigma)) return set_err(c, SWAM_E_INVALID, "dsigma is not finite");
+  const swam_config& cf = c->cfg;
+  const int l_lat = (int)(c->dv.l_full - cf.n_ctx);
+  Timed t(c, SWAM_T_SAMPLE);
+  SWAM_HIP(c, launch_sample_update(v, v_cache, z, c->ptr<int32_t>(c->lay.pack_pos), dsigma, kind,
+                                   (int64_t)cf.batch * l_lat, l_lat, (int)c->dv.l_full, cf.n_ctx,
+                                   (int)(cf.n_frames * c->dv.n_s), c_lat, c->st),
+           "sample update");
+  return SWAM_OK;
+}
+
+int swam_sample_update(swam_ctx* c, int32_t d_latent, const float* v, float* v_cache, float* z,
+                       float dsigma, int32_t kind) {
+  if (!c) return set_err(nullptr, SWAM_E_INVALID, "ctx is NULL");
+  if (d_latent < 1 || d_latent > 64) return set_err(c, SWAM_E_SHAPE, "d_latent must be in [1, 64]");
+  return sample_update(c, d_latent, v, v_cache, z, dsigma, kind);
+}
+
+int swam_sample_step(swam_ctx* c, const swam_model* model, const swam_latent_io* io, float* z,
+                     float* v, float* v_cache, void* x_full, void* y_full, const float* temb,
+                     int32_t tau, float dsigma, int32_t flags, int32_t* kind_out) {
+  if (!c) return set_err(nullptr, SWAM_E_INVALID, "ctx is NULL");
+  int rc = check_io(c, io);
+  if (rc != SWAM_OK) return rc;
+  if (!z || !v || !v_cache || !x_full || !y_full) return set_err(c, SWAM_E_INVALID, "NULL tensor");
+  if (x_full == y_full)
+    return set_err(c, SWAM_E_INVALID, "x_full must not alias y_full (its context rows are reused)");
+  int kind;
+  if ((rc = check_step(c, model, x_full, temb, tau, y_full, flags, &kind)) != SWAM_OK) return rc;
+  if ((rc = swam_embed(c, io, z, x_full)) != SWAM_OK) return rc;
+  if ((rc = enqueue_step(c, model, x_full, temb, kind, y_full)) != SWAM_OK) return rc;
+  if ((rc = swam_velocity(c, io, y_full, kind == SWAM_KIND_SPARSE, v)) != SWAM_OK) return rc;
+  if ((rc = sample_update(c, io->d_latent, v, v_cache, z, dsigma, kind)) != SWAM_OK) return rc;
   if (kind_out) *kind_out = kind;
   return SWAM_OK;
 }

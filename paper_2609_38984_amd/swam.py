@@ -21,14 +21,28 @@ STATUS = {0: "SWAM_OK", -1: "SWAM_E_INVALID", -2: "SWAM_E_SHAPE", -3: "SWAM_E_DT
 FORCE_DENSE, FORCE_REFRESH = 1, 2
 KIND_DENSE, KIND_REFRESH, KIND_SPARSE = 0, 1, 2
 TIMERS = ["ADALN", "LNMOD", "GEMM_QKV", "ATTN", "GEMM_OUT", "GEMM_UP", "GEMM_DOWN", "SCORE",
-          "REDUCE", "SELECT", "PACK", "UNPACK", "COPY"]
+          "REDUCE", "SELECT", "PACK", "UNPACK", "COPY", "SAMPLE"]
 T = {name: i for i, name in enumerate(TIMERS)}
 
 EXPORTS = ["swam_create", "swam_destroy", "swam_set_stream", "swam_plan", "swam_status_str",
            "swam_last_error", "swam_score", "swam_score_reduce", "swam_select",
            "swam_set_selection", "swam_packed_rows", "swam_export", "swam_pack", "swam_unpack",
            "swam_block", "swam_step", "swam_step_graph", "swam_graph_clear", "swam_timer_enable",
-           "swam_timer_reset", "swam_timer_read"]
+           "swam_timer_reset", "swam_timer_read", "swam_embed", "swam_velocity",
+           "swam_sample_update", "swam_sample_step"]
+
+# the flow-schedule shift of the paper's backbones (App. B.2)
+SCHEDULE_SHIFT = 5.0
+
+
+def flow_sigmas(n_steps: int, shift: float = SCHEDULE_SHIFT) -> list[float]:
+    """Host helper: sigma_i = shift s / (1 + (shift - 1) s) with s = 1 - i / N,
+    i = 0..N, the shifted flow schedule from 1 (noise) to 0."""
+    out = []
+    for i in range(n_steps + 1):
+        s = 1.0 - i / n_steps
+        out.append(shift * s / (1.0 + (shift - 1.0) * s))
+    return out
 
 
 class SwamError(RuntimeError):
@@ -72,6 +86,13 @@ class ModelStruct(C.Structure):
     _fields_ = [("n_blocks", C.c_int32), ("blocks", C.POINTER(BlockWeights))]
 
 
+LATENT_NAMES = ["w_in", "b_in", "w_v", "b_v"]
+
+
+class LatentIOStruct(C.Structure):
+    _fields_ = [("d_latent", C.c_int32)] + [(n, C.c_void_p) for n in LATENT_NAMES]
+
+
 _lib = None
 
 
@@ -102,6 +123,11 @@ def load_library(path: str = LIB_PATH):
         "swam_graph_clear": [P],
         "swam_timer_enable": [P, C.c_uint32, I32], "swam_timer_reset": [P],
         "swam_timer_read": [P, I32, C.POINTER(I64), C.POINTER(C.c_double)],
+        "swam_embed": [P, C.POINTER(LatentIOStruct), P, P],
+        "swam_velocity": [P, C.POINTER(LatentIOStruct), P, I32, P],
+        "swam_sample_update": [P, I32, P, P, P, F, I32],
+        "swam_sample_step": [P, C.POINTER(ModelStruct), C.POINTER(LatentIOStruct), P, P, P, P, P,
+                             P, I32, F, I32, C.POINTER(I32)],
     }
     for name, args in sig.items():
         fn = getattr(lib, name)
@@ -153,6 +179,16 @@ class Model:
             for n in WEIGHT_NAMES:
                 setattr(self._arr[i], n, _ptr(w[n], act_dtype, name=n))
         self.struct = ModelStruct(len(blocks), self._arr)
+
+
+class LatentIO:
+    """Device latent embedding / velocity head weights with their C descriptor."""
+
+    def __init__(self, weights: dict, act_dtype: torch.dtype):
+        self.weights = weights
+        self.d_latent = int(weights["w_in"].shape[1])
+        self.struct = LatentIOStruct(self.d_latent, *[_ptr(weights[n], act_dtype, name=n)
+                                                      for n in LATENT_NAMES])
 
 
 class Context:
@@ -308,6 +344,44 @@ class Context:
 
     def graph_clear(self):
         self._ok(self.lib.swam_graph_clear(self.h))
+
+    # -- sampling update -----------------------------------------------------------
+    def _n_lat(self):
+        c = self.c_cfg
+        return c.batch * (self.plan.l_full - c.n_ctx)
+
+    def embed(self, io: LatentIO, z, x_full):
+        n = self._n_lat() * io.d_latent
+        self._ok(self.lib.swam_embed(self.h, C.byref(io.struct), _ptr(z, torch.float32, n, "z"),
+                                     _ptr(x_full, self.act_dtype, self.rows_full * self.c_cfg.d_model,
+                                          "x_full")))
+
+    def velocity(self, io: LatentIO, y_full, v, retained_only: bool = False):
+        self._ok(self.lib.swam_velocity(
+            self.h, C.byref(io.struct),
+            _ptr(y_full, self.act_dtype, self.rows_full * self.c_cfg.d_model, "y_full"),
+            int(bool(retained_only)), _ptr(v, torch.float32, self._n_lat() * io.d_latent, "v")))
+
+    def sample_update(self, d_latent: int, v, v_cache, z, dsigma: float, kind: int):
+        n = self._n_lat() * d_latent
+        self._ok(self.lib.swam_sample_update(
+            self.h, int(d_latent), _ptr(v, torch.float32, n, "v"),
+            _ptr(v_cache, torch.float32, n, "v_cache"), _ptr(z, torch.float32, n, "z"),
+            float(dsigma), int(kind)))
+
+    def sample_step(self, model: Model, io: LatentIO, z, v, v_cache, x_full, y_full, temb,
+                    tau: int, dsigma: float, flags: int = 0) -> int:
+        c = self.c_cfg
+        n = self._n_lat() * io.d_latent
+        nt = self.rows_full * c.d_model
+        kind = C.c_int32(-1)
+        self._ok(self.lib.swam_sample_step(
+            self.h, C.byref(model.struct), C.byref(io.struct), _ptr(z, torch.float32, n, "z"),
+            _ptr(v, torch.float32, n, "v"), _ptr(v_cache, torch.float32, n, "v_cache"),
+            _ptr(x_full, self.act_dtype, nt, "x_full"), _ptr(y_full, self.act_dtype, nt, "y_full"),
+            _ptr(temb, torch.float32, c.d_temb, "temb"), int(tau), float(dsigma), int(flags),
+            C.byref(kind)))
+        return kind.value
 
     # -- timers ------------------------------------------------------------------
     def timer_enable(self, classes, capacity=8192):

@@ -28,7 +28,7 @@ def _declared():
 def test_every_declared_symbol_is_exported(lib):
     from paper_2609_38984_amd import swam
     names = _declared()
-    assert len(names) == 21
+    assert len(names) == 25
     assert sorted(swam.EXPORTS) == names
     for n in names:
         assert hasattr(lib, n), n
@@ -86,3 +86,22 @@ def test_null_context_is_rejected(lib):
     assert lib.swam_pack(None, None, None) == -1
     assert lib.swam_step(None, None, None, None, 0, None, 0, None) == -1
     assert lib.swam_destroy(None) == 0
+
+
+def test_sampler_entry_points_reject_bad_arguments_without_a_gpu(lib):
+    # NULL context and a latent io outside the supported channel range are
+    # rejected on the host before any HIP call
+    from paper_2609_38984_amd import swam
+    io = swam.LatentIOStruct(0, None, None, None, None)
+    assert lib.swam_embed(None, C.byref(io), None, None) == -1
+    assert lib.swam_velocity(None, C.byref(io), None, 0, None) == -1
+    assert lib.swam_sample_update(None, 16, None, None, None, 0.1, 1) == -1
+    assert lib.swam_sample_step(None, None, C.byref(io), None, None, None, None, None, None, 0,
+                                0.1, 0, None) == -1
+
+
+def test_flow_sigmas_host_helper():
+    from paper_2609_38984_amd import swam
+    s = swam.flow_sigmas(4)
+    assert s[0] == 1.0 and s[-1] == 0.0
+    assert abs(s[2] - 5.0 / 6.0) < 1e-15 and all(a > b for a, b in zip(s, s[1:]))
