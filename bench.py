@@ -388,6 +388,61 @@ def sweep(args):
          tembs)
 
 
+def sampler_bench(args):
+    """Closed-loop sampling (embed -> step -> velocity -> cached-velocity merge
+    and Euler update) over the workload's schedule: time per sampling step,
+    the share of the sampler kernels, and the same with the plain step.
+    One JSON line (not the default line)."""
+    import torch
+    import workload as W
+    from paper_2609_38984_amd import swam
+    cfg = workload_from_args(args)
+    dev = torch.device("cuda:0")
+    adt = torch.bfloat16 if cfg.dtype == "bf16" else torch.float32
+    c = args.d_latent
+    blocks_np, model = load_model(cfg, dev, adt)
+    wio = W.latent_io_weights(cfg, c)
+    io = swam.LatentIO({k: torch.from_numpy(v).to(dev, adt) for k, v in wio.items()}, adt)
+    si = W.make_sampler_inputs(cfg, c)
+    n_lat = cfg.batch * (cfg.l_full - cfg.n_ctx)
+    x = torch.zeros(cfg.batch * cfg.l_full, cfg.d_model, dtype=adt, device=dev)
+    for b in range(cfg.batch):
+        x[b * cfg.l_full:b * cfg.l_full + cfg.n_ctx] = torch.from_numpy(si.ctx[b]).to(dev, adt)
+    y = torch.empty_like(x)
+    z0 = torch.from_numpy(si.z0).to(dev)
+    z, v, vc = z0.clone(), torch.zeros(n_lat, c, device=dev), torch.zeros(n_lat, c, device=dev)
+    sig = swam.flow_sigmas(cfg.n_steps)
+    tembs = [torch.from_numpy(W.time_embedding(cfg, 1000.0 * sig[t])).to(dev) for t in range(cfg.n_steps)]
+    ctx = swam.Context(cfg)
+
+    def run_all():
+        z.copy_(z0)
+        kinds = []
+        for t in range(cfg.n_steps):
+            kinds.append(ctx.sample_step(model, io, z, v, vc, x, y, tembs[t], t, sig[t + 1] - sig[t]))
+        return kinds
+
+    run_all()
+    torch.cuda.synchronize()
+    ctx.timer_enable(["SAMPLE"], capacity=1 << 12)
+    reps = max(1, args.steps // cfg.n_steps)
+    t0 = time.perf_counter()
+    for _ in range(reps):
+        kinds = run_all()
+    torch.cuda.synchronize()
+    el = time.perf_counter() - t0
+    n_sample, ms_sample = ctx.timer_read("SAMPLE")
+    ctx.timer_enable([], 1)
+    steps = reps * cfg.n_steps
+    out = {"mode": "closed-loop sampler", "workload": cfg.name, "d_latent": c,
+           "steps": steps, "ms_per_step": round(el * 1e3 / steps, 4),
+           "tokens_per_s": round(steps * cfg.batch * cfg.l_full / el, 1), "kinds": kinds,
+           "sampler_kernels_ms_per_step": round(ms_sample / steps, 4),
+           "sampler_kernels_pct_of_step": round(100.0 * ms_sample / (el * 1e3), 3),
+           "latent_tokens": n_lat, "final_z_finite": bool(torch.isfinite(z).all().item())}
+    print(json.dumps(out), flush=True)
+
+
 KERNEL_SOURCES = {"ATTN": ["k_attn.hip"], "GEMM_QKV": ["k_gemm.hip"], "GEMM_OUT": ["k_gemm.hip"],
                   "GEMM_UP": ["k_gemm.hip"], "GEMM_DOWN": ["k_gemm.hip"], "SCORE": ["k_score.hip"],
                   "PACK": ["k_select.hip"], "UNPACK": ["k_select.hip"]}
@@ -560,6 +615,9 @@ def main():
     ap.add_argument("--sweep-reps", type=int, default=5, help="the same, per sweep workload")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--sweep", action="store_true", help="markdown table over all workloads")
+    ap.add_argument("--sampler", action="store_true",
+                    help="closed-loop sampling with the cached-velocity merge (own JSON line)")
+    ap.add_argument("--d-latent", type=int, default=16, help="latent channels for --sampler")
     args = ap.parse_args()
     if args.gpus != 1:
         print(json.dumps({"error": "this build runs on one GPU only: the step is single-GPU "
@@ -570,6 +628,9 @@ def main():
     torch.cuda.set_device(0)
     if args.sweep:
         sweep(args)
+        return
+    if args.sampler:
+        sampler_bench(args)
         return
     cfg = workload_from_args(args)
     dev = torch.device("cuda:0")

@@ -288,8 +288,9 @@ int swam_graph_clear(swam_ctx* ctx);
 /* ------------------------------------------ sampling update (Sec. 4.2) */
 
 /* Latent read-in and read-out of the backbone (c = d_latent channels per
- * token, 1..64; matrices [out_features][in_features] row-major in the config
- * dtype).  Latent tensors -- z, velocities v, the velocity cache -- are float
+ * token, 1..64, with c * d_model * element size <= 64 KB; matrices
+ * [out_features][in_features] row-major in the config dtype; weights, z,
+ * x_full and y_full 16-byte aligned, else SWAM_E_INVALID).  Latent tensors -- z, velocities v, the velocity cache -- are float
  * [B][L_lat][c] with L_lat = F*N_s + H: the future tokens of each sequence
  * (frame-major, row-major in a frame) followed by its action tokens, i.e. the
  * full-layout rows n_ctx .. l_full-1 of every sequence. */

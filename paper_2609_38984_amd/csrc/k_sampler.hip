@@ -14,8 +14,27 @@
 
 namespace swam {
 
-// one thread per (latent row, 8 token columns): 16-byte stores of x
+// 8 consecutive elements of a T row as fp32 (one 16-byte load for bf16)
 template <typename T>
+__device__ __forceinline__ void load8(const T* p, float (&o)[8]) {
+  if constexpr (sizeof(T) == 2) {
+    const uint4 u = *reinterpret_cast<const uint4*>(p);
+    const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      o[2 * e] = __uint_as_float(w[e] << 16);
+      o[2 * e + 1] = __uint_as_float(w[e] & 0xFFFF0000u);
+    }
+  } else {
+    const float4 a = reinterpret_cast<const float4*>(p)[0], b = reinterpret_cast<const float4*>(p)[1];
+    o[0] = a.x; o[1] = a.y; o[2] = a.z; o[3] = a.w; o[4] = b.x; o[5] = b.y; o[6] = b.z; o[7] = b.w;
+  }
+}
+
+// one thread per (latent row, 8 token columns): each output column reads its
+// W_in row (c contiguous values) in 16-byte pieces; 16-byte stores of x.
+// Needs c % 8 == 0 (the launcher falls back to scalar weight loads otherwise).
+template <typename T, bool VEC>
 __global__ void __launch_bounds__(256)
 embed_kernel(const float* __restrict__ z, const T* __restrict__ w_in, const T* __restrict__ b_in,
              T* __restrict__ x, int64_t n_lat_rows, int l_lat, int l_full, int n_ctx, int c, int d) {
@@ -30,13 +49,30 @@ embed_kernel(const float* __restrict__ z, const T* __restrict__ w_in, const T* _
   float acc[8];
 #pragma unroll
   for (int e = 0; e < 8; ++e) acc[e] = 0.0f;
-  for (int k = 0; k < c; ++k) {
-    const float zk = zr[k];
+  if constexpr (VEC) {
+    for (int k0 = 0; k0 < c; k0 += 8) {
+      const float4 za = *reinterpret_cast<const float4*>(zr + k0);
+      const float4 zb = *reinterpret_cast<const float4*>(zr + k0 + 4);
+      const float zk[8] = {za.x, za.y, za.z, za.w, zb.x, zb.y, zb.z, zb.w};
 #pragma unroll
-    for (int e = 0; e < 8; ++e) acc[e] = fmaf(zk, Elem<T>::load(w_in + (int64_t)(col + e) * c + k), acc[e]);
+      for (int e = 0; e < 8; ++e) {
+        float w[8];
+        load8(w_in + (int64_t)(col + e) * c + k0, w);
+#pragma unroll
+        for (int q = 0; q < 8; ++q) acc[e] = fmaf(zk[q], w[q], acc[e]);
+      }
+    }
+  } else {
+    for (int k = 0; k < c; ++k) {
+      const float zk = zr[k];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) acc[e] = fmaf(zk, Elem<T>::load(w_in + (int64_t)(col + e) * c + k), acc[e]);
+    }
   }
+  float bb[8];
+  load8(b_in + col, bb);
 #pragma unroll
-  for (int e = 0; e < 8; ++e) acc[e] += Elem<T>::load(b_in + col + e);
+  for (int e = 0; e < 8; ++e) acc[e] += bb[e];
   T* xo = x + row * d + col;
   if constexpr (sizeof(T) == 2) {
     *reinterpret_cast<uint4*>(xo) = make_uint4(pack_bf16x2(acc[0], acc[1]), pack_bf16x2(acc[2], acc[3]),
@@ -47,51 +83,150 @@ embed_kernel(const float* __restrict__ z, const T* __restrict__ w_in, const T* _
   }
 }
 
-// one wave per latent row; C = compile-time bound on the latent channels
+// c in {8, 16}: each thread keeps the W_in rows of its 8 columns in registers
+// and walks EMB_ROWS consecutive latent rows (the weights are read once per
+// thread instead of once per row; the z row is the same address across the
+// wave and 64 lanes store one contiguous kilobyte of x per row).
+constexpr int EMB_ROWS = 32;
+template <typename T, int C>
+__global__ void __launch_bounds__(256)
+embed_reg_kernel(const float* __restrict__ z, const T* __restrict__ w_in, const T* __restrict__ b_in,
+                 T* __restrict__ x, int64_t n_lat_rows, int l_lat, int l_full, int n_ctx, int d) {
+  const int64_t id = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int chunks = d / 8;
+  const int64_t groups = (n_lat_rows + EMB_ROWS - 1) / EMB_ROWS;
+  if (id >= groups * chunks) return;
+  const int col = (int)(id % chunks) * 8;
+  const int64_t i0 = (id / chunks) * EMB_ROWS;
+  float w[8][C], bb[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e)
+#pragma unroll
+    for (int k0 = 0; k0 < C; k0 += 8) {
+      float t[8];
+      load8(w_in + (int64_t)(col + e) * C + k0, t);
+#pragma unroll
+      for (int q = 0; q < 8; ++q) w[e][k0 + q] = t[q];
+    }
+  load8(b_in + col, bb);
+  const int64_t i1 = i0 + EMB_ROWS < n_lat_rows ? i0 + EMB_ROWS : n_lat_rows;
+  for (int64_t i = i0; i < i1; ++i) {
+    const int64_t b = i / l_lat;
+    const int64_t row = b * l_full + n_ctx + (i - b * l_lat);
+    float zk[C];
+#pragma unroll
+    for (int k0 = 0; k0 < C; k0 += 4) {
+      const float4 t = *reinterpret_cast<const float4*>(z + i * C + k0);
+      zk[k0] = t.x; zk[k0 + 1] = t.y; zk[k0 + 2] = t.z; zk[k0 + 3] = t.w;
+    }
+    float acc[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      acc[e] = 0.0f;
+#pragma unroll
+      for (int k = 0; k < C; ++k) acc[e] = fmaf(zk[k], w[e][k], acc[e]);
+      acc[e] += bb[e];
+    }
+    T* xo = x + row * d + col;
+    if constexpr (sizeof(T) == 2) {
+      *reinterpret_cast<uint4*>(xo) = make_uint4(pack_bf16x2(acc[0], acc[1]), pack_bf16x2(acc[2], acc[3]),
+                                                 pack_bf16x2(acc[4], acc[5]), pack_bf16x2(acc[6], acc[7]));
+    } else {
+      reinterpret_cast<float4*>(xo)[0] = make_float4(acc[0], acc[1], acc[2], acc[3]);
+      reinterpret_cast<float4*>(xo)[1] = make_float4(acc[4], acc[5], acc[6], acc[7]);
+    }
+  }
+}
+
+// one wave per latent row: each lane holds 8-element pieces of the row
+// (16-byte loads, kept in registers across the mean, variance and head
+// passes) and reads the matching 16-byte pieces of every W_v row.
+constexpr int VEL_MAXP = 8;          // pieces per lane: d <= 64 * 8 * 8 = 4096
+constexpr int VEL_LDS = 4096;        // uint4 slots: W_v staged in LDS when c * d * sizeof(T) <= 64 KB
 template <typename T, int C>
 __global__ void __launch_bounds__(256)
 velocity_kernel(const T* __restrict__ y, const int32_t* __restrict__ gather, int64_t n_items,
                 const T* __restrict__ w_v, const T* __restrict__ b_v, float* __restrict__ v,
                 int l_lat, int l_full, int n_ctx, int c, int d) {
+  __shared__ uint4 wl[VEL_LDS];
   const int lane = threadIdx.x & 63;
-  const int64_t item = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (item >= n_items) return;
-  // items are latent rows (gather == NULL) or packed rows of the cached selection
-  int64_t row, lat;
-  if (gather == nullptr) {
-    const int64_t b = item / l_lat;
-    lat = item;
-    row = b * l_full + n_ctx + (item - b * l_lat);
-  } else {
-    row = gather[item];
-    const int64_t b = row / l_full, in_seq = row - b * l_full;
-    if (in_seq < n_ctx) return;                    // context rows carry no latent
-    lat = b * l_lat + (in_seq - n_ctx);
-  }
-  const T* yr = y + row * d;
-  float s = 0.0f;
-  for (int k = lane; k < d; k += 64) s += Elem<T>::load(yr + k);
-  const float mean = warp_sum(s) / (float)d;
-  float q = 0.0f;
-  for (int k = lane; k < d; k += 64) {
-    const float t = Elem<T>::load(yr + k) - mean;
-    q = fmaf(t, t, q);
-  }
-  const float rstd = rsqrtf(warp_sum(q) / (float)d + 1e-6f);
-  float acc[C];
+  // the whole head matrix into LDS once per workgroup (the launcher checks the size)
+  const int n16 = c * d * (int)sizeof(T) / 16;
+  for (int t = threadIdx.x; t < n16; t += blockDim.x) wl[t] = reinterpret_cast<const uint4*>(w_v)[t];
+  __syncthreads();
+  const T* wv = reinterpret_cast<const T*>(wl);
+  const int np = (d + 511) / 512;                    // 8-element pieces per lane (uniform)
+  const int items = (int)n_items;
+  for (int item = blockIdx.x * 4 + (threadIdx.x >> 6); item < items; item += gridDim.x * 4) {
+    // items are latent rows (gather == NULL) or packed rows of the cached selection
+    int row, lat;
+    if (gather == nullptr) {
+      const int b = item / l_lat;
+      lat = item;
+      row = b * l_full + n_ctx + (item - b * l_lat);
+    } else {
+      row = gather[item];
+      const int b = row / l_full, in_seq = row - b * l_full;
+      if (in_seq < n_ctx) continue;                  // context rows carry no latent
+      lat = b * l_lat + (in_seq - n_ctx);
+    }
+    const T* yr = y + (int64_t)row * d;
+    float h[VEL_MAXP][8];
+    float s = 0.0f;
 #pragma unroll
-  for (int j = 0; j < C; ++j) acc[j] = 0.0f;
-  for (int k = lane; k < d; k += 64) {
-    const float h = (Elem<T>::load(yr + k) - mean) * rstd;
+    for (int p = 0; p < VEL_MAXP; ++p) {
+      if (p < np) {
+        const int k0 = 8 * lane + 512 * p;
+        if (k0 < d) {
+          load8(yr + k0, h[p]);
+        } else {
 #pragma unroll
-    for (int j = 0; j < C; ++j)
-      if (j < c) acc[j] = fmaf(h, Elem<T>::load(w_v + (int64_t)j * d + k), acc[j]);
-  }
+          for (int e = 0; e < 8; ++e) h[p][e] = 0.0f;
+        }
 #pragma unroll
-  for (int j = 0; j < C; ++j) {
-    if (j >= c) break;
-    const float t = warp_sum(acc[j]);
-    if (lane == 0) v[lat * c + j] = t + Elem<T>::load(b_v + j);
+        for (int e = 0; e < 8; ++e) s += h[p][e];
+      }
+    }
+    const float mean = warp_sum(s) / (float)d;
+    float q = 0.0f;
+#pragma unroll
+    for (int p = 0; p < VEL_MAXP; ++p) {
+      if (p < np) {
+        const bool live = 8 * lane + 512 * p < d;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          h[p][e] = live ? h[p][e] - mean : 0.0f;
+          q = fmaf(h[p][e], h[p][e], q);
+        }
+      }
+    }
+    const float rstd = rsqrtf(warp_sum(q) / (float)d + 1e-6f);
+    float acc[C];
+#pragma unroll
+    for (int j = 0; j < C; ++j) acc[j] = 0.0f;
+#pragma unroll
+    for (int p = 0; p < VEL_MAXP; ++p) {
+      if (p < np) {
+        // lanes past the end of the row read a valid piece of W_v and multiply it by 0
+        const int k0 = min(8 * lane + 512 * p, d - 8);
+#pragma unroll
+        for (int j = 0; j < C; ++j) {
+          if (j < c) {
+            float w[8];
+            load8(wv + j * d + k0, w);
+#pragma unroll
+            for (int e = 0; e < 8; ++e) acc[j] = fmaf(h[p][e], w[e], acc[j]);
+          }
+        }
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < C; ++j) {
+      if (j < c) {
+        const float t = warp_sum(acc[j]) * rstd;
+        if (lane == 0) v[(int64_t)lat * c + j] = t + Elem<T>::load(b_v + j);
+      }
+    }
   }
 }
 
@@ -119,12 +254,30 @@ hipError_t launch_embed(int dtype, const float* z, const void* w_in, const void*
   if (n_lat_rows <= 0) return hipSuccess;
   const int64_t n = n_lat_rows * (d / 8);
   const dim3 grid((unsigned)((n + 255) / 256));
-  if (dtype == 1)
-    hipLaunchKernelGGL(embed_kernel<bf16_t>, grid, dim3(256), 0, st, z, (const bf16_t*)w_in,
-                       (const bf16_t*)b_in, (bf16_t*)x, n_lat_rows, l_lat, l_full, n_ctx, c, d);
-  else
-    hipLaunchKernelGGL(embed_kernel<float>, grid, dim3(256), 0, st, z, (const float*)w_in,
-                       (const float*)b_in, (float*)x, n_lat_rows, l_lat, l_full, n_ctx, c, d);
+  if (c == 8 || c == 16) {
+    const int64_t groups = (n_lat_rows + EMB_ROWS - 1) / EMB_ROWS;
+    const dim3 g2((unsigned)((groups * (d / 8) + 255) / 256));
+#define SWAM_EMBR(T_, C_)                                                                      \
+  hipLaunchKernelGGL((embed_reg_kernel<T_, C_>), g2, dim3(256), 0, st, z, (const T_*)w_in,     \
+                     (const T_*)b_in, (T_*)x, n_lat_rows, l_lat, l_full, n_ctx, d)
+    if (dtype == 1) {
+      if (c == 8) SWAM_EMBR(bf16_t, 8); else SWAM_EMBR(bf16_t, 16);
+    } else {
+      if (c == 8) SWAM_EMBR(float, 8); else SWAM_EMBR(float, 16);
+    }
+#undef SWAM_EMBR
+    return hipGetLastError();
+  }
+  const bool vec = c % 8 == 0;
+#define SWAM_EMB(T_, V_)                                                                       \
+  hipLaunchKernelGGL((embed_kernel<T_, V_>), grid, dim3(256), 0, st, z, (const T_*)w_in,       \
+                     (const T_*)b_in, (T_*)x, n_lat_rows, l_lat, l_full, n_ctx, c, d)
+  if (dtype == 1) {
+    if (vec) SWAM_EMB(bf16_t, true); else SWAM_EMB(bf16_t, false);
+  } else {
+    if (vec) SWAM_EMB(float, true); else SWAM_EMB(float, false);
+  }
+#undef SWAM_EMB
   return hipGetLastError();
 }
 
@@ -132,7 +285,10 @@ template <typename T>
 static hipError_t velocity_c(const void* y, const int32_t* gather, int64_t n_items, const void* w_v,
                              const void* b_v, float* v, int l_lat, int l_full, int n_ctx, int c,
                              int d, hipStream_t st) {
-  const dim3 grid((unsigned)((n_items + 3) / 4));
+  if ((int64_t)c * d * (int64_t)sizeof(T) > (int64_t)VEL_LDS * 16 || d > 64 * 8 * VEL_MAXP)
+    return hipErrorInvalidValue;                     // checked at the API: c * d * esz <= 64 KB
+  const int64_t wgs = (n_items + 3) / 4;
+  const dim3 grid((unsigned)(wgs < 1024 ? wgs : 1024));
 #define SWAM_VEL(CB)                                                                              \
   hipLaunchKernelGGL((velocity_kernel<T, CB>), grid, dim3(256), 0, st, (const T*)y, gather,      \
                      n_items, (const T*)w_v, (const T*)b_v, v, l_lat, l_full, n_ctx, c, d)

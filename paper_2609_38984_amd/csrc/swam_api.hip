@@ -757,12 +757,19 @@ int swam_step(swam_ctx* c, const swam_model* model, const void* x_full, const fl
 
 // ------------------------------------------------------------- sampler
 
+static bool aligned16(const void* p) { return ((uintptr_t)p & 15) == 0; }
+
 static int check_io(swam_ctx* c, const swam_latent_io* io) {
   if (!io) return set_err(c, SWAM_E_INVALID, "latent io is NULL");
   if (io->d_latent < 1 || io->d_latent > 64)
     return set_err(c, SWAM_E_SHAPE, "d_latent must be in [1, 64]");
   if (!io->w_in || !io->b_in || !io->w_v || !io->b_v)
     return set_err(c, SWAM_E_INVALID, "NULL latent io weight");
+  if (!aligned16(io->w_in) || !aligned16(io->b_in) || !aligned16(io->w_v) || !aligned16(io->b_v))
+    return set_err(c, SWAM_E_INVALID, "latent io weights must be 16-byte aligned");
+  // the velocity head is staged in LDS: 64 KB at most
+  if ((int64_t)io->d_latent * c->dv.d * c->dv.esz > 65536)
+    return set_err(c, SWAM_E_SHAPE, "d_latent * d_model * element size must be <= 64 KB");
   return SWAM_OK;
 }
 
@@ -771,6 +778,7 @@ int swam_embed(swam_ctx* c, const swam_latent_io* io, const float* z, void* x_fu
   int rc = check_io(c, io);
   if (rc != SWAM_OK) return rc;
   if (!z || !x_full) return set_err(c, SWAM_E_INVALID, "NULL tensor");
+  if (!aligned16(z) || !aligned16(x_full)) return set_err(c, SWAM_E_INVALID, "tensors must be 16-byte aligned");
   const swam_config& cf = c->cfg;
   const int l_lat = (int)(c->dv.l_full - cf.n_ctx);
   Timed t(c, SWAM_T_SAMPLE);
@@ -786,6 +794,7 @@ int swam_velocity(swam_ctx* c, const swam_latent_io* io, const void* y_full, int
   int rc = check_io(c, io);
   if (rc != SWAM_OK) return rc;
   if (!y_full || !v) return set_err(c, SWAM_E_INVALID, "NULL tensor");
+  if (!aligned16(y_full)) return set_err(c, SWAM_E_INVALID, "tensors must be 16-byte aligned");
   if (retained_only && !c->sel_valid) return set_err(c, SWAM_E_STATE, "no selection cached");
   const swam_config& cf = c->cfg;
   const int l_lat = (int)(c->dv.l_full - cf.n_ctx);
