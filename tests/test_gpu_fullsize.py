@@ -230,3 +230,53 @@ def test_ragged_mass_threshold_step_fullsize():
     pruned = torch.from_numpy(pp.cpu().numpy() < 0)
     assert torch.equal(y1.cpu()[pruned].view(torch.int16), x1.cpu()[pruned].view(torch.int16))
     assert np.isfinite(host(y1)).all()
+
+
+def test_closed_loop_sampler_wam_fullsize_properties():
+    """Closed-loop sampling at the 10,160-token d=1536 shape for one refresh
+    and one sparse step: pruned future latents move by exactly dsigma times
+    the cached velocity, retained and action latents by the read-out of the
+    current output (checked against the oracle read-out on sampled rows)."""
+    from oracle import sampler_oracle as SO
+    from paper_2609_38984_amd import swam
+    cfg = W.preset(3)
+    print("sampler fullsize", flush=True)
+    blocks, dblocks, model = model_for(cfg)
+    wio = W.latent_io_weights(cfg)
+    io = swam.LatentIO({k: dev(v, torch.bfloat16) for k, v in wio.items()}, torch.bfloat16)
+    si = W.make_sampler_inputs(cfg)
+    ctx = swam.Context(cfg)
+    n_lat = cfg.batch * (cfg.l_full - cfg.n_ctx)
+    z = dev(si.z0)
+    v, vc = torch.zeros_like(z), torch.zeros_like(z)
+    x = torch.zeros(cfg.batch * cfg.l_full, cfg.d_model, dtype=torch.bfloat16, device="cuda:0")
+    x[:cfg.n_ctx] = dev(si.ctx[0], torch.bfloat16)
+    y = torch.empty_like(x)
+    sig = swam.flow_sigmas(cfg.n_steps)
+    rows = SO.latent_rows(cfg)
+    fut = np.arange(cfg.l_full - cfg.n_ctx) < cfg.n_fut
+    rng = np.random.default_rng(0)
+    pack_pos = torch.empty(cfg.l_full, dtype=torch.int32, device="cuda:0")
+    for tau in range(2):
+        z0, c0 = host(z), host(vc)
+        kind = ctx.sample_step(model, io, z, v, vc, x, y,
+                               dev(W.time_embedding(cfg, 1000.0 * sig[tau])), tau,
+                               sig[tau + 1] - sig[tau])
+        ctx.export(pack_pos=pack_pos)
+        torch.cuda.synchronize()
+        dsig = float(np.float32(sig[tau + 1] - sig[tau]))
+        z1, vn = host(z), host(v)
+        keep = (host(pack_pos)[rows] >= 0) | ~fut
+        assert kind == (swam.KIND_REFRESH if tau == 0 else swam.KIND_SPARSE)
+        if kind == swam.KIND_SPARSE:
+            pruned = ~keep
+            np.testing.assert_allclose(z1[pruned], SO.euler_update(z0[pruned], c0[pruned], dsig),
+                                       rtol=1.2e-7, atol=1e-30)
+            live = np.nonzero(keep)[0]
+        else:
+            live = np.arange(n_lat)
+        pick = rng.choice(live, 64, replace=False)
+        ref = SO.velocity(host(y)[rows[pick]], wio["w_v"], wio["b_v"])
+        assert maxrel(vn[pick], ref) < 1e-4
+        np.testing.assert_allclose(z1[pick], SO.euler_update(z0[pick], vn[pick], dsig),
+                                   rtol=1.2e-7, atol=1e-30)
