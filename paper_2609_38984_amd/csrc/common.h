@@ -124,6 +124,7 @@ struct ReduceArgs {
   double* qd;          // ws [B][L] float64 quality
   float* v;            // [B][F][N_s]
   float* a;            // [B][N_s]
+  double* vall;        // ws [B][F][N_s] float64 V_all
   int B, L, F, n_s, k_layer;
   float cv_penalty;
 };

@@ -173,48 +173,58 @@ reduce_layers(const double* __restrict__ fsum, const double* __restrict__ fent, 
   }
 }
 
-// one thread per (b, j): V over core layers, V_all over all layers, anchor key
+// one thread per (b, f, j): V over the core layers and V_all over all layers
+// (float64 sums in layer order; V stored as float32, V_all kept in float64)
 __global__ void __launch_bounds__(256)
 reduce_positions(const float* __restrict__ s_all, const double* __restrict__ qd,
                  const int32_t* __restrict__ core, const double* __restrict__ dens, int L,
-                 int F, int n_s, int k_eff, float cv, float* __restrict__ v_out,
-                 float* __restrict__ a_out) {
-  const int b = blockIdx.y;
+                 int F, int n_s, int k_eff, float* __restrict__ v_out,
+                 double* __restrict__ vall) {
+  const int bf = blockIdx.y;                 // b * F + f
+  const int b = bf / F, f = bf - b * F;
   const int j = blockIdx.x * 256 + threadIdx.x;
   if (j >= n_s) return;
   const double dc = dens[2 * b], da = dens[2 * b + 1];
-  const float* sb = s_all + (int64_t)b * L * F * n_s;
+  const float* sb = s_all + (int64_t)b * L * F * n_s + (int64_t)f * n_s + j;
+  const int64_t ls = (int64_t)F * n_s;       // layer stride
   const double* q = qd + (int64_t)b * L;
   const int32_t* cl = core + b * k_eff;
-  auto vall = [&](int f) {
-    double acc = 0.0;
-    if (da != 0.0) {
-      for (int l = 0; l < L; ++l) acc += q[l] * (double)sb[((int64_t)l * F + f) * n_s + j];
-      return acc / da;
+  double acc = 0.0;
+  if (dc != 0.0) {
+    for (int c = 0; c < k_eff; ++c) {
+      const int l = cl[c];
+      acc += q[l] * (double)sb[l * ls];
     }
-    for (int l = 0; l < L; ++l) acc += (double)sb[((int64_t)l * F + f) * n_s + j];
-    return acc / L;
-  };
-  double mu = 0.0;
-  for (int f = 0; f < F; ++f) {
-    double acc = 0.0;
-    if (dc != 0.0) {
-      for (int c = 0; c < k_eff; ++c) {
-        const int l = cl[c];
-        acc += q[l] * (double)sb[((int64_t)l * F + f) * n_s + j];
-      }
-      acc /= dc;
-    } else {
-      for (int c = 0; c < k_eff; ++c) acc += (double)sb[((int64_t)cl[c] * F + f) * n_s + j];
-      acc /= k_eff;
-    }
-    v_out[((int64_t)b * F + f) * n_s + j] = (float)acc;
-    mu += vall(f);
+    acc /= dc;
+  } else {
+    for (int c = 0; c < k_eff; ++c) acc += (double)sb[cl[c] * ls];
+    acc /= k_eff;
   }
+  v_out[(int64_t)bf * n_s + j] = (float)acc;
+  double all = 0.0;
+  if (da != 0.0) {
+    for (int l = 0; l < L; ++l) all += q[l] * (double)sb[l * ls];
+    all /= da;
+  } else {
+    for (int l = 0; l < L; ++l) all += (double)sb[l * ls];
+    all /= L;
+  }
+  vall[(int64_t)bf * n_s + j] = all;
+}
+
+// one thread per (b, j): mean and population std of V_all over frames, anchor key
+__global__ void __launch_bounds__(256)
+reduce_anchor(const double* __restrict__ vall, int F, int n_s, float cv, float* __restrict__ a_out) {
+  const int b = blockIdx.y;
+  const int j = blockIdx.x * 256 + threadIdx.x;
+  if (j >= n_s) return;
+  const double* vb = vall + (int64_t)b * F * n_s + j;
+  double mu = 0.0;
+  for (int f = 0; f < F; ++f) mu += vb[(int64_t)f * n_s];
   mu /= F;
   double var = 0.0;
   for (int f = 0; f < F; ++f) {
-    const double dv = vall(f) - mu;
+    const double dv = vb[(int64_t)f * n_s] - mu;
     var += dv * dv;
   }
   const double sd = sqrt(var / F);
@@ -232,9 +242,12 @@ hipError_t launch_score_reduce(const ReduceArgs& a, hipStream_t st) {
                      a.F, a.n_s, k_eff, a.q, a.qd, a.core, dens);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(reduce_positions, dim3((a.n_s + 255) / 256, a.B), dim3(256), 0, st,
-                     a.s_all, a.qd, a.core, dens, a.L, a.F, a.n_s, k_eff, a.cv_penalty, a.v,
-                     a.a);
+  hipLaunchKernelGGL(reduce_positions, dim3((a.n_s + 255) / 256, a.B * a.F), dim3(256), 0, st,
+                     a.s_all, a.qd, a.core, dens, a.L, a.F, a.n_s, k_eff, a.v, a.vall);
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(reduce_anchor, dim3((a.n_s + 255) / 256, a.B), dim3(256), 0, st, a.vall,
+                     a.F, a.n_s, a.cv_penalty, a.a);
   return hipGetLastError();
 }
 

@@ -29,8 +29,8 @@ struct Derived {
 
 // workspace layout (offsets into one arena)
 struct Layout {
-  size_t qkv, h, o, u, xp, lse, mod, alpha, lse_act, lse_part, s_all, q, qd, core, v, a, fsum,
-      fent, pool, corefl, keep_idx, keep_cnt, keep, pack_pos, gather, cu_packed, cu_dense, total;
+  size_t qkv, h, o, u, xp, lse, mod, alpha, lse_act, lse_part, s_all, q, qd, core, v, a, vall,
+      fsum, fent, pool, corefl, keep_idx, keep_cnt, keep, pack_pos, gather, cu_packed, cu_dense, total;
 };
 
 size_t align_up(size_t x) { return (x + 255) & ~(size_t)255; }
@@ -135,6 +135,7 @@ Layout layout_for(const swam_config* c, const Derived& dv) {
   L.core = take(B * dv.k_eff * 4);
   L.v = take(B * F * dv.n_s * 4);
   L.a = take(B * dv.n_s * 4);
+  L.vall = take(B * F * dv.n_s * 8);
   L.fsum = take((B * Lb * F + 2 * B) * 8);
   L.fent = take(B * Lb * F * 8);
   L.pool = take(B * dv.n_s);
@@ -294,6 +295,7 @@ int run_reduce(swam_ctx* c, const float* s_all) {
   r.qd = c->ptr<double>(c->lay.qd);
   r.v = c->ptr<float>(c->lay.v);
   r.a = c->ptr<float>(c->lay.a);
+  r.vall = c->ptr<double>(c->lay.vall);
   r.B = cf.batch;
   r.L = cf.n_blocks;
   r.F = cf.n_frames;
