@@ -569,8 +569,10 @@ def is_refresh(tau, reuse_R):
     return tau % reuse_R == 0
 
 
-def run_schedule(cfg, model, x_of_tau, temb_of_tau, n_steps=None):
-    """Open-loop schedule: refresh at tau mod R == 0, sparse otherwise.
+def run_schedule(cfg, model, x_of_tau, temb_of_tau, n_steps=None, refresh_at=None):
+    """Open-loop schedule: refresh at tau mod R == 0 (or at the steps listed in
+    ``refresh_at``, e.g. {0} for the paper's default of one full step per
+    action chunk; App. C.2 compares such schedules), sparse otherwise.
 
     Returns per-step outputs and the refresh results (keyed by tau)."""
     n = cfg.n_steps if n_steps is None else n_steps
@@ -578,7 +580,8 @@ def run_schedule(cfg, model, x_of_tau, temb_of_tau, n_steps=None):
     for tau in range(n):
         x = x_of_tau(tau)
         t = temb_of_tau(tau)
-        if is_refresh(tau, cfg.reuse_R):
+        full = is_refresh(tau, cfg.reuse_R) if refresh_at is None else tau in refresh_at
+        if full:
             r = refresh_step(x, model, t, cfg)
             refreshes[tau] = r
             cur = r.packmap
@@ -586,3 +589,18 @@ def run_schedule(cfg, model, x_of_tau, temb_of_tau, n_steps=None):
         else:
             ys.append(sparse_step(x, model, t, cfg, cur))
     return ys, refreshes
+
+
+# ---------------------------------------------------------------------------
+# diagnostics (App. C: cross-step and cross-frame attention overlap)
+# ---------------------------------------------------------------------------
+def overlap(P, Q):
+    """Overlap(P, Q) = sum_i min(P_i, Q_i) of two spatial distributions, each
+    non-negative map first normalised to unit mass (a map of zero mass counts
+    as all zeros, overlap 0)."""
+    P = np.asarray(P, np.float64).ravel()
+    Q = np.asarray(Q, np.float64).ravel()
+    sp, sq = P.sum(), Q.sum()
+    if sp <= 0 or sq <= 0:
+        return 0.0
+    return float(np.minimum(P / sp, Q / sq).sum())
