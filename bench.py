@@ -388,6 +388,38 @@ def sweep(args):
          tembs)
 
 
+def overlap_diagnostic(cfg, model, xs, tembs):
+    """Mean Overlap (App. C) of the frame score maps V between the first two
+    refreshes (cross-step) and between neighbouring frames of the first
+    refresh (cross-frame); untimed."""
+    import torch
+    from paper_2609_38984_amd import swam
+    if cfg.reuse_R >= cfg.n_steps:
+        return None
+    ctx = swam.Context(cfg)
+    dev = xs[0].device
+    y = torch.empty_like(xs[0])
+    F, n_s = cfg.n_frames, cfg.n_s
+    vs = []
+    for tau in range(cfg.reuse_R + 1):
+        ctx.step(model, xs[tau], tembs[tau], tau, y)
+        if tau % cfg.reuse_R == 0:
+            v = torch.empty(cfg.batch * F, n_s, dtype=torch.float32, device=dev)
+            ctx.export(v=v)
+            vs.append(v)
+    out = torch.empty(cfg.batch * F, dtype=torch.float32, device=dev)
+    ctx.overlap(vs[0], vs[1], out)
+    step = float(out.mean().item())
+    if F < 2:
+        return {"overlap_cross_step": round(step, 4)}
+    v0 = vs[0].view(cfg.batch, F, n_s)
+    p = v0[:, :-1].reshape(-1, n_s).contiguous()
+    q = v0[:, 1:].reshape(-1, n_s).contiguous()
+    out2 = torch.empty(p.shape[0], dtype=torch.float32, device=dev)
+    ctx.overlap(p, q, out2)
+    return {"overlap_cross_step": round(step, 4), "overlap_cross_frame": round(float(out2.mean().item()), 4)}
+
+
 def sampler_bench(args):
     """Closed-loop sampling (embed -> step -> velocity -> cached-velocity merge
     and Euler update) over the workload's schedule: time per sampling step,
@@ -663,6 +695,7 @@ def main():
               "speedup_schedule_vs_dense", "overhead_pct_of_dense", "overhead_pct_of_schedule_step",
               "phase_ms_per_step", "roofline"):
         out[k] = m[k]
+    out["selection_overlap"] = overlap_diagnostic(cfg, model, xs, tembs)
     if not args.no_cpu_baseline:
         log("[bench] timing the CPU oracle on a bounded sample")
         out["cpu_baseline"] = cpu_baseline(cfg, m["kinds"], blocks_np, inp)

@@ -285,6 +285,17 @@ int swam_step_graph(swam_ctx* ctx, const swam_model* model, const void* x_full,
 /* Synchronise and free every cached graph of ctx. */
 int swam_graph_clear(swam_ctx* ctx);
 
+/* --------------------------------------------------- diagnostics */
+
+/* Overlap of spatial distributions (App. C, attention-overlap eq.):
+ *   out[m] = sum_i min(p_m[i] / sum_i p_m[i], q_m[i] / sum_i q_m[i])
+ * for n_maps pairs of non-negative float maps of n values each, p and q
+ * [n_maps][n] contiguous, out float [n_maps]; a map of zero mass gives 0.
+ * Sums in float64.  E.g. cross-step overlap of V from two refreshes, or
+ * cross-frame overlap of V(f) and V(f+1). */
+int swam_overlap(swam_ctx* ctx, const float* p, const float* q, int64_t n_maps, int64_t n,
+                 float* out);
+
 /* ------------------------------------------ sampling update (Sec. 4.2) */
 
 /* Latent read-in and read-out of the backbone (c = d_latent channels per

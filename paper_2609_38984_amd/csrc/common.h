@@ -158,6 +158,9 @@ hipError_t launch_unpack_scatter(const void* y_packed, void* y_full, const int32
 hipError_t launch_unpack_merge(const void* y_packed, const void* x_full, void* y_full,
                                const int32_t* pack_pos, int64_t rows, int64_t row_bytes,
                                hipStream_t st);
+hipError_t launch_overlap(const float* p, const float* q, int64_t n_maps, int64_t n,
+                          float* out, hipStream_t st);
+
 // sampling update (k_sampler.hip)
 hipError_t launch_embed(int dtype, const float* z, const void* w_in, const void* b_in, void* x,
                         int64_t n_lat_rows, int l_lat, int l_full, int n_ctx, int c, int d,

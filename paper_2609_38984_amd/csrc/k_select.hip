@@ -231,6 +231,48 @@ reduce_anchor(const double* __restrict__ vall, int F, int n_s, float cv, float* 
   a_out[(int64_t)b * n_s + j] = mu != 0.0 ? (float)(mu / (1.0 + (double)cv * (sd / mu))) : 0.0f;
 }
 
+// Overlap(P, Q) = sum_i min(P_i / sum P, Q_i / sum Q) per map (App. C
+// attention-overlap eq.); one workgroup per map, float64 sums in a fixed
+// order (per-thread strided partials, then a tree over the workgroup)
+__device__ __forceinline__ double block_sum_d(double v, double* red) {
+  v = warp_sum_d(v);
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  __syncthreads();
+  if (lane == 0) red[w] = v;
+  __syncthreads();
+  double t = 0.0;
+  for (int i = 0; i < (int)(blockDim.x >> 6); ++i) t += red[i];
+  return t;
+}
+
+__global__ void __launch_bounds__(256)
+overlap_kernel(const float* __restrict__ p, const float* __restrict__ q, int64_t n,
+               float* __restrict__ out) {
+  __shared__ double red[4];
+  const float* pm = p + (int64_t)blockIdx.x * n;
+  const float* qm = q + (int64_t)blockIdx.x * n;
+  double sp = 0.0, sq = 0.0;
+  for (int64_t i = threadIdx.x; i < n; i += blockDim.x) {
+    sp += (double)pm[i];
+    sq += (double)qm[i];
+  }
+  sp = block_sum_d(sp, red);
+  sq = block_sum_d(sq, red);
+  double acc = 0.0;
+  if (sp > 0.0 && sq > 0.0)
+    for (int64_t i = threadIdx.x; i < n; i += blockDim.x)
+      acc += fmin((double)pm[i] / sp, (double)qm[i] / sq);
+  acc = block_sum_d(acc, red);
+  if (threadIdx.x == 0) out[blockIdx.x] = (float)acc;
+}
+
+hipError_t launch_overlap(const float* p, const float* q, int64_t n_maps, int64_t n,
+                          float* out, hipStream_t st) {
+  if (n_maps <= 0) return hipSuccess;
+  hipLaunchKernelGGL(overlap_kernel, dim3((unsigned)n_maps), dim3(256), 0, st, p, q, n, out);
+  return hipGetLastError();
+}
+
 hipError_t launch_score_reduce(const ReduceArgs& a, hipStream_t st) {
   hipLaunchKernelGGL(reduce_frames, dim3(a.B * a.L * a.F), dim3(256), 0, st, a.s_all, a.n_s,
                      a.frame_sum, a.frame_ent);

@@ -757,6 +757,17 @@ int swam_step(swam_ctx* c, const swam_model* model, const void* x_full, const fl
   return SWAM_OK;
 }
 
+// ---------------------------------------------------------- diagnostics
+
+int swam_overlap(swam_ctx* c, const float* p, const float* q, int64_t n_maps, int64_t n,
+                 float* out) {
+  if (!c) return set_err(nullptr, SWAM_E_INVALID, "ctx is NULL");
+  if (!p || !q || !out) return set_err(c, SWAM_E_INVALID, "NULL tensor");
+  if (n_maps < 0 || n < 1 || n_maps > (1ll << 31) - 1) return set_err(c, SWAM_E_SHAPE, "bad map count or size");
+  SWAM_HIP(c, launch_overlap(p, q, n_maps, n, out, c->st), "overlap");
+  return SWAM_OK;
+}
+
 // ------------------------------------------------------------- sampler
 
 static bool aligned16(const void* p) { return ((uintptr_t)p & 15) == 0; }

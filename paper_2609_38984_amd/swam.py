@@ -29,7 +29,7 @@ EXPORTS = ["swam_create", "swam_destroy", "swam_set_stream", "swam_plan", "swam_
            "swam_set_selection", "swam_packed_rows", "swam_export", "swam_pack", "swam_unpack",
            "swam_block", "swam_step", "swam_step_graph", "swam_graph_clear", "swam_timer_enable",
            "swam_timer_reset", "swam_timer_read", "swam_embed", "swam_velocity",
-           "swam_sample_update", "swam_sample_step"]
+           "swam_sample_update", "swam_sample_step", "swam_overlap"]
 
 # the flow-schedule shift of the paper's backbones (App. B.2)
 SCHEDULE_SHIFT = 5.0
@@ -123,6 +123,7 @@ def load_library(path: str = LIB_PATH):
         "swam_graph_clear": [P],
         "swam_timer_enable": [P, C.c_uint32, I32], "swam_timer_reset": [P],
         "swam_timer_read": [P, I32, C.POINTER(I64), C.POINTER(C.c_double)],
+        "swam_overlap": [P, P, P, I64, I64, P],
         "swam_embed": [P, C.POINTER(LatentIOStruct), P, P],
         "swam_velocity": [P, C.POINTER(LatentIOStruct), P, I32, P],
         "swam_sample_update": [P, I32, P, P, P, F, I32],
@@ -344,6 +345,14 @@ class Context:
 
     def graph_clear(self):
         self._ok(self.lib.swam_graph_clear(self.h))
+
+    # -- diagnostics ---------------------------------------------------------------
+    def overlap(self, p, q, out):
+        """out[m] = Overlap(p[m], q[m]) of normalised maps (rows of p and q)."""
+        n_maps, n = int(p.shape[0]), int(p[0].numel())
+        self._ok(self.lib.swam_overlap(self.h, _ptr(p, torch.float32, n_maps * n, "p"),
+                                       _ptr(q, torch.float32, n_maps * n, "q"), n_maps, n,
+                                       _ptr(out, torch.float32, n_maps, "out")))
 
     # -- sampling update -----------------------------------------------------------
     def _n_lat(self):
