@@ -11,5 +11,5 @@ from .swam_oracle import (  # noqa: F401
     threshold_fraction, mass_count, MASS_SCALE_BITS, select, Selection, keep_mask,
     pack_map, PackMap, pack, unpack, dense_cu, run_blocks, dense_step, layer_scores,
     selection_from_scores, refresh_step, sparse_step, is_refresh, run_schedule,
-    RefreshResult, overlap,
+    RefreshResult, overlap, rope_angles, apply_rope, qk_rms_norm, qk_post, dense_positions,
 )

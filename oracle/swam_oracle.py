@@ -125,6 +125,55 @@ def attention(q, k, v, cu_seqlens, n_heads):
     return o, lse
 
 
+ROPE_BASE = 10000.0
+
+
+def rope_angles(positions, hd=64, base=ROPE_BASE):
+    """Rotary angles pos * base^(-2i/hd) for pairs i = 0..hd/2-1, [T][hd/2]."""
+    pos = np.asarray(positions, np.float64)
+    inv = base ** (-2.0 * np.arange(hd // 2, dtype=np.float64) / hd)
+    return pos[:, None] * inv[None, :]
+
+
+def apply_rope(x, positions, n_heads):
+    """Rotary position embedding (RoFormer convention): in every head, the pair
+    (x_2i, x_2i+1) is rotated by the angle of its row's position."""
+    x = np.asarray(x, np.float64)
+    T, D = x.shape
+    hd = D // n_heads
+    ang = rope_angles(positions, hd)
+    c, s = np.cos(ang), np.sin(ang)
+    y = x.reshape(T, n_heads, hd // 2, 2)
+    a, b = y[..., 0], y[..., 1]
+    out = np.stack([a * c[:, None, :] - b * s[:, None, :], a * s[:, None, :] + b * c[:, None, :]], axis=-1)
+    return out.reshape(T, D)
+
+
+def qk_rms_norm(x, n_heads, eps=LN_EPS):
+    """RMS normalisation of every head vector, unit gain."""
+    x = np.asarray(x, np.float64)
+    T, D = x.shape
+    y = x.reshape(T, n_heads, D // n_heads)
+    return (y / np.sqrt((y * y).mean(axis=2, keepdims=True) + eps)).reshape(T, D)
+
+
+def qk_post(qkv, n_heads, positions, rope, qk_norm, st):
+    """Optional backbone variants on the stored q and k (v untouched): QK-norm,
+    then RoPE at the rows' original positions; re-stored."""
+    if not (rope or qk_norm):
+        return qkv
+    qkv = np.array(qkv, np.float64, copy=True)
+    d = qkv.shape[1] // 3
+    for sl in (slice(0, d), slice(d, 2 * d)):
+        t = qkv[:, sl]
+        if qk_norm:
+            t = qk_rms_norm(t, n_heads)
+        if rope:
+            t = apply_rope(t, positions, n_heads)
+        qkv[:, sl] = st(t)
+    return qkv
+
+
 @dataclass
 class BlockTrace:
     """Intermediate tensors of one block (as stored), for scoring and tests."""
@@ -133,7 +182,7 @@ class BlockTrace:
     x_mid: np.ndarray  # residual stream after the attention half
 
 
-def block(x, w, temb, cu_seqlens, n_heads, dtype):
+def block(x, w, temb, cu_seqlens, n_heads, dtype, positions=None, rope=False, qk_norm=False):
     """One DiT block on rows ``x`` [T][d] grouped into sequences by cu_seqlens.
 
     h  = LN(x) (1 + scale1) + shift1
@@ -144,7 +193,9 @@ def block(x, w, temb, cu_seqlens, n_heads, dtype):
     y  = x1 + gate2 * (GELU_tanh(h2 W_1^T + b_1) W_2^T + b_2)
 
     Every tensor the GPU stores (h, qkv, o, x1, h2, the GELU output, y) is
-    rounded to the storage precision; math in between is float64.
+    rounded to the storage precision; math in between is float64.  With the
+    backbone variants, q and k are QK-normed and/or rotated at ``positions``
+    (the rows' original indices in their full sequences) and stored again.
     """
     st = storage_round(dtype)
     x = np.asarray(x, np.float64)
@@ -153,6 +204,7 @@ def block(x, w, temb, cu_seqlens, n_heads, dtype):
     W = {k: np.asarray(v, np.float64) for k, v in w.items()}
     h = st(layer_norm(x) * (1.0 + sc1) + sh1)
     qkv = st(h @ W["w_qkv"].T + W["b_qkv"])
+    qkv = qk_post(qkv, n_heads, positions, rope, qk_norm, st)
     q, k, v = qkv[:, :d], qkv[:, d:2 * d], qkv[:, 2 * d:]
     o, lse = attention(q, k, v, cu_seqlens, n_heads)
     o = st(o)
@@ -163,7 +215,8 @@ def block(x, w, temb, cu_seqlens, n_heads, dtype):
     return y, BlockTrace(qkv=qkv, lse=round_f32(lse), x_mid=x1)
 
 
-def block_rows(x, w, temb, cu_seqlens, rows, n_heads, dtype):
+def block_rows(x, w, temb, cu_seqlens, rows, n_heads, dtype, positions=None, rope=False,
+               qk_norm=False):
     """The block output of selected rows only (same arithmetic as ``block``).
 
     Keys and values need every row of the sampled rows' sequences; queries,
@@ -188,9 +241,16 @@ def block_rows(x, w, temb, cu_seqlens, rows, n_heads, dtype):
             continue
         h = st(layer_norm(x[s0:s1]) * (1.0 + sc1) + sh1)
         kv = st(h @ W["w_qkv"][d:].T + W["b_qkv"][d:])
-        k, v = kv[:, :d], kv[:, d:]
         r = rows[sel]
         q = st(h[r - s0] @ W["w_qkv"][:d].T + W["b_qkv"][:d])
+        if rope or qk_norm:
+            pos = np.asarray(positions)
+            zq = np.zeros((len(r), d))
+            q = qk_post(np.concatenate([q, zq, zq], axis=1), n_heads, pos[r], rope, qk_norm, st)[:, :d]
+            zk = np.zeros((s1 - s0, d))
+            kv = np.concatenate([zk, kv], axis=1)
+            kv = qk_post(kv, n_heads, pos[s0:s1], rope, qk_norm, st)[:, d:]
+        k, v = kv[:, :d], kv[:, d:]
         o = np.zeros((len(r), d))
         for hh in range(n_heads):
             cols = slice(hh * hd, (hh + 1) * hd)
@@ -508,10 +568,18 @@ class RefreshResult:
     packmap: PackMap
 
 
-def run_blocks(x, model, temb, cu, cfg, trace_cb=None):
+def dense_positions(cfg):
+    """Original index of every full-layout row inside its sequence."""
+    return np.tile(np.arange(cfg.l_full), cfg.batch)
+
+
+def run_blocks(x, model, temb, cu, cfg, trace_cb=None, positions=None):
     y = np.asarray(x, np.float64)
+    rope, qkn = bool(getattr(cfg, "rope", 0)), bool(getattr(cfg, "qk_norm", 0))
+    if positions is None:
+        positions = dense_positions(cfg)
     for l, w in enumerate(model):
-        y, tr = block(y, w, temb, cu, cfg.n_heads, cfg.dtype)
+        y, tr = block(y, w, temb, cu, cfg.n_heads, cfg.dtype, positions, rope, qkn)
         if trace_cb is not None:
             trace_cb(l, tr)
     return y
@@ -561,7 +629,8 @@ def refresh_step(x_full, model, temb, cfg):
 def sparse_step(x_full, model, temb, cfg, pm: PackMap):
     """Blocks on the packed sequence only; pruned rows carry x_full unchanged."""
     xp = pack(x_full, pm)
-    yp = run_blocks(xp, model, temb, pm.cu_seqlens, cfg)
+    # packed rows keep the positions of their original rows (Sec. 4.2)
+    yp = run_blocks(xp, model, temb, pm.cu_seqlens, cfg, positions=pm.gather % cfg.l_full)
     return unpack(yp, x_full, pm)
 
 

@@ -67,6 +67,8 @@ class SwamConfig:
     cv_penalty: float = 1.0
     mass_threshold: float = 0.0
     retain_percent: int = 0     # informational: per-frame core percent
+    rope: int = 0               # backbone variant: rotary embedding at original positions
+    qk_norm: int = 0            # backbone variant: RMS-normalised q and k per head
 
     # derived sizes ----------------------------------------------------------
     @property
