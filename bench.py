@@ -42,10 +42,14 @@ def log(*a):
 def workload_from_args(args):
     import workload as W
     if args.config == 4:
-        return W.preset(4, percent=args.percent, reuse_R=args.reuse or 2)
-    cfg = W.preset(args.config)
+        cfg = W.preset(4, percent=args.percent, reuse_R=args.reuse or 2)
+    else:
+        cfg = W.preset(args.config)
     if args.reuse:
         cfg = cfg.replace(reuse_R=args.reuse)
+    if args.rope or args.qk_norm:
+        tag = "+rope" * args.rope + "+qknorm" * args.qk_norm
+        cfg = cfg.replace(rope=int(args.rope), qk_norm=int(args.qk_norm), name=cfg.name + tag)
     return cfg
 
 
@@ -72,11 +76,14 @@ def kernel_work(cfg, cls, rows_per_seq):
                                   + cfg.n_act * cfg.n_heads * 4 + cfg.n_fut * 4))
     if cls in ("PACK", "UNPACK"):
         return 2.0 * m * d * esz
+    if cls == "QK_POST":
+        # q and k of every row read and written once (the rotation table is L2-resident)
+        return 4.0 * m * d * esz
     raise KeyError(cls)
 
 
 BOUND = {"GEMM_QKV": "mfma", "GEMM_OUT": "mfma", "GEMM_UP": "mfma", "GEMM_DOWN": "mfma",
-         "ATTN": "mfma", "SCORE": "hbm", "PACK": "hbm", "UNPACK": "hbm"}
+         "ATTN": "mfma", "SCORE": "hbm", "PACK": "hbm", "UNPACK": "hbm", "QK_POST": "hbm"}
 
 
 def step_flops(cfg, rows):
@@ -267,6 +274,15 @@ def measure(cfg, model, xs, tembs, steps, warmup, reps):
         run(t)
     torch.cuda.synchronize()
     phase_ms = {cls: round(ctx.timer_read(cls)[1] / n_sched, 4) for cls in swam.TIMERS}
+    qk_post = None
+    if cfg.rope or cfg.qk_norm:
+        n_qk, ms_qk = ctx.timer_read("QK_POST")
+        rows = [full_rows if t % cfg.reuse_R == 0 else packed_rows for t in range(n_sched)]
+        work = sum(kernel_work(cfg, "QK_POST", r) * cfg.n_blocks for r in rows)
+        gbs = work / (ms_qk * 1e-3) / 1e9
+        qk_post = {"rope": cfg.rope, "qk_norm": cfg.qk_norm, "launches": n_qk,
+                   "ms_per_step": round(ms_qk / n_sched, 4), "achieved": round(gbs, 1),
+                   "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": round(gbs / PEAK_HBM_GBS, 4)}
     ctx.timer_enable([], 1)
     over = sum(phase_ms[c] for c in ("SCORE", "REDUCE", "SELECT", "PACK", "UNPACK"))
     tok = cfg.batch * cfg.l_full
@@ -283,7 +299,7 @@ def measure(cfg, model, xs, tembs, steps, warmup, reps):
         "speedup_schedule_vs_dense": round(t_dense / sched_ms, 3),
         "overhead_pct_of_dense": round(100.0 * over / t_dense, 3),
         "overhead_pct_of_schedule_step": round(100.0 * over / sched_ms, 3),
-        "phase_ms_per_step": phase_ms, "roofline": roofline,
+        "phase_ms_per_step": phase_ms, "roofline": roofline, "qk_post": qk_post,
     }
 
 
@@ -650,6 +666,9 @@ def main():
     ap.add_argument("--sampler", action="store_true",
                     help="closed-loop sampling with the cached-velocity merge (own JSON line)")
     ap.add_argument("--d-latent", type=int, default=16, help="latent channels for --sampler")
+    ap.add_argument("--rope", action="store_true",
+                    help="backbone variant: rotary embedding at the original positions")
+    ap.add_argument("--qk-norm", action="store_true", help="backbone variant: per-head QK-norm")
     args = ap.parse_args()
     if args.gpus != 1:
         print(json.dumps({"error": "this build runs on one GPU only: the step is single-GPU "
@@ -688,6 +707,7 @@ def main():
                    "n_ctx": cfg.n_ctx, "n_act": cfg.n_act,
                    "k_core": cfg.k_core, "k_anchor": cfg.k_anchor,
                    "mass_threshold": cfg.mass_threshold, "reuse_R": cfg.reuse_R,
+                   "rope": cfg.rope, "qk_norm": cfg.qk_norm,
                    "packed_rows": m["packed_rows"], "schedule_kinds": m["kinds"]},
     }
     for k in ("dense_step_ms", "refresh_step_ms", "sparse_step_ms", "dense_tokens_per_s",
@@ -695,6 +715,8 @@ def main():
               "speedup_schedule_vs_dense", "overhead_pct_of_dense", "overhead_pct_of_schedule_step",
               "phase_ms_per_step", "roofline"):
         out[k] = m[k]
+    if m["qk_post"] is not None:
+        out["qk_post"] = m["qk_post"]
     out["selection_overlap"] = overlap_diagnostic(cfg, model, xs, tembs)
     if not args.no_cpu_baseline:
         log("[bench] timing the CPU oracle on a bounded sample")

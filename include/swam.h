@@ -99,6 +99,14 @@ typedef struct {
                              the threshold (an extension giving ragged lengths) */
   int32_t reuse_R;        /* refresh when tau mod R == 0; >= 1 */
   int32_t dtype;          /* swam_dtype */
+  /* Backbone variants (0 = off): rope = rotary embedding of q and k at each
+   * token's original position in its full sequence (pairs (2i, 2i+1) of a
+   * head rotated by pos * 10000^(-2i/64); packed rows of a sparse step keep
+   * their original positions, Sec. 4.2); qk_norm = unit-gain RMS
+   * normalisation of every q and k head vector (eps 1e-6), applied before
+   * the rotation. */
+  int32_t rope;
+  int32_t qk_norm;
 } swam_config;
 
 /* Sizes derived from a configuration (host-only, no GPU needed). */
@@ -242,6 +250,10 @@ int swam_unpack(swam_ctx* ctx, const void* y_packed, const void* x_full, void* y
  *   o = softmax(q k^T / 8) v over the keys of the row's own sequence
  *   x += g1 (o W_o^T + b_o); h2 = LN(x)(1+sc2)+sh2
  *   x += g2 (GELU_tanh(h2 W_1^T + b_1) W_2^T + b_2)
+ * With rope / qk_norm set, q and k are normalised / rotated after the
+ * projection; a row's position is its index in its full sequence for the
+ * dense layout (cu_seqlens == NULL) and its index inside its cu_seqlens
+ * sequence otherwise (swam_step's sparse blocks use the original positions).
  * LN: biased variance, eps 1e-6, no affine.  temb: float [d_temb] (shared by
  * the batch).  cu_seqlens: device int32 [n_seqs+1] with cu[n_seqs] == n_rows,
  * or NULL for the dense layout (n_rows == B*l_full).  lse_out (optional):
@@ -352,7 +364,7 @@ int swam_sample_step(swam_ctx* ctx, const swam_model* model, const swam_latent_i
 enum {
   SWAM_T_ADALN = 0, SWAM_T_LNMOD, SWAM_T_GEMM_QKV, SWAM_T_ATTN, SWAM_T_GEMM_OUT,
   SWAM_T_GEMM_UP, SWAM_T_GEMM_DOWN, SWAM_T_SCORE, SWAM_T_REDUCE, SWAM_T_SELECT,
-  SWAM_T_PACK, SWAM_T_UNPACK, SWAM_T_COPY, SWAM_T_SAMPLE, SWAM_T_COUNT
+  SWAM_T_PACK, SWAM_T_UNPACK, SWAM_T_COPY, SWAM_T_SAMPLE, SWAM_T_QK_POST, SWAM_T_COUNT
 };
 
 /* Bracket every launch (phase) of the classes in `mask` (bit i = class i)

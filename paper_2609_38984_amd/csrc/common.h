@@ -89,6 +89,12 @@ hipError_t launch_adaln(int dtype, const AdalnArgs& a, int n_blk, const float* t
 hipError_t launch_ln_mod(int dtype, const void* x, void* h, const float* shift,
                          const float* scale, int64_t rows, int d, hipStream_t st);
 
+// backbone variants: rotary table and QK-norm / RoPE of the stored q and k
+hipError_t launch_rope_table(float2* tab, int n_pos, hipStream_t st);
+hipError_t launch_qk_post(int dtype, void* qkv, int64_t n_rows, int d, int pos_mode,
+                          const int32_t* gather, const int32_t* cu, int n_seqs, int l_full,
+                          const float2* tab, int n_pos, int qk_norm, hipStream_t st);
+
 // o = softmax(q k^T / 8) v per head inside each sequence; lse (optional).
 // Sequence bounds are clamped to [0, n_rows].
 hipError_t launch_attention(int dtype, const void* qkv, void* o, float* lse,

@@ -129,4 +129,111 @@ hipError_t launch_ln_mod(int dtype, const void* x, void* h, const float* shift,
   return hipGetLastError();
 }
 
+// ---------------------------------------------------------------------------
+// backbone variants on the stored q and k: QK-norm (unit-gain RMS per head),
+// then the rotary embedding at each row's original position
+// ---------------------------------------------------------------------------
+// [l_full][32] (cos, sin) of pos * 10000^(-2i/64), evaluated in float64
+// cos / sin of position * 10000^(-2i/64) for positions [0, n_pos), i < 32
+__global__ void rope_table_kernel(float2* __restrict__ tab, int n_pos) {
+  const int id = blockIdx.x * blockDim.x + threadIdx.x;
+  if (id >= n_pos * 32) return;
+  const int pos = id >> 5, i = id & 31;
+  const double ang = (double)pos * pow(10000.0, -2.0 * i / 64.0);
+  tab[id] = make_float2((float)cos(ang), (float)sin(ang));
+}
+
+hipError_t launch_rope_table(float2* tab, int n_pos, hipStream_t st) {
+  hipLaunchKernelGGL(rope_table_kernel, dim3((n_pos * 32 + 255) / 256), dim3(256), 0, st, tab,
+                     n_pos);
+  return hipGetLastError();
+}
+
+// one thread per 8 consecutive elements of q or k (a head is 8 threads, which
+// are 8 consecutive lanes); pos_mode 0: row % l_full, 1: gather[row] % l_full,
+// 2: row - cu[b] for the row's sequence b; positions are clamped to the
+// table's n_pos rows
+template <typename T>
+__global__ void __launch_bounds__(256)
+qk_post_kernel(T* __restrict__ qkv, int64_t n_rows, int d, int pos_mode,
+               const int32_t* __restrict__ gather, const int32_t* __restrict__ cu, int n_seqs,
+               int l_full, const float2* __restrict__ tab, int n_pos, int qk_norm) {
+  const int64_t id = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int chunks = 2 * d / 8;               // q and k columns of a row
+  const bool live = id < n_rows * chunks;
+  const int64_t row = live ? id / chunks : 0;
+  const int c8 = live ? (int)(id % chunks) * 8 : 0;
+  T* p = qkv + row * 3 * d + c8;
+  float x[8];
+  if constexpr (sizeof(T) == 2) {
+    const uint4 u = *reinterpret_cast<const uint4*>(p);
+    const uint32_t wv[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      x[2 * e] = __uint_as_float(wv[e] << 16);
+      x[2 * e + 1] = __uint_as_float(wv[e] & 0xFFFF0000u);
+    }
+  } else {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) x[e] = p[e];
+  }
+  if (qk_norm) {
+    // the 8 lanes of a head are consecutive and aligned (chunks per row and per
+    // head are multiples of 8); every lane takes part in the exchange
+    float ss = 0.0f;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) ss = fmaf(x[e], x[e], ss);
+    ss += __shfl_xor(ss, 1);
+    ss += __shfl_xor(ss, 2);
+    ss += __shfl_xor(ss, 4);
+    const float r = rsqrtf(ss / 64.0f + 1e-6f);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) x[e] *= r;
+  }
+  if (!live) return;
+  if (tab != nullptr) {
+    int pos;
+    if (pos_mode == 0) {
+      pos = (int)(row % l_full);
+    } else if (pos_mode == 1) {
+      pos = gather[row] % l_full;
+    } else {
+      int b = 0;
+      while (b + 1 < n_seqs && cu[b + 1] <= row) ++b;
+      pos = (int)(row - cu[b]);
+    }
+    pos = min(max(pos, 0), n_pos - 1);
+    const float2* t = tab + (int64_t)pos * 32 + ((c8 & 63) >> 1);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const float2 cs = t[e];
+      const float a = x[2 * e], b = x[2 * e + 1];
+      x[2 * e] = a * cs.x - b * cs.y;
+      x[2 * e + 1] = a * cs.y + b * cs.x;
+    }
+  }
+  if constexpr (sizeof(T) == 2) {
+    *reinterpret_cast<uint4*>(p) = make_uint4(pack_bf16x2(x[0], x[1]), pack_bf16x2(x[2], x[3]),
+                                              pack_bf16x2(x[4], x[5]), pack_bf16x2(x[6], x[7]));
+  } else {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) p[e] = x[e];
+  }
+}
+
+hipError_t launch_qk_post(int dtype, void* qkv, int64_t n_rows, int d, int pos_mode,
+                          const int32_t* gather, const int32_t* cu, int n_seqs, int l_full,
+                          const float2* tab, int n_pos, int qk_norm, hipStream_t st) {
+  if (n_rows <= 0) return hipSuccess;
+  const int64_t n = n_rows * (2 * d / 8);
+  const dim3 grid((unsigned)((n + 255) / 256));
+  if (dtype == 1)
+    hipLaunchKernelGGL(qk_post_kernel<bf16_t>, grid, dim3(256), 0, st, (bf16_t*)qkv, n_rows, d,
+                       pos_mode, gather, cu, n_seqs, l_full, tab, n_pos, qk_norm);
+  else
+    hipLaunchKernelGGL(qk_post_kernel<float>, grid, dim3(256), 0, st, (float*)qkv, n_rows, d,
+                       pos_mode, gather, cu, n_seqs, l_full, tab, n_pos, qk_norm);
+  return hipGetLastError();
+}
+
 }  // namespace swam

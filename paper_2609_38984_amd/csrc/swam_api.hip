@@ -29,7 +29,7 @@ struct Derived {
 
 // workspace layout (offsets into one arena)
 struct Layout {
-  size_t qkv, h, o, u, xp, lse, mod, alpha, lse_act, lse_part, s_all, q, qd, core, v, a, vall,
+  size_t qkv, h, o, u, xp, lse, mod, alpha, rope, lse_act, lse_part, s_all, q, qd, core, v, a, vall,
       fsum, fent, pool, corefl, keep_idx, keep_cnt, keep, pack_pos, gather, cu_packed, cu_dense, total;
 };
 
@@ -74,6 +74,8 @@ int derive(const swam_config* c, Derived* dv, std::string* err) {
   if (!(c->cv_penalty >= 0.0f) || !isfinite(c->cv_penalty))
     return fail(err, SWAM_E_INVALID, "cv_penalty must be finite and >= 0");
   if (c->reuse_R < 1) return fail(err, SWAM_E_INVALID, "reuse_R must be >= 1");
+  if (c->rope != 0 && c->rope != 1) return fail(err, SWAM_E_INVALID, "rope must be 0 or 1");
+  if (c->qk_norm != 0 && c->qk_norm != 1) return fail(err, SWAM_E_INVALID, "qk_norm must be 0 or 1");
   const int64_t d = c->d_model;
   if (c->dtype == SWAM_BF16 && d > 4096) return fail(err, SWAM_E_SHAPE, "bf16 d_model <= 4096");
   const int64_t l_full = c->n_ctx + (int64_t)c->n_frames * n_s + c->n_act;
@@ -127,6 +129,9 @@ Layout layout_for(const swam_config* c, const Derived& dv) {
   L.lse = take(Lb * R * c->n_heads * 4);
   L.mod = take(Lb * 6 * dv.d * 4);
   L.alpha = take(16 * 4);
+  // positions up to batch * l_full - 1: a cu_seqlens sequence of swam_block may
+  // span every row of the workspace
+  L.rope = take(c->rope ? dv.rows_full * 32 * 8 : 0);
   L.lse_act = take(B * c->n_act * c->n_heads * 4);
   L.lse_part = take(B * chunks * c->n_act * c->n_heads * 2 * 4);
   L.s_all = take(B * Lb * F * dv.n_s * 4);
@@ -225,8 +230,11 @@ bool any_null_block(const swam_block_weights* w) {
 }
 
 // one block in place on x [n_rows][d]; mod = this block's [6][d] modulation
+// pos_mode (rope only): 0 = dense layout, 1 = packed rows of the cached
+// selection (original positions), 2 = index inside the cu_seqlens sequence
 int run_block(swam_ctx* c, const swam_block_weights* w, const float* mod, void* x,
-              int64_t n_rows, const int32_t* cu, int n_seqs, float* lse_out, void* qkv) {
+              int64_t n_rows, const int32_t* cu, int n_seqs, float* lse_out, void* qkv,
+              int pos_mode) {
   const int dt = c->cfg.dtype;
   const int64_t d = c->dv.d, hid = c->dv.hidden;
   void* h = c->ptr<char>(c->lay.h);
@@ -244,6 +252,15 @@ int run_block(swam_ctx* c, const swam_block_weights* w, const float* mod, void* 
     Timed t(c, SWAM_T_GEMM_QKV);
     SWAM_HIP(c, launch_gemm(dt, EPI_BIAS, h, d, w->w_qkv, d, w->b_qkv, nullptr, qkv, 3 * d,
                             n_rows, 3 * d, d, st), "gemm qkv");
+  }
+  if (c->cfg.rope || c->cfg.qk_norm) {
+    Timed t(c, SWAM_T_QK_POST);
+    SWAM_HIP(c, launch_qk_post(dt, qkv, n_rows, (int)d, pos_mode, c->ptr<int32_t>(c->lay.gather),
+                               cu, n_seqs, (int)c->dv.l_full,
+                               c->cfg.rope ? c->ptr<float2>(c->lay.rope) : nullptr,
+                               (int)c->dv.rows_full,
+                               c->cfg.qk_norm, st),
+             "qk post");
   }
   {
     Timed t(c, SWAM_T_ATTN);
@@ -443,6 +460,10 @@ int swam_create(const swam_config* cfg, void* stream, swam_ctx** out) {
     e = hipMemcpy(c->ptr<int32_t>(c->lay.cu_dense), cu.data(), cu.size() * 4,
                   hipMemcpyHostToDevice);
   }
+  if (e == hipSuccess && cfg->rope) {
+    e = launch_rope_table(c->ptr<float2>(c->lay.rope), (int)dv.rows_full, c->st);
+    if (e == hipSuccess) e = hipStreamSynchronize(c->st);
+  }
   if (e != hipSuccess) {
     g_err = std::string("context setup: ") + hipGetErrorString(e);
     swam_destroy(c);
@@ -629,7 +650,8 @@ int swam_block(swam_ctx* c, const swam_block_weights* w, const float* temb, void
   int rc = run_adaln(c, w, 1, temb);
   if (rc != SWAM_OK) return rc;
   void* qkv = qkv_out ? qkv_out : c->ptr<char>(c->lay.qkv);
-  return run_block(c, w, c->ptr<float>(c->lay.mod), x, n_rows, cu, n_seqs, lse_out, qkv);
+  return run_block(c, w, c->ptr<float>(c->lay.mod), x, n_rows, cu, n_seqs, lse_out, qkv,
+                   cu_seqlens ? 2 : 0);
 }
 
 }  // extern "C"
@@ -674,7 +696,7 @@ int enqueue_step(swam_ctx* c, const swam_model* model, const void* x_full, const
       rc = run_block(c, &model->blocks[l], mod + (int64_t)l * 6 * d, y_full, c->dv.rows_full,
                      c->ptr<int32_t>(c->lay.cu_dense), cf.batch,
                      score ? c->ptr<float>(c->lay.lse) + l * lse_slot : nullptr,
-                     score ? (void*)((char*)qkv + l * qkv_slot) : qkv);
+                     score ? (void*)((char*)qkv + l * qkv_slot) : qkv, 0);
       if (rc != SWAM_OK) return rc;
     }
     if (score) {
@@ -717,7 +739,7 @@ int enqueue_step(swam_ctx* c, const swam_model* model, const void* x_full, const
     if ((rc = swam_pack(c, x_full, xp)) != SWAM_OK) return rc;
     for (int l = 0; l < cf.n_blocks; ++l) {
       rc = run_block(c, &model->blocks[l], mod + (int64_t)l * 6 * d, xp, c->packed_rows,
-                     c->ptr<int32_t>(c->lay.cu_packed), cf.batch, nullptr, qkv);
+                     c->ptr<int32_t>(c->lay.cu_packed), cf.batch, nullptr, qkv, 1);
       if (rc != SWAM_OK) return rc;
     }
     if ((rc = swam_unpack(c, xp, x_full, y_full)) != SWAM_OK) return rc;

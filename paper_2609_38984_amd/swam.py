@@ -21,7 +21,7 @@ STATUS = {0: "SWAM_OK", -1: "SWAM_E_INVALID", -2: "SWAM_E_SHAPE", -3: "SWAM_E_DT
 FORCE_DENSE, FORCE_REFRESH = 1, 2
 KIND_DENSE, KIND_REFRESH, KIND_SPARSE = 0, 1, 2
 TIMERS = ["ADALN", "LNMOD", "GEMM_QKV", "ATTN", "GEMM_OUT", "GEMM_UP", "GEMM_DOWN", "SCORE",
-          "REDUCE", "SELECT", "PACK", "UNPACK", "COPY", "SAMPLE"]
+          "REDUCE", "SELECT", "PACK", "UNPACK", "COPY", "SAMPLE", "QK_POST"]
 T = {name: i for i, name in enumerate(TIMERS)}
 
 EXPORTS = ["swam_create", "swam_destroy", "swam_set_stream", "swam_plan", "swam_status_str",
@@ -56,7 +56,7 @@ class Config(C.Structure):
         "batch", "d_model", "n_heads", "head_dim", "mlp_ratio", "n_blocks", "d_temb", "n_ctx",
         "n_frames", "frame_h", "frame_w", "n_act", "k_core", "k_anchor", "k_layer")] + [
         ("cv_penalty", C.c_float), ("mass_threshold", C.c_float), ("reuse_R", C.c_int32),
-        ("dtype", C.c_int32)]
+        ("dtype", C.c_int32), ("rope", C.c_int32), ("qk_norm", C.c_int32)]
 
     @classmethod
     def from_obj(cls, o) -> "Config":
@@ -65,6 +65,8 @@ class Config(C.Structure):
         for n, _ in cls._fields_:
             if n == "dtype":
                 c.dtype = SWAM_BF16 if o.dtype == "bf16" else SWAM_F32
+            elif n in ("rope", "qk_norm"):
+                setattr(c, n, int(getattr(o, n, 0)))
             else:
                 setattr(c, n, getattr(o, n))
         return c

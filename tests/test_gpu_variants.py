@@ -1,0 +1,185 @@
+"""GPU parity of the backbone variants -- rotary embedding of q and k at the
+rows' original positions and per-head QK-norm (Sec. 4.2 keeps the original
+position indices of the retained tokens) -- against the oracle.
+
+Tolerances as for the plain blocks: 1e-4 (fp32) and 2e-2 (bf16) max-relative
+on block outputs and stored q/k/v; the fp32 schedule checks selection
+bit-exact and pruned rows byte-identical, so a packed row rotated at its
+packed index instead of its original position fails it.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+import workload as W
+from helpers import act_dtype, dev, host, maxrel, model_for
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    torch.cuda.set_device(0)
+
+
+def _ctx(cfg):
+    from paper_2609_38984_amd import swam
+    return swam.Context(cfg)
+
+
+def _positions_in_seqs(cu):
+    pos = np.zeros(int(cu[-1]), np.int64)
+    for a, b in zip(cu[:-1], cu[1:]):
+        pos[a:b] = np.arange(b - a)
+    return pos
+
+
+def _small_bf16(**kw):
+    base = dict(name="bf16-small", batch=1, d_model=256, n_heads=4, n_blocks=2, n_ctx=20,
+                n_frames=2, frame_h=8, frame_w=9, n_act=8, k_core=18, k_anchor=6, reuse_R=2,
+                n_steps=4, dtype="bf16", seed=7, blob_sigma=1.5)
+    base.update(kw)
+    return W.SwamConfig(**base)
+
+
+def _block_case(cfg, cu, tol, lse_tol, dense_layout=False):
+    print(f"variant block {cfg.name} rope={cfg.rope} qk_norm={cfg.qk_norm} cu={list(cu)}",
+          flush=True)
+    blocks, dblocks, _ = model_for(cfg, 1)
+    n_rows = int(cu[-1])
+    x = W.make_inputs(cfg, blocks[0]["w_qkv"]).x(1)[:n_rows]
+    temb = W.timestep_embedding(cfg, 1)
+    pos = _positions_in_seqs(cu)
+    y_ref, tr = O.block(x, blocks[0], temb, cu, cfg.n_heads, cfg.dtype, pos, bool(cfg.rope),
+                        bool(cfg.qk_norm))
+    ctx = _ctx(cfg)
+    xd = dev(x, act_dtype(cfg))
+    lse = torch.empty(n_rows, cfg.n_heads, dtype=torch.float32, device="cuda:0")
+    qkv = torch.empty(n_rows, 3 * cfg.d_model, dtype=act_dtype(cfg), device="cuda:0")
+    if dense_layout:
+        ctx.block(dblocks[0], dev(temb), xd, n_rows, None, 0, lse, qkv)
+    else:
+        ctx.block(dblocks[0], dev(temb), xd, n_rows, dev(np.asarray(cu, np.int32)), len(cu) - 1,
+                  lse, qkv)
+    torch.cuda.synchronize()
+    e_y = maxrel(host(xd), y_ref)
+    e_q = maxrel(host(qkv), tr.qkv)
+    valid = np.zeros(n_rows, bool)
+    for a, b in zip(cu[:-1], cu[1:]):
+        valid[a:b] = True
+    e_l = float(np.abs(host(lse)[valid] - tr.lse[valid]).max()) if valid.any() else 0.0
+    print(f"  y {e_y:.2e} qkv {e_q:.2e} lse-abs {e_l:.2e}", flush=True)
+    assert e_q < tol and e_y < tol and e_l < lse_tol
+
+
+@pytest.mark.parametrize("rope,qk_norm", [(1, 0), (0, 1), (1, 1)])
+def test_variant_block_fp32_dense_layout(rope, qk_norm):
+    cfg = W.preset(1).replace(batch=2, rope=rope, qk_norm=qk_norm)
+    _block_case(cfg, O.dense_cu(cfg), 1e-4, 1e-5, dense_layout=True)
+
+
+def test_variant_block_fp32_ragged():
+    cfg = W.preset(1).replace(batch=3, rope=1, qk_norm=1)
+    _block_case(cfg, np.array([0, 37, 37, 190, 301]), 1e-4, 1e-5)
+
+
+def test_variant_block_bf16_ragged_tails():
+    cfg = _small_bf16(batch=4, rope=1, qk_norm=1)
+    _block_case(cfg, np.array([0, 37, 37, 237, 366, 367]), 2e-2, 5e-2)
+
+
+def test_variant_block_bf16_dense_layout():
+    cfg = _small_bf16(batch=2, rope=1, qk_norm=1)
+    _block_case(cfg, O.dense_cu(cfg), 2e-2, 5e-2, dense_layout=True)
+
+
+@pytest.mark.parametrize("rope,qk_norm", [(1, 0), (1, 1)])
+def test_variant_step_fp32_schedule_matches_oracle(rope, qk_norm):
+    from paper_2609_38984_amd import swam
+    cfg = W.preset(1).replace(rope=rope, qk_norm=qk_norm)
+    print(f"variant step schedule {cfg.name} rope={rope} qk_norm={qk_norm}", flush=True)
+    blocks, _, model = model_for(cfg)
+    inp = W.make_inputs(cfg, blocks[0]["w_qkv"])
+    ys, refr = O.run_schedule(cfg, blocks, inp.x, inp.temb)
+    ctx = _ctx(cfg)
+    kinds = []
+    for tau in range(cfg.n_steps):
+        x = dev(inp.x(tau))
+        y = torch.empty_like(x)
+        kinds.append(ctx.step(model, x, dev(inp.temb(tau)), tau, y))
+        torch.cuda.synchronize()
+        err = maxrel(host(y), ys[tau])
+        print(f"  tau {tau} kind {kinds[-1]} max-rel {err:.2e}", flush=True)
+        assert err < 1e-4
+        if tau in refr:
+            ki = torch.empty(cfg.n_frames * ctx.k_max, dtype=torch.int32, device="cuda:0")
+            ctx.export(keep_idx=ki)
+            torch.cuda.synchronize()
+            want = np.concatenate([np.asarray(r) for r in refr[tau].selection[0].retained])
+            np.testing.assert_array_equal(ki.cpu().numpy(), want)
+        else:
+            pm = refr[cfg.reuse_R * (tau // cfg.reuse_R)].packmap
+            pruned = pm.pack_pos < 0
+            xc = x.cpu().numpy()
+            assert y.cpu().numpy()[pruned].tobytes() == xc[pruned].tobytes()
+    assert kinds == [swam.KIND_REFRESH, swam.KIND_SPARSE] * 2
+
+
+def test_variant_step_bf16_sparse_matches_oracle_on_gpu_selection():
+    """bf16 sparse step with both variants, packed by the selection the GPU
+    made at the refresh step: the oracle's sparse step on that same packing."""
+    cfg = _small_bf16(batch=2, rope=1, qk_norm=1)
+    blocks, _, model = model_for(cfg)
+    inp = W.make_inputs(cfg, blocks[0]["w_qkv"])
+    ctx = _ctx(cfg)
+    x0 = dev(inp.x(0), act_dtype(cfg))
+    y0 = torch.empty_like(x0)
+    ctx.step(model, x0, dev(inp.temb(0)), 0, y0)
+    pp = torch.empty(cfg.batch * cfg.l_full, dtype=torch.int32, device="cuda:0")
+    ga = torch.empty(cfg.batch * cfg.l_full, dtype=torch.int32, device="cuda:0")
+    cu = torch.empty(cfg.batch + 1, dtype=torch.int32, device="cuda:0")
+    ctx.export(pack_pos=pp, gather=ga, cu_seqlens=cu)
+    torch.cuda.synchronize()
+    cu_h = cu.cpu().numpy().astype(np.int64)
+    t_pack = int(cu_h[-1])
+    pm = O.PackMap(pack_pos=pp.cpu().numpy().astype(np.int64),
+                   gather=ga.cpu().numpy()[:t_pack].astype(np.int64), cu_seqlens=cu_h)
+    x1 = inp.x(1)
+    y_ref = O.sparse_step(x1, blocks, inp.temb(1), cfg, pm)
+    x1d = dev(x1, act_dtype(cfg))
+    y1 = torch.empty_like(x1d)
+    ctx.step(model, x1d, dev(inp.temb(1)), 1, y1)
+    torch.cuda.synchronize()
+    kept = pm.pack_pos >= 0
+    err = maxrel(host(y1)[kept], y_ref[kept])
+    print(f"  bf16 sparse step with variants: kept rows max-rel {err:.2e}", flush=True)
+    assert err < 2e-2
+    assert host(y1)[~kept].tobytes() == host(x1d)[~kept].tobytes()
+
+
+def test_variant_block_wam_packed_sampled():
+    """Full WAM width with both variants on the packed layout the bench times:
+    sampled rows against the oracle one by one."""
+    cfg = W.preset(3).replace(rope=1, qk_norm=1)
+    print(f"variant full-size packed block {cfg.name} rows={cfg.t_pack_fixed}", flush=True)
+    blocks, dblocks, _ = model_for(cfg, 1)
+    x = W.make_inputs(cfg, blocks[0]["w_qkv"]).x(0)
+    temb = W.timestep_embedding(cfg, 0)
+    cu = np.array([0, cfg.t_pack_fixed])
+    n_rows = int(cu[-1])
+    ctx = _ctx(cfg)
+    xd = dev(x[:n_rows], act_dtype(cfg))
+    lse = torch.empty(n_rows, cfg.n_heads, dtype=torch.float32, device="cuda:0")
+    ctx.block(dblocks[0], dev(temb), xd, n_rows, dev(np.asarray(cu, np.int32)), 1, lse)
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(5)
+    rows = np.unique(np.concatenate([[0, n_rows - 1], rng.integers(0, n_rows, 24)]))
+    y_ref, l_ref = O.block_rows(x[:n_rows], blocks[0], temb, cu, rows, cfg.n_heads, cfg.dtype,
+                                np.arange(n_rows), True, True)
+    e_y = maxrel(host(xd)[rows], y_ref)
+    e_l = float(np.abs(host(lse)[rows] - l_ref).max())
+    print(f"  sampled {len(rows)} rows: y max-rel {e_y:.2e}, lambda abs {e_l:.2e}", flush=True)
+    assert e_y < 2e-2 and e_l < 5e-2
