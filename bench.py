@@ -50,6 +50,10 @@ def workload_from_args(args):
     if args.rope or args.qk_norm:
         tag = "+rope" * args.rope + "+qknorm" * args.qk_norm
         cfg = cfg.replace(rope=int(args.rope), qk_norm=int(args.qk_norm), name=cfg.name + tag)
+    if args.guidance is not None:
+        # every sequence gets an unconditional partner: the batch doubles
+        cfg = cfg.replace(batch=2 * cfg.batch, cfg_pairs=1, guidance=args.guidance,
+                          name=f"{cfg.name}+cfg{args.guidance:g}")
     return cfg
 
 
@@ -420,15 +424,15 @@ def overlap_diagnostic(cfg, model, xs, tembs):
     for tau in range(cfg.reuse_R + 1):
         ctx.step(model, xs[tau], tembs[tau], tau, y)
         if tau % cfg.reuse_R == 0:
-            v = torch.empty(cfg.batch * F, n_s, dtype=torch.float32, device=dev)
+            v = torch.empty(cfg.n_scored * F, n_s, dtype=torch.float32, device=dev)
             ctx.export(v=v)
             vs.append(v)
-    out = torch.empty(cfg.batch * F, dtype=torch.float32, device=dev)
+    out = torch.empty(cfg.n_scored * F, dtype=torch.float32, device=dev)
     ctx.overlap(vs[0], vs[1], out)
     step = float(out.mean().item())
     if F < 2:
         return {"overlap_cross_step": round(step, 4)}
-    v0 = vs[0].view(cfg.batch, F, n_s)
+    v0 = vs[0].view(cfg.n_scored, F, n_s)
     p = v0[:, :-1].reshape(-1, n_s).contiguous()
     q = v0[:, 1:].reshape(-1, n_s).contiguous()
     out2 = torch.empty(p.shape[0], dtype=torch.float32, device=dev)
@@ -452,13 +456,14 @@ def sampler_bench(args):
     wio = W.latent_io_weights(cfg, c)
     io = swam.LatentIO({k: torch.from_numpy(v).to(dev, adt) for k, v in wio.items()}, adt)
     si = W.make_sampler_inputs(cfg, c)
-    n_lat = cfg.batch * (cfg.l_full - cfg.n_ctx)
+    n_lat = cfg.batch * (cfg.l_full - cfg.n_ctx)          # rows of v (both branches with pairs)
+    n_state = cfg.n_scored * (cfg.l_full - cfg.n_ctx)     # rows of z and the cache
     x = torch.zeros(cfg.batch * cfg.l_full, cfg.d_model, dtype=adt, device=dev)
     for b in range(cfg.batch):
         x[b * cfg.l_full:b * cfg.l_full + cfg.n_ctx] = torch.from_numpy(si.ctx[b]).to(dev, adt)
     y = torch.empty_like(x)
     z0 = torch.from_numpy(si.z0).to(dev)
-    z, v, vc = z0.clone(), torch.zeros(n_lat, c, device=dev), torch.zeros(n_lat, c, device=dev)
+    z, v, vc = z0.clone(), torch.zeros(n_lat, c, device=dev), torch.zeros(n_state, c, device=dev)
     sig = swam.flow_sigmas(cfg.n_steps)
     tembs = [torch.from_numpy(W.time_embedding(cfg, 1000.0 * sig[t])).to(dev) for t in range(cfg.n_steps)]
     ctx = swam.Context(cfg)
@@ -484,7 +489,10 @@ def sampler_bench(args):
     steps = reps * cfg.n_steps
     out = {"mode": "closed-loop sampler", "workload": cfg.name, "d_latent": c,
            "steps": steps, "ms_per_step": round(el * 1e3 / steps, 4),
-           "tokens_per_s": round(steps * cfg.batch * cfg.l_full / el, 1), "kinds": kinds,
+           "tokens_per_s": round(steps * cfg.batch * cfg.l_full / el, 1),
+           "sample_tokens_per_s": round(steps * cfg.n_scored * cfg.l_full / el, 1),
+           "cfg_pairs": cfg.cfg_pairs, "guidance": cfg.guidance if cfg.cfg_pairs else None,
+           "kinds": kinds,
            "sampler_kernels_ms_per_step": round(ms_sample / steps, 4),
            "sampler_kernels_pct_of_step": round(100.0 * ms_sample / (el * 1e3), 3),
            "latent_tokens": n_lat, "final_z_finite": bool(torch.isfinite(z).all().item())}
@@ -669,6 +677,8 @@ def main():
     ap.add_argument("--rope", action="store_true",
                     help="backbone variant: rotary embedding at the original positions")
     ap.add_argument("--qk-norm", action="store_true", help="backbone variant: per-head QK-norm")
+    ap.add_argument("--guidance", type=float, default=None,
+                    help="classifier-free guidance pairs with this scale (the batch doubles)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(json.dumps({"error": "this build runs on one GPU only: the step is single-GPU "
@@ -707,7 +717,8 @@ def main():
                    "n_ctx": cfg.n_ctx, "n_act": cfg.n_act,
                    "k_core": cfg.k_core, "k_anchor": cfg.k_anchor,
                    "mass_threshold": cfg.mass_threshold, "reuse_R": cfg.reuse_R,
-                   "rope": cfg.rope, "qk_norm": cfg.qk_norm,
+                   "rope": cfg.rope, "qk_norm": cfg.qk_norm, "cfg_pairs": cfg.cfg_pairs,
+                   "guidance": cfg.guidance if cfg.cfg_pairs else None,
                    "packed_rows": m["packed_rows"], "schedule_kinds": m["kinds"]},
     }
     for k in ("dense_step_ms", "refresh_step_ms", "sparse_step_ms", "dense_tokens_per_s",

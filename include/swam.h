@@ -107,6 +107,17 @@ typedef struct {
    * the rotation. */
   int32_t rope;
   int32_t qk_norm;
+  /* Classifier-free guidance (App. B.2 lists guidance scale 3.0 for two of
+   * the backbones).  cfg_pairs = 1: the batch (even) holds P = batch/2
+   * conditional sequences followed by their P unconditional partners
+   * (sequence P + b pairs with b).  Scoring, score reduction and selection
+   * run on the conditional half only (the statistics come from the dense
+   * conditional forward, Sec. 4.2); the partner of b keeps b's retained
+   * positions.  The sampler entry points keep one latent state per pair and
+   * use the guided velocity v_u + guidance * (v_c - v_u).  guidance is read
+   * only with cfg_pairs = 1 (must be finite). */
+  int32_t cfg_pairs;
+  float guidance;
 } swam_config;
 
 /* Sizes derived from a configuration (host-only, no GPU needed). */
@@ -174,7 +185,9 @@ const char* swam_last_error(const swam_ctx* ctx);
  *           sequence, row r at k_all + b*kall_seq_stride + r*k_row_stride;
  *           lambda is then computed over all l_full keys in-kernel.
  *   s_out : float [B][F][N_s].
- * Strides may point inside a fused QKV buffer (row stride 3d). */
+ * Strides may point inside a fused QKV buffer (row stride 3d).  With
+ * guidance pairs B here (and in swam_score_reduce, swam_select's v / a and
+ * the score, Q, V, A exports) is the conditional half, batch / 2. */
 int swam_score(swam_ctx* ctx,
                const void* q_act, int64_t q_seq_stride, int64_t q_row_stride,
                const void* k_fut, int64_t k_seq_stride, int64_t k_row_stride,
@@ -218,7 +231,8 @@ int swam_select(swam_ctx* ctx, const float* v, const float* a, int32_t* keep_idx
                 int32_t* cu_seqlens);
 
 /* Import a selection (int32 [B][F][k_max] ascending, -1 padded; counts
- * [B][F]) and rebuild the packing metadata.  Indices outside [0, N_s) are
+ * [B][F]; with guidance pairs B is the whole batch, partners included) and
+ * rebuild the packing metadata.  Indices outside [0, N_s) are
  * ignored.  Synchronises once to read the packed lengths. */
 int swam_set_selection(swam_ctx* ctx, const int32_t* keep_idx, const int32_t* keep_cnt);
 
@@ -316,7 +330,10 @@ int swam_overlap(swam_ctx* ctx, const float* p, const float* q, int64_t n_maps, 
  * x_full and y_full 16-byte aligned, else SWAM_E_INVALID).  Latent tensors -- z, velocities v, the velocity cache -- are float
  * [B][L_lat][c] with L_lat = F*N_s + H: the future tokens of each sequence
  * (frame-major, row-major in a frame) followed by its action tokens, i.e. the
- * full-layout rows n_ctx .. l_full-1 of every sequence. */
+ * full-layout rows n_ctx .. l_full-1 of every sequence.  With guidance pairs
+ * z and the cache cover the P conditional sequences ([P][L_lat][c], one
+ * state per pair) while v holds both branches ([B][L_lat][c], conditional
+ * half first). */
 typedef struct {
   int32_t d_latent;
   const void* w_in;  const void* b_in;     /* [d][c], [d]: token = z W_in^T + b_in */
@@ -324,7 +341,8 @@ typedef struct {
 } swam_latent_io;
 
 /* Tokens of the latent rows of x_full [B*l_full][d] from z (stored in the
- * config dtype); context rows are not touched. */
+ * config dtype); context rows are not touched.  With guidance pairs both
+ * sequences of a pair get the tokens of the pair's latent state. */
 int swam_embed(swam_ctx* ctx, const swam_latent_io* io, const float* z, void* x_full);
 
 /* Velocity read-out v = LN(y) W_v^T + b_v (LayerNorm without affine, eps
@@ -341,7 +359,9 @@ int swam_velocity(swam_ctx* ctx, const swam_latent_io* io, const void* y_full,
  *   kind SWAM_KIND_SPARSE : the paper's merge M v + (1 - M) v_cache over the
  *                           future tokens, M = the cached selection (Sec. 4.2,
  *                           cached visual prediction eq.); action rows take v.
- * (fp32 FMA per element.)  v_cache may be NULL for SWAM_KIND_DENSE. */
+ * (fp32 FMA per element.)  v_cache may be NULL for SWAM_KIND_DENSE.  With
+ * guidance pairs "v" above is the guided v_u + guidance * (v_c - v_u) of the
+ * two branch rows of v (one fp32 FMA), which is also what the cache holds. */
 int swam_sample_update(swam_ctx* ctx, int32_t d_latent, const float* v, float* v_cache,
                        float* z, float dsigma, int32_t kind);
 

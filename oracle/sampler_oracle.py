@@ -18,7 +18,13 @@ storage points as the GPU path:
   action velocities are always the current ones;
 * the sampler is the flow-matching Euler step z <- z + (sigma_next - sigma) v
   over a shifted schedule sigma(s) = shift s / (1 + (shift - 1) s), s = 1 - i/N,
-  shift 5.0 (App. B.2), with the model time t = 1000 sigma.
+  shift 5.0 (App. B.2), with the model time t = 1000 sigma;
+* with classifier-free guidance (scale g, App. B.2) the batch holds P
+  conditional sequences and their P unconditional partners, both branches
+  denoise one latent state per pair, the guided velocity is
+  v = v_u + g (v_c - v_u), and that guided velocity is what a full step
+  caches and a sparse step merges; the selection comes from the conditional
+  branch and the partner reuses it.
 
 The linear embedding / head, the LayerNorm in the head and the Euler
 integrator are readings (the paper names the merge, the shift and that the
@@ -32,7 +38,7 @@ from dataclasses import dataclass
 import numpy as np
 
 from .swam_oracle import (round_f32, storage_round, layer_norm, is_refresh, refresh_step,
-                          sparse_step, dense_step)
+                          sparse_step, dense_step, n_scored)
 
 SCHEDULE_SHIFT = 5.0     # App. B.2: noise schedule shift of every backbone
 
@@ -69,6 +75,13 @@ def merge_velocity(v_cur, v_cached, keep):
     return np.where(keep[:, None], np.asarray(v_cur, np.float64), np.asarray(v_cached, np.float64))
 
 
+def guided_velocity(v_cond, v_uncond, g):
+    """Classifier-free guidance of two branch velocities: v_u + g (v_c - v_u)."""
+    vc = np.asarray(v_cond, np.float64)
+    vu = np.asarray(v_uncond, np.float64)
+    return vu + float(g) * (vc - vu)
+
+
 def euler_update(z, v, dsigma):
     """One flow-matching Euler step of the float32 latent state."""
     return round_f32(np.asarray(z, np.float64) + float(dsigma) * np.asarray(v, np.float64))
@@ -91,12 +104,24 @@ def run_sampler(cfg, model, io, ctx_tokens, z0, temb_of_t, n_steps=None,
     reference the sparse sampler approximates).
 
     io: dict w_in [d][c], b_in [d], w_v [c][d], b_v [c];
-    ctx_tokens: [B][n_ctx][d]; z0: [B*L_lat][c]; temb_of_t(t) -> [d_temb]."""
+    ctx_tokens: [B][n_ctx][d]; z0: [P*L_lat][c] (P = B, or B/2 with guidance
+    pairs); temb_of_t(t) -> [d_temb]."""
     n = cfg.n_steps if n_steps is None else n_steps
     sig = sigmas(n, shift)
     rows = latent_rows(cfg)
     L_lat = cfg.l_full - cfg.n_ctx
-    fut = np.tile(np.arange(L_lat) < cfg.n_fut, cfg.batch)
+    P = n_scored(cfg)
+    pairs = P != cfg.batch
+    g = float(getattr(cfg, "guidance", 1.0))
+    fut = np.tile(np.arange(L_lat) < cfg.n_fut, P)
+    cond_rows = rows[:P * L_lat]
+
+    def branch_velocity(v_all):
+        # per-sequence read-outs [B*L_lat][c] -> the velocity of each latent state
+        if not pairs:
+            return v_all
+        return guided_velocity(v_all[:P * L_lat], v_all[P * L_lat:], g)
+
     x = np.zeros((cfg.batch * cfg.l_full, cfg.d_model))
     for b in range(cfg.batch):
         x[b * cfg.l_full:b * cfg.l_full + cfg.n_ctx] = ctx_tokens[b]
@@ -106,22 +131,23 @@ def run_sampler(cfg, model, io, ctx_tokens, z0, temb_of_t, n_steps=None,
     tr = SamplerTrace(z=[], kinds=[], v_tilde=[], x=[])
     for tau in range(n):
         x = x.copy()
-        x[rows] = embed(z, io["w_in"], io["b_in"], cfg.dtype)
+        z_rows = np.concatenate([z, z]) if pairs else z
+        x[rows] = embed(z_rows, io["w_in"], io["b_in"], cfg.dtype)
         temb = temb_of_t(1000.0 * sig[tau])
         if dense:
             y = dense_step(x, model, temb, cfg)
-            v_t = velocity(y[rows], io["w_v"], io["b_v"])
+            v_t = branch_velocity(velocity(y[rows], io["w_v"], io["b_v"]))
             kind = 0
         elif is_refresh(tau, cfg.reuse_R):
             r = refresh_step(x, model, temb, cfg)
             pm = r.packmap
-            v_t = velocity(r.y[rows], io["w_v"], io["b_v"])
+            v_t = branch_velocity(velocity(r.y[rows], io["w_v"], io["b_v"]))
             v_cache = np.where(fut[:, None], v_t, v_cache)
             kind = 1
         else:
             y = sparse_step(x, model, temb, cfg, pm)
-            v_cur = velocity(y[rows], io["w_v"], io["b_v"])
-            keep = (pm.pack_pos[rows] >= 0) | ~fut
+            v_cur = branch_velocity(velocity(y[rows], io["w_v"], io["b_v"]))
+            keep = (pm.pack_pos[cond_rows] >= 0) | ~fut
             v_t = merge_velocity(v_cur, v_cache, keep)
             kind = 2
         z = euler_update(z, v_t, sig[tau + 1] - sig[tau])

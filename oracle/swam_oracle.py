@@ -562,9 +562,9 @@ def dense_cu(cfg):
 @dataclass
 class RefreshResult:
     y: np.ndarray
-    S_all: np.ndarray      # [B][L][F][N_s] float32 values
-    reduced: list          # per sequence Reduced
-    selection: list        # per sequence Selection
+    S_all: np.ndarray      # [B_s][L][F][N_s] float32 values (B_s = scored sequences)
+    reduced: list          # per scored sequence Reduced
+    selection: list        # per scored sequence Selection
     packmap: PackMap
 
 
@@ -590,11 +590,18 @@ def dense_step(x_full, model, temb, cfg):
     return run_blocks(x_full, model, temb, dense_cu(cfg), cfg)
 
 
+def n_scored(cfg):
+    """Sequences whose attention is scored: with guidance pairs only the
+    conditional half [0, B/2) (the selection statistics come from the dense
+    conditional forward, Sec. 4.2 / App. B.2); otherwise every sequence."""
+    return cfg.batch // 2 if getattr(cfg, "cfg_pairs", 0) else cfg.batch
+
+
 def layer_scores(cfg, tr: BlockTrace):
-    """S_l for every sequence from one block's stored q, k and lambda."""
+    """S_l for every scored sequence from one block's stored q, k and lambda."""
     d = cfg.d_model
     out = []
-    for b in range(cfg.batch):
+    for b in range(n_scored(cfg)):
         base = b * cfg.l_full
         act = slice(base + cfg.n_ctx + cfg.n_fut, base + cfg.l_full)
         fut = slice(base + cfg.n_ctx, base + cfg.n_ctx + cfg.n_fut)
@@ -604,18 +611,22 @@ def layer_scores(cfg, tr: BlockTrace):
 
 
 def selection_from_scores(cfg, S_all):
+    """Reduce and select every scored sequence; with guidance pairs the
+    unconditional partner b + B/2 keeps the positions selected for b."""
     reduced, sel = [], []
-    for b in range(cfg.batch):
+    P = n_scored(cfg)
+    for b in range(P):
         r = score_reduce(S_all[b], cfg.k_layer, cfg.cv_penalty)
         reduced.append(r)
         sel.append(select(r.V, r.A, cfg.k_core, cfg.k_anchor, cfg.mass_threshold))
-    pm = pack_map(keep_mask(cfg, [s.retained for s in sel]), cfg.batch)
+    retained = [sel[b % P].retained for b in range(cfg.batch)]
+    pm = pack_map(keep_mask(cfg, retained), cfg.batch)
     return reduced, sel, pm
 
 
 def refresh_step(x_full, model, temb, cfg):
     """Full step: dense forward, per-layer scores, reduce, select, pack map."""
-    S_all = np.zeros((cfg.batch, len(model), cfg.n_frames, cfg.n_s))
+    S_all = np.zeros((n_scored(cfg), len(model), cfg.n_frames, cfg.n_s))
 
     def cb(l, tr):
         for b, S in enumerate(layer_scores(cfg, tr)):

@@ -168,15 +168,20 @@ hipError_t launch_overlap(const float* p, const float* q, int64_t n_maps, int64_
                           float* out, hipStream_t st);
 
 // sampling update (k_sampler.hip)
+// z_rows: latent rows of z; the latent rows of sequences past them (the
+// unconditional partners of guidance pairs) read z row i - z_rows
 hipError_t launch_embed(int dtype, const float* z, const void* w_in, const void* b_in, void* x,
-                        int64_t n_lat_rows, int l_lat, int l_full, int n_ctx, int c, int d,
-                        hipStream_t st);
+                        int64_t n_lat_rows, int64_t z_rows, int l_lat, int l_full, int n_ctx,
+                        int c, int d, hipStream_t st);
 hipError_t launch_velocity(int dtype, const void* y, const int32_t* gather, int64_t n_items,
                            const void* w_v, const void* b_v, float* v, int l_lat, int l_full,
                            int n_ctx, int c, int d, hipStream_t st);
+// pairs: v holds 2 * n_lat_rows rows (conditional, then unconditional) that
+// are combined as v_u + guidance * (v_c - v_u) before the merge
 hipError_t launch_sample_update(const float* v, float* v_cache, float* z, const int32_t* pack_pos,
                                 float dsigma, int kind, int64_t n_lat_rows, int l_lat, int l_full,
-                                int n_ctx, int n_fut, int c, hipStream_t st);
+                                int n_ctx, int n_fut, int c, int pairs, float guidance,
+                                hipStream_t st);
 hipError_t launch_copy(const void* src, void* dst, int64_t bytes, hipStream_t st);
 
 }  // namespace swam

@@ -4,10 +4,12 @@
 //             fp32 latents, x = z W_in^T + b_in, stored in the config dtype;
 //   velocity: v = LN(y) W_v^T + b_v for every latent row, or only for the rows
 //             of the cached selection (retained future tokens and actions);
-//   update  : a full step stores the future velocities in the cache; a sparse
-//             step uses the current velocity where the token was retained and
-//             the cached one elsewhere (actions always current); then
-//             z <- z + dsigma * v with one fp32 FMA.
+//   update  : with guidance pairs the two branch velocities of a latent row
+//             are first combined as v_u + g (v_c - v_u); a full step stores the
+//             future velocities in the cache; a sparse step uses the current
+//             velocity where the token was retained and the cached one
+//             elsewhere (actions always current); then z <- z + dsigma * v
+//             with one fp32 FMA.
 // All three are memory-bound (c <= 64 latent channels against d >= 64 token
 // channels); latents, velocities and the cache are fp32.
 #include "common.h"
@@ -37,7 +39,8 @@ __device__ __forceinline__ void load8(const T* p, float (&o)[8]) {
 template <typename T, bool VEC>
 __global__ void __launch_bounds__(256)
 embed_kernel(const float* __restrict__ z, const T* __restrict__ w_in, const T* __restrict__ b_in,
-             T* __restrict__ x, int64_t n_lat_rows, int l_lat, int l_full, int n_ctx, int c, int d) {
+             T* __restrict__ x, int64_t n_lat_rows, int64_t z_rows, int l_lat, int l_full, int n_ctx,
+             int c, int d) {
   const int64_t id = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   const int chunks = d / 8;
   if (id >= n_lat_rows * chunks) return;
@@ -45,7 +48,7 @@ embed_kernel(const float* __restrict__ z, const T* __restrict__ w_in, const T* _
   const int col = (int)(id % chunks) * 8;
   const int64_t b = i / l_lat;
   const int64_t row = b * l_full + n_ctx + (i - b * l_lat);
-  const float* zr = z + i * c;
+  const float* zr = z + (i < z_rows ? i : i - z_rows) * c;
   float acc[8];
 #pragma unroll
   for (int e = 0; e < 8; ++e) acc[e] = 0.0f;
@@ -91,7 +94,8 @@ constexpr int EMB_ROWS = 32;
 template <typename T, int C>
 __global__ void __launch_bounds__(256)
 embed_reg_kernel(const float* __restrict__ z, const T* __restrict__ w_in, const T* __restrict__ b_in,
-                 T* __restrict__ x, int64_t n_lat_rows, int l_lat, int l_full, int n_ctx, int d) {
+                 T* __restrict__ x, int64_t n_lat_rows, int64_t z_rows, int l_lat, int l_full,
+                 int n_ctx, int d) {
   const int64_t id = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   const int chunks = d / 8;
   const int64_t groups = (n_lat_rows + EMB_ROWS - 1) / EMB_ROWS;
@@ -114,9 +118,10 @@ embed_reg_kernel(const float* __restrict__ z, const T* __restrict__ w_in, const 
     const int64_t b = i / l_lat;
     const int64_t row = b * l_full + n_ctx + (i - b * l_lat);
     float zk[C];
+    const float* zr = z + (i < z_rows ? i : i - z_rows) * C;
 #pragma unroll
     for (int k0 = 0; k0 < C; k0 += 4) {
-      const float4 t = *reinterpret_cast<const float4*>(z + i * C + k0);
+      const float4 t = *reinterpret_cast<const float4*>(zr + k0);
       zk[k0] = t.x; zk[k0 + 1] = t.y; zk[k0 + 2] = t.z; zk[k0 + 3] = t.w;
     }
     float acc[8];
@@ -230,17 +235,21 @@ velocity_kernel(const T* __restrict__ y, const int32_t* __restrict__ gather, int
   }
 }
 
-// one thread per latent element
+// one thread per latent element (of the conditional half with pairs)
 __global__ void __launch_bounds__(256)
 update_kernel(const float* __restrict__ v, float* __restrict__ v_cache, float* __restrict__ z,
               const int32_t* __restrict__ pack_pos, float dsigma, int kind, int64_t n,
-              int l_lat, int l_full, int n_ctx, int n_fut, int c) {
+              int l_lat, int l_full, int n_ctx, int n_fut, int c, int pairs, float guidance) {
   const int64_t id = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (id >= n) return;
   const int64_t i = id / c;
   const int64_t b = i / l_lat;
   const int r = (int)(i - b * l_lat);
   float vt = v[id];
+  if (pairs) {
+    const float vu = v[id + n];
+    vt = fmaf(guidance, vt - vu, vu);
+  }
   if (r < n_fut) {
     if (kind == 1) v_cache[id] = vt;
     else if (kind == 2 && pack_pos[b * l_full + n_ctx + r] < 0) vt = v_cache[id];
@@ -249,8 +258,8 @@ update_kernel(const float* __restrict__ v, float* __restrict__ v_cache, float* _
 }
 
 hipError_t launch_embed(int dtype, const float* z, const void* w_in, const void* b_in, void* x,
-                        int64_t n_lat_rows, int l_lat, int l_full, int n_ctx, int c, int d,
-                        hipStream_t st) {
+                        int64_t n_lat_rows, int64_t z_rows, int l_lat, int l_full, int n_ctx,
+                        int c, int d, hipStream_t st) {
   if (n_lat_rows <= 0) return hipSuccess;
   const int64_t n = n_lat_rows * (d / 8);
   const dim3 grid((unsigned)((n + 255) / 256));
@@ -259,7 +268,7 @@ hipError_t launch_embed(int dtype, const float* z, const void* w_in, const void*
     const dim3 g2((unsigned)((groups * (d / 8) + 255) / 256));
 #define SWAM_EMBR(T_, C_)                                                                      \
   hipLaunchKernelGGL((embed_reg_kernel<T_, C_>), g2, dim3(256), 0, st, z, (const T_*)w_in,     \
-                     (const T_*)b_in, (T_*)x, n_lat_rows, l_lat, l_full, n_ctx, d)
+                     (const T_*)b_in, (T_*)x, n_lat_rows, z_rows, l_lat, l_full, n_ctx, d)
     if (dtype == 1) {
       if (c == 8) SWAM_EMBR(bf16_t, 8); else SWAM_EMBR(bf16_t, 16);
     } else {
@@ -271,7 +280,7 @@ hipError_t launch_embed(int dtype, const float* z, const void* w_in, const void*
   const bool vec = c % 8 == 0;
 #define SWAM_EMB(T_, V_)                                                                       \
   hipLaunchKernelGGL((embed_kernel<T_, V_>), grid, dim3(256), 0, st, z, (const T_*)w_in,       \
-                     (const T_*)b_in, (T_*)x, n_lat_rows, l_lat, l_full, n_ctx, c, d)
+                     (const T_*)b_in, (T_*)x, n_lat_rows, z_rows, l_lat, l_full, n_ctx, c, d)
   if (dtype == 1) {
     if (vec) SWAM_EMB(bf16_t, true); else SWAM_EMB(bf16_t, false);
   } else {
@@ -311,11 +320,13 @@ hipError_t launch_velocity(int dtype, const void* y, const int32_t* gather, int6
 
 hipError_t launch_sample_update(const float* v, float* v_cache, float* z, const int32_t* pack_pos,
                                 float dsigma, int kind, int64_t n_lat_rows, int l_lat, int l_full,
-                                int n_ctx, int n_fut, int c, hipStream_t st) {
+                                int n_ctx, int n_fut, int c, int pairs, float guidance,
+                                hipStream_t st) {
   const int64_t n = n_lat_rows * c;
   if (n <= 0) return hipSuccess;
   hipLaunchKernelGGL(update_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, v,
-                     v_cache, z, pack_pos, dsigma, kind, n, l_lat, l_full, n_ctx, n_fut, c);
+                     v_cache, z, pack_pos, dsigma, kind, n, l_lat, l_full, n_ctx, n_fut, c, pairs,
+                     guidance);
   return hipGetLastError();
 }
 

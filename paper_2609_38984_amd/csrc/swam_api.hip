@@ -24,6 +24,7 @@ thread_local std::string g_err;
 
 struct Derived {
   int64_t n_s, g, l_full, rows_full, k_max, k_eff, d, hidden, esz, t_pack_fixed;
+  int64_t n_scored;   // sequences that are scored and selected (the conditional half with pairs)
   int mass_num, mass_den;
 };
 
@@ -76,6 +77,11 @@ int derive(const swam_config* c, Derived* dv, std::string* err) {
   if (c->reuse_R < 1) return fail(err, SWAM_E_INVALID, "reuse_R must be >= 1");
   if (c->rope != 0 && c->rope != 1) return fail(err, SWAM_E_INVALID, "rope must be 0 or 1");
   if (c->qk_norm != 0 && c->qk_norm != 1) return fail(err, SWAM_E_INVALID, "qk_norm must be 0 or 1");
+  if (c->cfg_pairs != 0 && c->cfg_pairs != 1)
+    return fail(err, SWAM_E_INVALID, "cfg_pairs must be 0 or 1");
+  if (c->cfg_pairs && c->batch % 2)
+    return fail(err, SWAM_E_SHAPE, "guidance pairs need an even batch");
+  if (!std::isfinite(c->guidance)) return fail(err, SWAM_E_INVALID, "guidance must be finite");
   const int64_t d = c->d_model;
   if (c->dtype == SWAM_BF16 && d > 4096) return fail(err, SWAM_E_SHAPE, "bf16 d_model <= 4096");
   const int64_t l_full = c->n_ctx + (int64_t)c->n_frames * n_s + c->n_act;
@@ -85,6 +91,7 @@ int derive(const swam_config* c, Derived* dv, std::string* err) {
   if (c->dtype == SWAM_BF16 && rows * 3 * d >= (1ll << 31))
     return fail(err, SWAM_E_SHAPE, "batch * tokens * 3 * d_model must stay below 2^31");
   dv->n_s = n_s;
+  dv->n_scored = c->cfg_pairs ? c->batch / 2 : c->batch;
   dv->g = g;
   dv->l_full = l_full;
   dv->rows_full = rows;
@@ -313,7 +320,7 @@ int run_reduce(swam_ctx* c, const float* s_all) {
   r.v = c->ptr<float>(c->lay.v);
   r.a = c->ptr<float>(c->lay.a);
   r.vall = c->ptr<double>(c->lay.vall);
-  r.B = cf.batch;
+  r.B = (int)c->dv.n_scored;
   r.L = cf.n_blocks;
   r.F = cf.n_frames;
   r.n_s = (int)c->dv.n_s;
@@ -344,7 +351,7 @@ int run_select(swam_ctx* c, const float* v, const float* a) {
   s.keep_idx = c->ptr<int32_t>(c->lay.keep_idx);
   s.keep_cnt = c->ptr<int32_t>(c->lay.keep_cnt);
   s.keep = c->ptr<int32_t>(c->lay.keep);
-  s.B = cf.batch;
+  s.B = (int)c->dv.n_scored;
   s.F = cf.n_frames;
   s.n_s = (int)c->dv.n_s;
   s.k_core = cf.k_core;
@@ -357,6 +364,18 @@ int run_select(swam_ctx* c, const float* v, const float* a) {
   {
     Timed t(c, SWAM_T_SELECT);
     SWAM_HIP(c, launch_select(s, c->st), "select");
+    if (cf.cfg_pairs) {
+      // the unconditional partner b + B/2 keeps the positions selected for b
+      const int64_t P = c->dv.n_scored;
+      const size_t kb = (size_t)(P * c->dv.l_full) * 4, ib = (size_t)(P * cf.n_frames * c->dv.k_max) * 4,
+                   cb = (size_t)(P * cf.n_frames) * 4;
+      SWAM_HIP(c, hipMemcpyAsync((char*)s.keep + kb, s.keep, kb, hipMemcpyDeviceToDevice, c->st),
+               "share keep");
+      SWAM_HIP(c, hipMemcpyAsync((char*)s.keep_idx + ib, s.keep_idx, ib, hipMemcpyDeviceToDevice,
+                                 c->st), "share keep_idx");
+      SWAM_HIP(c, hipMemcpyAsync((char*)s.keep_cnt + cb, s.keep_cnt, cb, hipMemcpyDeviceToDevice,
+                                 c->st), "share keep_cnt");
+    }
     SWAM_HIP(c, launch_packmap(s.keep, c->ptr<int32_t>(c->lay.pack_pos),
                                c->ptr<int32_t>(c->lay.gather), c->ptr<int32_t>(c->lay.cu_packed),
                                cf.batch, c->dv.l_full, c->st), "packmap");
@@ -507,7 +526,7 @@ int swam_score(swam_ctx* c, const void* q_act, int64_t q_seq_stride, int64_t q_r
     Timed t(c, SWAM_T_SCORE);
     float* ws = c->ptr<float>(c->lay.lse_act);
     SWAM_HIP(c, launch_lse_all(cf.dtype, q_act, q_seq_stride, q_row_stride, k_all,
-                               kall_seq_stride, k_row_stride, c->dv.l_full, cf.batch, cf.n_act,
+                               kall_seq_stride, k_row_stride, c->dv.l_full, (int)c->dv.n_scored, cf.n_act,
                                cf.n_heads, ws, c->ptr<float>(c->lay.lse_part), c->st),
              "lse (mode B)");
     lse = ws;
@@ -518,7 +537,7 @@ int swam_score(swam_ctx* c, const void* q_act, int64_t q_seq_stride, int64_t q_r
   a.lse = lse; a.lse_seq = lse_seq;
   a.s_out = s_out; a.s_seq = (int64_t)cf.n_frames * c->dv.n_s;
   a.alpha = c->ptr<float>(c->lay.alpha);
-  a.B = cf.batch; a.F = cf.n_frames; a.n_s = (int)c->dv.n_s; a.H = cf.n_act;
+  a.B = (int)c->dv.n_scored; a.F = cf.n_frames; a.n_s = (int)c->dv.n_s; a.H = cf.n_act;
   a.n_heads = cf.n_heads;
   a.n_layers = 1;
   Timed t(c, SWAM_T_SCORE);
@@ -533,7 +552,7 @@ int swam_score_reduce(swam_ctx* c, const float* s_all, float* q_out, float* v_ou
   int rc = run_reduce(c, s_all);
   if (rc != SWAM_OK) return rc;
   const swam_config& cf = c->cfg;
-  const int64_t B = cf.batch;
+  const int64_t B = c->dv.n_scored;
   if ((rc = copy_out(c, q_out, c->lay.q, B * cf.n_blocks * 4, "copy Q"))) return rc;
   if ((rc = copy_out(c, v_out, c->lay.v, B * cf.n_frames * c->dv.n_s * 4, "copy V"))) return rc;
   if ((rc = copy_out(c, a_out, c->lay.a, B * c->dv.n_s * 4, "copy A"))) return rc;
@@ -594,10 +613,11 @@ int swam_export(swam_ctx* c, float* s_all, float* q, float* v, float* a, int32_t
   if ((keep_idx || keep_cnt || pack_pos || gather || cu_seqlens) && !c->sel_valid)
     return set_err(c, SWAM_E_STATE, "no selection cached");
   int rc;
-  if ((rc = copy_out(c, s_all, c->lay.s_all, B * cf.n_blocks * F * n_s * 4, "copy S"))) return rc;
-  if ((rc = copy_out(c, q, c->lay.q, B * cf.n_blocks * 4, "copy Q"))) return rc;
-  if ((rc = copy_out(c, v, c->lay.v, B * F * n_s * 4, "copy V"))) return rc;
-  if ((rc = copy_out(c, a, c->lay.a, B * n_s * 4, "copy A"))) return rc;
+  const int64_t Bs = c->dv.n_scored;
+  if ((rc = copy_out(c, s_all, c->lay.s_all, Bs * cf.n_blocks * F * n_s * 4, "copy S"))) return rc;
+  if ((rc = copy_out(c, q, c->lay.q, Bs * cf.n_blocks * 4, "copy Q"))) return rc;
+  if ((rc = copy_out(c, v, c->lay.v, Bs * F * n_s * 4, "copy V"))) return rc;
+  if ((rc = copy_out(c, a, c->lay.a, Bs * n_s * 4, "copy A"))) return rc;
   if ((rc = copy_out(c, keep_idx, c->lay.keep_idx, B * F * c->dv.k_max * 4, "copy keep_idx"))) return rc;
   if ((rc = copy_out(c, keep_cnt, c->lay.keep_cnt, B * F * 4, "copy keep_cnt"))) return rc;
   if ((rc = copy_out(c, pack_pos, c->lay.pack_pos, c->dv.rows_full * 4, "copy pack_pos"))) return rc;
@@ -716,7 +736,7 @@ int enqueue_step(swam_ctx* c, const swam_model* model, const void* x_full, const
       a.s_out = c->ptr<float>(c->lay.s_all);
       a.s_seq = (int64_t)cf.n_blocks * cf.n_frames * c->dv.n_s;
       a.alpha = c->ptr<float>(c->lay.alpha);
-      a.B = cf.batch;
+      a.B = (int)c->dv.n_scored;
       a.F = cf.n_frames;
       a.n_s = (int)c->dv.n_s;
       a.H = cf.n_act;
@@ -817,8 +837,9 @@ int swam_embed(swam_ctx* c, const swam_latent_io* io, const float* z, void* x_fu
   const swam_config& cf = c->cfg;
   const int l_lat = (int)(c->dv.l_full - cf.n_ctx);
   Timed t(c, SWAM_T_SAMPLE);
-  SWAM_HIP(c, launch_embed(cf.dtype, z, io->w_in, io->b_in, x_full, (int64_t)cf.batch * l_lat, l_lat,
-                           (int)c->dv.l_full, cf.n_ctx, io->d_latent, (int)c->dv.d, c->st),
+  SWAM_HIP(c, launch_embed(cf.dtype, z, io->w_in, io->b_in, x_full, (int64_t)cf.batch * l_lat,
+                           c->dv.n_scored * l_lat, l_lat, (int)c->dv.l_full, cf.n_ctx,
+                           io->d_latent, (int)c->dv.d, c->st),
            "embed");
   return SWAM_OK;
 }
@@ -854,8 +875,9 @@ static int sample_update(swam_ctx* c, int c_lat, const float* v, float* v_cache,
   const int l_lat = (int)(c->dv.l_full - cf.n_ctx);
   Timed t(c, SWAM_T_SAMPLE);
   SWAM_HIP(c, launch_sample_update(v, v_cache, z, c->ptr<int32_t>(c->lay.pack_pos), dsigma, kind,
-                                   (int64_t)cf.batch * l_lat, l_lat, (int)c->dv.l_full, cf.n_ctx,
-                                   (int)(cf.n_frames * c->dv.n_s), c_lat, c->st),
+                                   c->dv.n_scored * l_lat, l_lat, (int)c->dv.l_full, cf.n_ctx,
+                                   (int)(cf.n_frames * c->dv.n_s), c_lat, cf.cfg_pairs,
+                                   cf.guidance, c->st),
            "sample update");
   return SWAM_OK;
 }

@@ -56,7 +56,8 @@ class Config(C.Structure):
         "batch", "d_model", "n_heads", "head_dim", "mlp_ratio", "n_blocks", "d_temb", "n_ctx",
         "n_frames", "frame_h", "frame_w", "n_act", "k_core", "k_anchor", "k_layer")] + [
         ("cv_penalty", C.c_float), ("mass_threshold", C.c_float), ("reuse_R", C.c_int32),
-        ("dtype", C.c_int32), ("rope", C.c_int32), ("qk_norm", C.c_int32)]
+        ("dtype", C.c_int32), ("rope", C.c_int32), ("qk_norm", C.c_int32),
+        ("cfg_pairs", C.c_int32), ("guidance", C.c_float)]
 
     @classmethod
     def from_obj(cls, o) -> "Config":
@@ -65,8 +66,10 @@ class Config(C.Structure):
         for n, _ in cls._fields_:
             if n == "dtype":
                 c.dtype = SWAM_BF16 if o.dtype == "bf16" else SWAM_F32
-            elif n in ("rope", "qk_norm"):
+            elif n in ("rope", "qk_norm", "cfg_pairs"):
                 setattr(c, n, int(getattr(o, n, 0)))
+            elif n == "guidance":
+                c.guidance = float(getattr(o, n, 1.0))
             else:
                 setattr(c, n, getattr(o, n))
         return c
@@ -234,34 +237,41 @@ class Context:
     def k_max(self):
         return self.plan.k_max
 
+    @property
+    def n_scored(self):
+        """Sequences that are scored and selected (the conditional half with
+        guidance pairs)."""
+        c = self.c_cfg
+        return c.batch // 2 if c.cfg_pairs else c.batch
+
     # -- (1) scoring -----------------------------------------------------------
     def score(self, q_act, q_seq, q_row, k_fut, k_seq, k_row, s_out, lse_act=None, k_all=None,
               kall_seq=0):
         c = self.c_cfg
         n_s = self.n_s
-        _ptr(s_out, torch.float32, c.batch * c.n_frames * n_s, "s_out")
+        _ptr(s_out, torch.float32, self.n_scored * c.n_frames * n_s, "s_out")
         self._ok(self.lib.swam_score(
             self.h, _ptr(q_act, self.act_dtype, name="q_act"), q_seq, q_row,
             _ptr(k_fut, self.act_dtype, name="k_fut"), k_seq, k_row,
-            _ptr(lse_act, torch.float32, c.batch * c.n_act * c.n_heads, "lse_act"),
+            _ptr(lse_act, torch.float32, self.n_scored * c.n_act * c.n_heads, "lse_act"),
             _ptr(k_all, self.act_dtype, name="k_all"), kall_seq, s_out.data_ptr()))
 
     def score_reduce(self, s_all, v_out, a_out, q_out=None, core_out=None):
         c = self.c_cfg
         self._ok(self.lib.swam_score_reduce(
-            self.h, _ptr(s_all, torch.float32, c.batch * c.n_blocks * c.n_frames * self.n_s, "s_all"),
-            _ptr(q_out, torch.float32, c.batch * c.n_blocks, "q_out"),
-            _ptr(v_out, torch.float32, c.batch * c.n_frames * self.n_s, "v_out"),
-            _ptr(a_out, torch.float32, c.batch * self.n_s, "a_out"),
-            _ptr(core_out, torch.int32, c.batch * self.plan.k_layer_eff, "core_out")))
+            self.h, _ptr(s_all, torch.float32, self.n_scored * c.n_blocks * c.n_frames * self.n_s, "s_all"),
+            _ptr(q_out, torch.float32, self.n_scored * c.n_blocks, "q_out"),
+            _ptr(v_out, torch.float32, self.n_scored * c.n_frames * self.n_s, "v_out"),
+            _ptr(a_out, torch.float32, self.n_scored * self.n_s, "a_out"),
+            _ptr(core_out, torch.int32, self.n_scored * self.plan.k_layer_eff, "core_out")))
 
     # -- (2) selection ---------------------------------------------------------
     def select(self, v=None, a=None, keep_idx=None, keep_cnt=None, pack_pos=None, gather=None,
                cu_seqlens=None):
         c = self.c_cfg
         self._ok(self.lib.swam_select(
-            self.h, _ptr(v, torch.float32, c.batch * c.n_frames * self.n_s, "v"),
-            _ptr(a, torch.float32, c.batch * self.n_s, "a"),
+            self.h, _ptr(v, torch.float32, self.n_scored * c.n_frames * self.n_s, "v"),
+            _ptr(a, torch.float32, self.n_scored * self.n_s, "a"),
             _ptr(keep_idx, torch.int32, c.batch * c.n_frames * self.k_max, "keep_idx"),
             _ptr(keep_cnt, torch.int32, c.batch * c.n_frames, "keep_cnt"),
             _ptr(pack_pos, torch.int32, self.rows_full, "pack_pos"),
@@ -284,10 +294,10 @@ class Context:
         c = self.c_cfg
         n_s = self.n_s
         self._ok(self.lib.swam_export(
-            self.h, _ptr(s_all, torch.float32, c.batch * c.n_blocks * c.n_frames * n_s, "s_all"),
-            _ptr(q, torch.float32, c.batch * c.n_blocks, "q"),
-            _ptr(v, torch.float32, c.batch * c.n_frames * n_s, "v"),
-            _ptr(a, torch.float32, c.batch * n_s, "a"),
+            self.h, _ptr(s_all, torch.float32, self.n_scored * c.n_blocks * c.n_frames * n_s, "s_all"),
+            _ptr(q, torch.float32, self.n_scored * c.n_blocks, "q"),
+            _ptr(v, torch.float32, self.n_scored * c.n_frames * n_s, "v"),
+            _ptr(a, torch.float32, self.n_scored * n_s, "a"),
             _ptr(keep_idx, torch.int32, c.batch * c.n_frames * self.k_max, "keep_idx"),
             _ptr(keep_cnt, torch.int32, c.batch * c.n_frames, "keep_cnt"),
             _ptr(pack_pos, torch.int32, self.rows_full, "pack_pos"),
@@ -358,11 +368,17 @@ class Context:
 
     # -- sampling update -----------------------------------------------------------
     def _n_lat(self):
+        """Latent rows of every sequence (the rows of v)."""
         c = self.c_cfg
         return c.batch * (self.plan.l_full - c.n_ctx)
 
+    def _n_state(self):
+        """Latent rows of the state z and the velocity cache (one per pair
+        with guidance)."""
+        return self.n_scored * (self.plan.l_full - self.c_cfg.n_ctx)
+
     def embed(self, io: LatentIO, z, x_full):
-        n = self._n_lat() * io.d_latent
+        n = self._n_state() * io.d_latent
         self._ok(self.lib.swam_embed(self.h, C.byref(io.struct), _ptr(z, torch.float32, n, "z"),
                                      _ptr(x_full, self.act_dtype, self.rows_full * self.c_cfg.d_model,
                                           "x_full")))
@@ -374,21 +390,22 @@ class Context:
             int(bool(retained_only)), _ptr(v, torch.float32, self._n_lat() * io.d_latent, "v")))
 
     def sample_update(self, d_latent: int, v, v_cache, z, dsigma: float, kind: int):
-        n = self._n_lat() * d_latent
+        n = self._n_state() * d_latent
         self._ok(self.lib.swam_sample_update(
-            self.h, int(d_latent), _ptr(v, torch.float32, n, "v"),
+            self.h, int(d_latent), _ptr(v, torch.float32, self._n_lat() * d_latent, "v"),
             _ptr(v_cache, torch.float32, n, "v_cache"), _ptr(z, torch.float32, n, "z"),
             float(dsigma), int(kind)))
 
     def sample_step(self, model: Model, io: LatentIO, z, v, v_cache, x_full, y_full, temb,
                     tau: int, dsigma: float, flags: int = 0) -> int:
         c = self.c_cfg
-        n = self._n_lat() * io.d_latent
+        n = self._n_state() * io.d_latent
         nt = self.rows_full * c.d_model
         kind = C.c_int32(-1)
         self._ok(self.lib.swam_sample_step(
             self.h, C.byref(model.struct), C.byref(io.struct), _ptr(z, torch.float32, n, "z"),
-            _ptr(v, torch.float32, n, "v"), _ptr(v_cache, torch.float32, n, "v_cache"),
+            _ptr(v, torch.float32, self._n_lat() * io.d_latent, "v"),
+            _ptr(v_cache, torch.float32, n, "v_cache"),
             _ptr(x_full, self.act_dtype, nt, "x_full"), _ptr(y_full, self.act_dtype, nt, "y_full"),
             _ptr(temb, torch.float32, c.d_temb, "temb"), int(tau), float(dsigma), int(flags),
             C.byref(kind)))

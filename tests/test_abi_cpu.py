@@ -40,7 +40,8 @@ def test_status_strings(lib):
 
 
 @pytest.mark.parametrize("n,want", [(1, (152, 64, 20)), (2, (1312, 660, 93)), (3, (10160, 3472, 364)),
-                                    (5, (3360, -1, 768))])
+                                    (5, (3360, -1, 768)), (6, (3092, 1844, 184)),
+                                    (7, (326, 192, 31))])
 def test_plan_sizes(lib, n, want):
     from paper_2609_38984_amd import swam
     cfg = W.preset(n)
@@ -63,6 +64,10 @@ def test_plan_sizes(lib, n, want):
     (dict(frame_h=1, frame_w=1), -2),
     (dict(mass_threshold=1.5), -1),
     (dict(n_act=2 * 17, n_frames=2), -2),  # more than 16 queries per group
+    (dict(rope=2), -1),
+    (dict(qk_norm=-1), -1),
+    (dict(cfg_pairs=1, batch=3), -2),  # guidance pairs need an even batch
+    (dict(cfg_pairs=1, batch=2, guidance=float("nan")), -1),
     # bf16 QKV buffer beyond 2^31 elements: 64 x 4112 rows x 3 x 4096
     (dict(dtype=1, batch=64, n_heads=64, d_model=4096, n_frames=1, frame_h=64, frame_w=64,
           n_act=16, n_ctx=0, k_core=100, k_anchor=10), -2),

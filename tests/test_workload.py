@@ -52,3 +52,26 @@ def test_timestep_embedding():
     e = W.timestep_embedding(cfg, 0)
     assert e.shape == (128,)
     assert e[0] == np.float32(np.cos(1000.0)) and e[64] == np.float32(np.sin(1000.0))
+
+
+def test_multi_view_frames_concatenate_unequal_views():
+    for n, views, n_s in ((6, ((14, 14), (8, 9), (8, 9)), 340), (7, ((7, 7), (7, 7)), 98)):
+        cfg = W.preset(n)
+        assert cfg.views == views and cfg.n_s == n_s and (cfg.frame_h, cfg.frame_w) == (1, n_s)
+        grids = W.view_grids(cfg)
+        assert [g[0] for g in grids] == list(np.cumsum([0] + [h * w for h, w in views])[:-1])
+
+
+def test_multi_view_blobs_stay_inside_their_view():
+    cfg = W.preset(6).replace(n_blocks=1, d_model=128, n_heads=2)
+    inp = W.make_inputs(cfg)
+    grids = W.view_grids(cfg)
+    for b in range(cfg.batch):
+        base = inp.base[b][cfg.n_ctx:cfg.n_ctx + cfg.n_fut].reshape(cfg.n_frames, cfg.n_s, -1)
+        got = inp.x(0)[b * cfg.l_full + cfg.n_ctx:b * cfg.l_full + cfg.n_ctx + cfg.n_fut]
+        moved = np.abs(got.reshape(cfg.n_frames, cfg.n_s, -1) - W._storage(cfg, base)).max(axis=2) > 0
+        views = {bl.view for bl in inp.blobs[b]}
+        for v, (off, h, w) in enumerate(grids):
+            if v not in views:
+                assert not moved[:, off:off + h * w].any()
+        assert moved.any()

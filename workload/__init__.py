@@ -9,6 +9,9 @@ without sharing any code of the method.
 Token layout of one sequence (the paper leaves the order open; this is the
 reading adopted here): ``[context | future frames, frame-major, row-major inside
 a frame | action tokens]``.  Sequences of a batch are concatenated row-wise.
+A multi-view frame (several cameras of unequal resolution) is the views'
+row-major token grids concatenated, so a frame has N_s = sum_v h_v w_v tokens
+and is described to the step as one frame of 1 x N_s.
 
 Every array is float32.  For bf16 configurations every value is already on the
 bf16 grid (round-to-nearest-even), so converting to ``torch.bfloat16`` is exact.
@@ -24,7 +27,7 @@ import numpy as np
 __all__ = [
     "SwamConfig", "preset", "PRESETS", "budgets", "rng_for", "block_weights",
     "timestep_embedding", "StepInputs", "make_inputs", "blob_direction",
-    "time_embedding", "latent_io_weights", "SamplerInputs", "make_sampler_inputs",
+    "time_embedding", "latent_io_weights", "SamplerInputs", "make_sampler_inputs", "view_grids",
 ]
 
 
@@ -69,6 +72,9 @@ class SwamConfig:
     retain_percent: int = 0     # informational: per-frame core percent
     rope: int = 0               # backbone variant: rotary embedding at original positions
     qk_norm: int = 0            # backbone variant: RMS-normalised q and k per head
+    cfg_pairs: int = 0          # guidance: sequences [P, 2P) are the unconditional partners of [0, P)
+    guidance: float = 1.0       # guidance scale g of the sampler (with cfg_pairs)
+    views: tuple = ()           # multi-view frames: ((h, w), ...) per camera; frame is 1 x sum(h w)
 
     # derived sizes ----------------------------------------------------------
     @property
@@ -90,6 +96,12 @@ class SwamConfig:
     @property
     def k_ret(self) -> int:
         return self.k_core + self.k_anchor
+
+    @property
+    def n_scored(self) -> int:
+        """Sequences that are scored and selected: the conditional half with
+        guidance pairs, else every sequence."""
+        return self.batch // 2 if self.cfg_pairs else self.batch
 
     @property
     def t_pack_fixed(self) -> int:
@@ -153,11 +165,39 @@ def _cfg5() -> SwamConfig:
                       blob_sigma_range=(2.0, 6.0), mass_threshold=0.8)
 
 
-PRESETS = {1: _cfg1, 2: _cfg2, 3: _cfg3, 4: _cfg4, 5: _cfg5}
+def _cfg6() -> SwamConfig:
+    # three cameras (one wrist view and two smaller third-person views) of
+    # 340 tokens per future frame, 8 future frames, 4 denoising steps with one
+    # full step per chunk, K_c + K_s = 80 + 104, guidance pairs at scale 3.0,
+    # 28 blocks (the shape of the paper's 28-layer backbone, App. B.2 table)
+    views = ((14, 14), (8, 9), (8, 9))
+    n_s = sum(h * w for h, w in views)
+    return SwamConfig(name="bf16-28blk-d1536-3view-340tok-cfg3", batch=2, d_model=1536,
+                      n_heads=24, n_blocks=28, n_ctx=n_s, n_frames=8, frame_h=1, frame_w=n_s,
+                      n_act=32, k_core=80, k_anchor=104, reuse_R=4, n_steps=4, dtype="bf16",
+                      seed=6, blob_count=(1, 3), blob_sigma_range=(1.5, 3.0), views=views,
+                      cfg_pairs=1, guidance=3.0)
+
+
+def _cfg7() -> SwamConfig:
+    # two cameras of 98 tokens per future frame in total, 2 future frames,
+    # 16 aligned action queries per frame, 10 steps with one full step,
+    # K_c + K_s = 19 + 12, no guidance, 30 blocks (App. B.2 table)
+    views = ((7, 7), (7, 7))
+    n_s = sum(h * w for h, w in views)
+    return SwamConfig(name="bf16-30blk-d1536-2view-98tok", batch=1, d_model=1536,
+                      n_heads=24, n_blocks=30, n_ctx=n_s, n_frames=2, frame_h=1, frame_w=n_s,
+                      n_act=32, k_core=19, k_anchor=12, reuse_R=10, n_steps=10, dtype="bf16",
+                      seed=7, blob_count=(1, 2), blob_sigma_range=(1.0, 2.0), views=views)
+
+
+PRESETS = {1: _cfg1, 2: _cfg2, 3: _cfg3, 4: _cfg4, 5: _cfg5, 6: _cfg6, 7: _cfg7}
 
 
 def preset(n: int, **kw) -> SwamConfig:
-    """Named workload ``n`` (1..5); config 4 takes ``percent`` and ``reuse_R``."""
+    """Named workload ``n`` (1..7); config 4 takes ``percent`` and ``reuse_R``.
+    6 and 7 are multi-view workloads at the shapes of the paper's backbone
+    table (App. B.2)."""
     if n == 4:
         return _cfg4(**kw)
     cfg = PRESETS[n]()
@@ -244,6 +284,7 @@ class _Blob:
     sigma: float
     centers: np.ndarray   # [F][2] (row, col) at tau = 0
     dirs: np.ndarray      # [F][2] unit grid step per denoising step
+    view: int = -1        # multi-view frames: the camera the blob lives in
 
 
 @dataclass
@@ -270,8 +311,29 @@ class StepInputs:
         return timestep_embedding(self.cfg, tau)
 
 
+def view_grids(cfg: SwamConfig):
+    """(offset in the frame, h, w) of every camera view; one view of
+    frame_h x frame_w for single-view workloads."""
+    if not cfg.views:
+        return [(0, cfg.frame_h, cfg.frame_w)]
+    out, off = [], 0
+    for h, w in cfg.views:
+        out.append((off, h, w))
+        off += h * w
+    return out
+
+
 def _blob_weights(cfg: SwamConfig, blobs, tau: int) -> np.ndarray:
-    """Sum over blobs of exp(-dist^2 / (2 sigma^2)) on the torus, [F][N_s]."""
+    """Sum over blobs of exp(-dist^2 / (2 sigma^2)) on the torus of the blob's
+    view, [F][N_s]."""
+    if cfg.views:
+        acc = np.zeros((cfg.n_frames, cfg.n_s))
+        grids = view_grids(cfg)
+        for bl in blobs:
+            off, hh, ww = grids[bl.view]
+            sub = cfg.replace(frame_h=hh, frame_w=ww, views=())
+            acc[:, off:off + hh * ww] += _blob_weights(sub, [dataclasses.replace(bl, view=-1)], tau)
+        return acc
     hh, ww = cfg.frame_h, cfg.frame_w
     rows = np.arange(hh)[:, None].astype(np.float64)
     cols = np.arange(ww)[None, :].astype(np.float64)
@@ -334,10 +396,14 @@ def make_inputs(cfg: SwamConfig, w_qkv0: np.ndarray | None = None) -> StepInputs
                 sigma = float(rb.uniform(*cfg.blob_sigma_range))
             else:
                 sigma = float(cfg.blob_sigma)
-            centers = np.stack([rb.integers(0, cfg.frame_h, cfg.n_frames),
-                                rb.integers(0, cfg.frame_w, cfg.n_frames)], axis=1).astype(np.float64)
+            view, hh, ww = -1, cfg.frame_h, cfg.frame_w
+            if cfg.views:
+                view = int(rb.integers(0, len(cfg.views)))
+                hh, ww = cfg.views[view]
+            centers = np.stack([rb.integers(0, hh, cfg.n_frames),
+                                rb.integers(0, ww, cfg.n_frames)], axis=1).astype(np.float64)
             dirs = steps[rb.integers(0, 4, cfg.n_frames)]
-            blobs.append(_Blob(sigma=sigma, centers=centers, dirs=dirs))
+            blobs.append(_Blob(sigma=sigma, centers=centers, dirs=dirs, view=view))
         inp.blobs.append(blobs)
         inp.direction.append(blob_direction(cfg, w_qkv0, act))
     return inp
@@ -376,5 +442,6 @@ def make_sampler_inputs(cfg: SwamConfig, d_latent: int = 16) -> SamplerInputs:
     base = make_inputs(cfg)
     ctx = np.stack([b[:cfg.n_ctx] for b in base.base]).astype(np.float32)
     rng = rng_for(cfg, _STREAM_LATENT_Z)
-    z0 = rng.standard_normal((cfg.batch * (cfg.l_full - cfg.n_ctx), d_latent), dtype=np.float32)
+    # one latent state per pair with guidance (both branches denoise the same z)
+    z0 = rng.standard_normal((cfg.n_scored * (cfg.l_full - cfg.n_ctx), d_latent), dtype=np.float32)
     return SamplerInputs(ctx=_storage(cfg, ctx), z0=z0)
