@@ -69,13 +69,18 @@ __device__ __forceinline__ double warp_sum_d(double v) {
 // ---------------------------------------------------------------------------
 // launchers (host side), one per kernel family; all asynchronous on `st`
 // ---------------------------------------------------------------------------
-enum Epilogue { EPI_BIAS = 0, EPI_BIAS_GELU = 1, EPI_BIAS_GATED_RESIDUAL = 2 };
+// EPI_PARTIAL is internal to the bf16 split-K path (fp32 partial sums)
+enum Epilogue { EPI_BIAS = 0, EPI_BIAS_GELU = 1, EPI_BIAS_GATED_RESIDUAL = 2, EPI_PARTIAL = 3 };
 
 // C[M][N] = epi(A[M][K] . B[N][K]^T + bias[N]); for the gated residual
 // C[m][n] = C[m][n] + gate[n] * (acc + bias[n]) (C read then written).
+// ws / ws_floats: fp32 workspace the bf16 path may use to split K when the
+// output tiles alone cannot fill the CUs (partial sums, then one reduce +
+// epilogue pass); NULL or too small means no split.
 hipError_t launch_gemm(int dtype, int epi, const void* A, int64_t lda, const void* B,
                        int64_t ldb, const void* bias, const float* gate, void* C,
-                       int64_t ldc, int64_t M, int64_t N, int64_t K, hipStream_t st);
+                       int64_t ldc, int64_t M, int64_t N, int64_t K, hipStream_t st,
+                       float* ws = nullptr, int64_t ws_floats = 0);
 
 // mod[blk][6d] = W_ada[blk] SiLU(temb) + b_ada[blk] for n_blk blocks at once.
 struct AdalnArgs {

@@ -9,6 +9,9 @@
 // so that each XCD (dispatch round-robins over 8) receives a contiguous run
 // of tiles, grouped GROUP_M tile-rows deep, to share its L2.
 // Epilogues (bias, tanh-GELU, gated residual) are fused into the store.
+// Split K: when the output tiles cannot fill the 256 CUs (few rows, or a
+// narrow N), grid.y workgroups share a tile along K, store fp32 partial sums,
+// and one memory-bound pass sums them and applies the epilogue.
 #include "common.h"
 
 namespace swam {
@@ -88,7 +91,8 @@ template <int BM, int BN, int WM, int WN, int EPI>
 __global__ void __launch_bounds__(WM * WN * 64)
 gemm_bf16_nt(const bf16_t* __restrict__ A, int64_t lda, const bf16_t* __restrict__ B,
              int64_t ldb, const bf16_t* __restrict__ bias, const float* __restrict__ gate,
-             bf16_t* C, int64_t ldc, int M, int N, int K, int tiles_m, int tiles_n) {
+             bf16_t* C, int64_t ldc, int M, int N, int K, int tiles_m, int tiles_n,
+             float* __restrict__ part) {
   constexpr int NW = WM * WN;
   constexpr int TM = BM / WM, TN = BN / WN;
   constexpr int FM = TM / 32, FN = TN / 32;
@@ -134,13 +138,16 @@ gemm_bf16_nt(const bf16_t* __restrict__ A, int64_t lda, const bf16_t* __restrict
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
 
   constexpr int STAGE = (BM + BN) * 8;
-  const int KT = K / GEMM_BK;
-  issue(lds, lds + BM * 8, 0);
+  // k-stages of this workgroup: all of them, or split slice blockIdx.y of gridDim.y
+  const int KT_all = K / GEMM_BK;
+  const int kt0 = (int)((int64_t)KT_all * blockIdx.y / gridDim.y);
+  const int KT = (int)((int64_t)KT_all * (blockIdx.y + 1) / gridDim.y);
+  issue(lds, lds + BM * 8, kt0 * GEMM_BK);
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   __syncthreads();
-  for (int kt = 0; kt < KT; ++kt) {
-    uint4* cur = lds + (kt & 1) * STAGE;
-    uint4* nxt = lds + ((kt + 1) & 1) * STAGE;
+  for (int kt = kt0; kt < KT; ++kt) {
+    uint4* cur = lds + ((kt - kt0) & 1) * STAGE;
+    uint4* nxt = lds + ((kt - kt0 + 1) & 1) * STAGE;
     // prefetch stage kt + 1 into the other buffer (released by the previous barrier)
     if (kt + 1 < KT) issue(nxt, nxt + BM * 8, (kt + 1) * GEMM_BK);
     mma_stage<BM, BN, TM, TN, FM, FN>(cur, cur + BM * 8, wm, wn, lane, acc);
@@ -172,7 +179,12 @@ gemm_bf16_nt(const bf16_t* __restrict__ A, int64_t lda, const bf16_t* __restrict
     for (int c = lane; c < 32 * TN / 8; c += 64) {
       const int rl = c / (TN / 8), cl = (c % (TN / 8)) * 8;
       const int row = row0 + rl, col = col0 + cl;
-      if (row < M && col < N) {
+      if (EPI == EPI_PARTIAL && row < M && col < N) {
+        // fp32 partial sums of this K slice: part[slice][M][N]
+        float* q = part + ((int64_t)blockIdx.y * M + row) * N + col;
+        reinterpret_cast<float4*>(q)[0] = *reinterpret_cast<const float4*>(stage + rl * EP_LD + cl);
+        reinterpret_cast<float4*>(q)[1] = *reinterpret_cast<const float4*>(stage + rl * EP_LD + cl + 4);
+      } else if (EPI != EPI_PARTIAL && row < M && col < N) {
         const float4 v0 = *reinterpret_cast<const float4*>(stage + rl * EP_LD + cl);
         const float4 v1 = *reinterpret_cast<const float4*>(stage + rl * EP_LD + cl + 4);
         const float v[8] = {v0.x, v0.y, v0.z, v0.w, v1.x, v1.y, v1.z, v1.w};
@@ -202,6 +214,48 @@ gemm_bf16_nt(const bf16_t* __restrict__ A, int64_t lda, const bf16_t* __restrict
     }
     __builtin_amdgcn_wave_barrier();
   }
+}
+
+// Sum of the split-K partials and the epilogue: one thread per 8 columns of
+// a row (16-byte bias / residual loads and stores, 32-byte partial loads).
+template <int EPI>
+__global__ void __launch_bounds__(256)
+splitk_epilogue(const float* __restrict__ part, int splits, int M, int N,
+                const bf16_t* __restrict__ bias, const float* __restrict__ gate, bf16_t* C,
+                int64_t ldc) {
+  const int64_t id = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int cpr = N / 8;
+  if (id >= (int64_t)M * cpr) return;
+  const int row = (int)(id / cpr), col = (int)(id % cpr) * 8;
+  float v[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+  for (int z = 0; z < splits; ++z) {
+    const float* q = part + ((int64_t)z * M + row) * N + col;
+    const float4 a = reinterpret_cast<const float4*>(q)[0], b = reinterpret_cast<const float4*>(q)[1];
+    v[0] += a.x; v[1] += a.y; v[2] += a.z; v[3] += a.w;
+    v[4] += b.x; v[5] += b.y; v[6] += b.z; v[7] += b.w;
+  }
+  const uint4 bw = *reinterpret_cast<const uint4*>(bias + col);
+  const uint32_t bb[4] = {bw.x, bw.y, bw.z, bw.w};
+  bf16_t* p = C + (int64_t)row * ldc + col;
+  uint32_t rr[4] = {0u, 0u, 0u, 0u};
+  float gg[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+  if (EPI == EPI_BIAS_GATED_RESIDUAL) {
+    const uint4 rw = *reinterpret_cast<const uint4*>(p);
+    rr[0] = rw.x; rr[1] = rw.y; rr[2] = rw.z; rr[3] = rw.w;
+    const float4 g0 = *reinterpret_cast<const float4*>(gate + col);
+    const float4 g1 = *reinterpret_cast<const float4*>(gate + col + 4);
+    gg[0] = g0.x; gg[1] = g0.y; gg[2] = g0.z; gg[3] = g0.w;
+    gg[4] = g1.x; gg[5] = g1.y; gg[6] = g1.z; gg[7] = g1.w;
+  }
+  uint32_t out[4];
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const float b0 = __uint_as_float(bb[e] << 16), b1 = __uint_as_float(bb[e] & 0xFFFF0000u);
+    const float x0 = __uint_as_float(rr[e] << 16), x1 = __uint_as_float(rr[e] & 0xFFFF0000u);
+    out[e] = pack_bf16x2(epi_value<EPI>(v[2 * e], b0, gg[2 * e], x0),
+                         epi_value<EPI>(v[2 * e + 1], b1, gg[2 * e + 1], x1));
+  }
+  *reinterpret_cast<uint4*>(p) = make_uint4(out[0], out[1], out[2], out[3]);
 }
 
 // ---------------------------------------------------------------------------
@@ -261,35 +315,63 @@ gemm_f32_nt(const float* __restrict__ A, int64_t lda, const float* __restrict__ 
 template <int BM, int BN, int WM, int WN, int EPI>
 static hipError_t run_bf16(const void* A, int64_t lda, const void* B, int64_t ldb,
                            const void* bias, const float* gate, void* C, int64_t ldc, int M,
-                           int N, int K, hipStream_t st) {
+                           int N, int K, int splits, float* part, hipStream_t st) {
   const int tiles_m = (M + BM - 1) / BM, tiles_n = (N + BN - 1) / BN;
-  auto kern = gemm_bf16_nt<BM, BN, WM, WN, EPI>;
-  hipLaunchKernelGGL(kern, dim3(tiles_m * tiles_n), dim3(WM * WN * 64), 0, st,
-                     (const bf16_t*)A, lda, (const bf16_t*)B, ldb, (const bf16_t*)bias, gate,
-                     (bf16_t*)C, ldc, M, N, K, tiles_m, tiles_n);
+  if (splits <= 1) {
+    hipLaunchKernelGGL((gemm_bf16_nt<BM, BN, WM, WN, EPI>), dim3(tiles_m * tiles_n),
+                       dim3(WM * WN * 64), 0, st, (const bf16_t*)A, lda, (const bf16_t*)B, ldb,
+                       (const bf16_t*)bias, gate, (bf16_t*)C, ldc, M, N, K, tiles_m, tiles_n,
+                       (float*)nullptr);
+    return hipGetLastError();
+  }
+  hipLaunchKernelGGL((gemm_bf16_nt<BM, BN, WM, WN, EPI_PARTIAL>), dim3(tiles_m * tiles_n, splits),
+                     dim3(WM * WN * 64), 0, st, (const bf16_t*)A, lda, (const bf16_t*)B, ldb,
+                     (const bf16_t*)bias, gate, (bf16_t*)C, ldc, M, N, K, tiles_m, tiles_n, part);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const int64_t n = (int64_t)M * (N / 8);
+  hipLaunchKernelGGL(splitk_epilogue<EPI>, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st,
+                     part, splits, M, N, (const bf16_t*)bias, gate, (bf16_t*)C, ldc);
   return hipGetLastError();
 }
 
-// Tile choice: time ~ rounds * (per-CU work of one round / efficiency), where a
-// round places `per_cu` workgroups on each of the 256 CUs (LDS-limited) and the
-// efficiencies are the measured per-tile MFMA rates of the three kernels.
-static int choose_tile(int64_t M, int64_t N) {
-  static int forced = -2;
+// Tile and K-split choice: modelled time = rounds * (per-CU MFMA work of one
+// round / tile efficiency) + (split > 1) the partial-sum pass over HBM, where
+// a round places `per_cu` workgroups on each of the 256 CUs (LDS-limited),
+// the efficiencies are the measured per-tile MFMA rates of the three kernels
+// relative to a 40%-of-peak base, and the pass moves splits * M * N fp32
+// partials plus the bf16 output (and residual) at about 4 TB/s.
+struct GemmPlan { int tile, splits; };
+static GemmPlan choose_gemm(int64_t M, int64_t N, int64_t K, int64_t ws_floats) {
+  static int forced = -2, forced_split = -2;
   if (forced == -2) {
     const char* e = getenv("SWAM_GEMM_TILE");
     forced = e ? atoi(e) : -1;
+    const char* f = getenv("SWAM_GEMM_SPLIT");
+    forced_split = f ? atoi(f) : -1;
   }
-  if (forced >= 0 && forced <= 2) return forced;
   struct Cand { int bm, bn, per_cu; double eff; };
   const Cand c[3] = {{256, 256, 1, 1.0}, {256, 128, 1, 0.85}, {128, 128, 2, 0.75}};
-  int best = 0;
+  const int split_opts[6] = {1, 2, 3, 4, 6, 8};
+  const int64_t kt = K / GEMM_BK;
+  const double cu_flops = 2.5e15 / 256.0 * 0.40;        // sustained MFMA rate per CU
+  GemmPlan best{0, 1};
   double best_t = 1e30;
   for (int i = 0; i < 3; ++i) {
+    if (forced >= 0 && forced <= 2 && i != forced) continue;
     const int64_t tiles = ((M + c[i].bm - 1) / c[i].bm) * ((N + c[i].bn - 1) / c[i].bn);
     const int64_t slots = 256ll * c[i].per_cu;
-    const int64_t rounds = (tiles + slots - 1) / slots;
-    const double t = (double)rounds * c[i].bm * c[i].bn * c[i].per_cu / c[i].eff;
-    if (t < best_t) { best_t = t; best = i; }
+    for (int s : split_opts) {
+      if (forced_split >= 1 && s != forced_split) continue;
+      if (s > 1 && (kt / s < 4 || (int64_t)s * M * N > ws_floats)) continue;
+      const int64_t wgs = tiles * s;
+      const int64_t rounds = (wgs + slots - 1) / slots;
+      const double k_slice = (double)((kt + s - 1) / s) * GEMM_BK;
+      double t = (double)rounds * 2.0 * c[i].bm * c[i].bn * c[i].per_cu * k_slice /
+                 (cu_flops * c[i].eff);
+      if (s > 1) t += ((double)s * M * N * 4.0 + 4.0 * M * N) / 4.0e12 + 3e-6;
+      if (t < best_t) { best_t = t; best = {i, s}; }
+    }
   }
   return best;
 }
@@ -297,11 +379,13 @@ static int choose_tile(int64_t M, int64_t N) {
 template <int EPI>
 static hipError_t dispatch_bf16(const void* A, int64_t lda, const void* B, int64_t ldb,
                                 const void* bias, const float* gate, void* C, int64_t ldc,
-                                int M, int N, int K, hipStream_t st) {
-  switch (choose_tile(M, N)) {
-    case 0: return run_bf16<256, 256, 2, 4, EPI>(A, lda, B, ldb, bias, gate, C, ldc, M, N, K, st);
-    case 1: return run_bf16<256, 128, 4, 2, EPI>(A, lda, B, ldb, bias, gate, C, ldc, M, N, K, st);
-    default: return run_bf16<128, 128, 2, 2, EPI>(A, lda, B, ldb, bias, gate, C, ldc, M, N, K, st);
+                                int M, int N, int K, float* ws, int64_t ws_floats,
+                                hipStream_t st) {
+  const GemmPlan p = choose_gemm(M, N, K, ws ? ws_floats : 0);
+  switch (p.tile) {
+    case 0: return run_bf16<256, 256, 2, 4, EPI>(A, lda, B, ldb, bias, gate, C, ldc, M, N, K, p.splits, ws, st);
+    case 1: return run_bf16<256, 128, 4, 2, EPI>(A, lda, B, ldb, bias, gate, C, ldc, M, N, K, p.splits, ws, st);
+    default: return run_bf16<128, 128, 2, 2, EPI>(A, lda, B, ldb, bias, gate, C, ldc, M, N, K, p.splits, ws, st);
   }
 }
 
@@ -317,14 +401,15 @@ static hipError_t run_f32(const void* A, int64_t lda, const void* B, int64_t ldb
 
 hipError_t launch_gemm(int dtype, int epi, const void* A, int64_t lda, const void* B,
                        int64_t ldb, const void* bias, const float* gate, void* C,
-                       int64_t ldc, int64_t M, int64_t N, int64_t K, hipStream_t st) {
+                       int64_t ldc, int64_t M, int64_t N, int64_t K, hipStream_t st,
+                       float* ws, int64_t ws_floats) {
   if (M <= 0) return hipSuccess;
   const int m = (int)M, n = (int)N, k = (int)K;
   if (dtype == 1) {
     switch (epi) {
-      case EPI_BIAS: return dispatch_bf16<EPI_BIAS>(A, lda, B, ldb, bias, gate, C, ldc, m, n, k, st);
-      case EPI_BIAS_GELU: return dispatch_bf16<EPI_BIAS_GELU>(A, lda, B, ldb, bias, gate, C, ldc, m, n, k, st);
-      default: return dispatch_bf16<EPI_BIAS_GATED_RESIDUAL>(A, lda, B, ldb, bias, gate, C, ldc, m, n, k, st);
+      case EPI_BIAS: return dispatch_bf16<EPI_BIAS>(A, lda, B, ldb, bias, gate, C, ldc, m, n, k, ws, ws_floats, st);
+      case EPI_BIAS_GELU: return dispatch_bf16<EPI_BIAS_GELU>(A, lda, B, ldb, bias, gate, C, ldc, m, n, k, ws, ws_floats, st);
+      default: return dispatch_bf16<EPI_BIAS_GATED_RESIDUAL>(A, lda, B, ldb, bias, gate, C, ldc, m, n, k, ws, ws_floats, st);
     }
   }
   switch (epi) {

@@ -25,12 +25,13 @@ thread_local std::string g_err;
 struct Derived {
   int64_t n_s, g, l_full, rows_full, k_max, k_eff, d, hidden, esz, t_pack_fixed;
   int64_t n_scored;   // sequences that are scored and selected (the conditional half with pairs)
+  int64_t splitk_floats;  // fp32 workspace of the split-K GEMM path (bf16 only)
   int mass_num, mass_den;
 };
 
 // workspace layout (offsets into one arena)
 struct Layout {
-  size_t qkv, h, o, u, xp, lse, mod, alpha, rope, lse_act, lse_part, s_all, q, qd, core, v, a, vall,
+  size_t qkv, h, o, u, xp, lse, mod, alpha, rope, splitk, lse_act, lse_part, s_all, q, qd, core, v, a, vall,
       fsum, fent, pool, corefl, keep_idx, keep_cnt, keep, pack_pos, gather, cu_packed, cu_dense, total;
 };
 
@@ -92,6 +93,10 @@ int derive(const swam_config* c, Derived* dv, std::string* err) {
     return fail(err, SWAM_E_SHAPE, "batch * tokens * 3 * d_model must stay below 2^31");
   dv->n_s = n_s;
   dv->n_scored = c->cfg_pairs ? c->batch / 2 : c->batch;
+  // split-K partial sums: up to 8 slices of the widest projection, at most 128 MB
+  dv->splitk_floats = c->dtype == SWAM_BF16
+      ? std::min<int64_t>(8 * rows * std::max<int64_t>(3 * d, (int64_t)c->mlp_ratio * d), 32ll << 20)
+      : 0;
   dv->g = g;
   dv->l_full = l_full;
   dv->rows_full = rows;
@@ -139,6 +144,7 @@ Layout layout_for(const swam_config* c, const Derived& dv) {
   // positions up to batch * l_full - 1: a cu_seqlens sequence of swam_block may
   // span every row of the workspace
   L.rope = take(c->rope ? dv.rows_full * 32 * 8 : 0);
+  L.splitk = take(dv.splitk_floats * 4);
   L.lse_act = take(B * c->n_act * c->n_heads * 4);
   L.lse_part = take(B * chunks * c->n_act * c->n_heads * 2 * 4);
   L.s_all = take(B * Lb * F * dv.n_s * 4);
@@ -248,6 +254,8 @@ int run_block(swam_ctx* c, const swam_block_weights* w, const float* mod, void* 
   void* o = c->ptr<char>(c->lay.o);
   void* u = c->ptr<char>(c->lay.u);
   hipStream_t st = c->st;
+  float* sk = c->ptr<float>(c->lay.splitk);
+  const int64_t sk_n = c->dv.splitk_floats;
   const float *sh1 = mod, *sc1 = mod + d, *g1 = mod + 2 * d;
   const float *sh2 = mod + 3 * d, *sc2 = mod + 4 * d, *g2 = mod + 5 * d;
   if (n_rows <= 0) return SWAM_OK;
@@ -258,7 +266,7 @@ int run_block(swam_ctx* c, const swam_block_weights* w, const float* mod, void* 
   {
     Timed t(c, SWAM_T_GEMM_QKV);
     SWAM_HIP(c, launch_gemm(dt, EPI_BIAS, h, d, w->w_qkv, d, w->b_qkv, nullptr, qkv, 3 * d,
-                            n_rows, 3 * d, d, st), "gemm qkv");
+                            n_rows, 3 * d, d, st, sk, sk_n), "gemm qkv");
   }
   if (c->cfg.rope || c->cfg.qk_norm) {
     Timed t(c, SWAM_T_QK_POST);
@@ -277,7 +285,7 @@ int run_block(swam_ctx* c, const swam_block_weights* w, const float* mod, void* 
   {
     Timed t(c, SWAM_T_GEMM_OUT);
     SWAM_HIP(c, launch_gemm(dt, EPI_BIAS_GATED_RESIDUAL, o, d, w->w_o, d, w->b_o, g1, x, d,
-                            n_rows, d, d, st), "gemm out");
+                            n_rows, d, d, st, sk, sk_n), "gemm out");
   }
   {
     Timed t(c, SWAM_T_LNMOD);
@@ -286,12 +294,12 @@ int run_block(swam_ctx* c, const swam_block_weights* w, const float* mod, void* 
   {
     Timed t(c, SWAM_T_GEMM_UP);
     SWAM_HIP(c, launch_gemm(dt, EPI_BIAS_GELU, h, d, w->w_1, d, w->b_1, nullptr, u, hid, n_rows,
-                            hid, d, st), "gemm up");
+                            hid, d, st, sk, sk_n), "gemm up");
   }
   {
     Timed t(c, SWAM_T_GEMM_DOWN);
     SWAM_HIP(c, launch_gemm(dt, EPI_BIAS_GATED_RESIDUAL, u, hid, w->w_2, hid, w->b_2, g2, x, d,
-                            n_rows, d, hid, st), "gemm down");
+                            n_rows, d, hid, st, sk, sk_n), "gemm down");
   }
   return SWAM_OK;
 }
