@@ -12,5 +12,5 @@ from .swam_oracle import (  # noqa: F401
     pack_map, PackMap, pack, unpack, dense_cu, run_blocks, dense_step, layer_scores,
     selection_from_scores, refresh_step, sparse_step, is_refresh, run_schedule,
     RefreshResult, overlap, rope_angles, apply_rope, qk_rms_norm, qk_post, dense_positions,
-    n_scored,
+    n_scored, philox4x64_10, random_keys, random_selection,
 )

@@ -507,6 +507,63 @@ def select(V, A, k_core, k_anchor, mass_threshold=0.0):
 
 
 # ---------------------------------------------------------------------------
+# random-selection baseline (the component ablation compares against tokens
+# chosen at random at the same per-frame budget)
+# ---------------------------------------------------------------------------
+PHILOX_M = (0xD2E7470EE14C6C93, 0xCA5A826395121157)   # Philox4x64 round multipliers
+PHILOX_W = (0x9E3779B97F4A7C15, 0xBB67AE8584CAA73B)   # Philox4x64 key increments
+_M32 = np.uint64(0xFFFFFFFF)
+
+
+def _mulhilo64(a, b):
+    """(high, low) 64-bit halves of the 128-bit product of uint64 arrays."""
+    a = np.asarray(a, np.uint64)
+    b = np.uint64(b)
+    a0, a1 = a & _M32, a >> np.uint64(32)
+    b0, b1 = b & _M32, b >> np.uint64(32)
+    p00, p01, p10, p11 = a0 * b0, a0 * b1, a1 * b0, a1 * b1
+    mid = (p00 >> np.uint64(32)) + (p01 & _M32) + (p10 & _M32)
+    hi = p11 + (p01 >> np.uint64(32)) + (p10 >> np.uint64(32)) + (mid >> np.uint64(32))
+    return hi, a * b
+
+
+def philox4x64_10(counter, key):
+    """Philox4x64 with 10 rounds (the counter-based generator of Salmon et al.,
+    SC 2011): each round multiplies words 0 and 2 by the round constants,
+    crosses the halves with words 1 and 3 and the key, and bumps the key by
+    the Weyl increments.  counter: [n][4] uint64, key: 2 ints -> [n][4]."""
+    x = [np.asarray(c, np.uint64).copy() for c in np.asarray(counter, np.uint64).T]
+    k0, k1 = int(key[0]) & ((1 << 64) - 1), int(key[1]) & ((1 << 64) - 1)
+    with np.errstate(over="ignore"):
+        for _ in range(10):
+            hi0, lo0 = _mulhilo64(x[0], PHILOX_M[0])
+            hi1, lo1 = _mulhilo64(x[2], PHILOX_M[1])
+            x = [hi1 ^ x[1] ^ np.uint64(k0), lo1, hi0 ^ x[3] ^ np.uint64(k1), lo0]
+            k0 = (k0 + PHILOX_W[0]) & ((1 << 64) - 1)
+            k1 = (k1 + PHILOX_W[1]) & ((1 << 64) - 1)
+    return np.stack(x, axis=1)
+
+
+def random_keys(seed, n_seqs, F, N_s):
+    """Uniform keys in [0, 1) on the float32 grid for every (sequence, frame,
+    position): word 0 of Philox4x64-10 at counter (index, 0, 0, 0), key
+    (seed, 0), top 24 bits scaled by 2^-24.  [n_seqs][F][N_s] float32."""
+    n = n_seqs * F * N_s
+    ctr = np.zeros((n, 4), np.uint64)
+    ctr[:, 0] = np.arange(n, dtype=np.uint64)
+    w = philox4x64_10(ctr, (seed, 0))[:, 0]
+    u = (w >> np.uint64(40)).astype(np.float64) * 2.0 ** -24
+    return u.astype(np.float32).reshape(n_seqs, F, N_s)
+
+
+def random_selection(keys, k_ret):
+    """Per frame the k_ret positions of largest key (ties to the lower index): a uniformly random subset of the frame, independent across
+    frames; expressed as the selection with V = keys, K_c = k_ret, K_s = 0."""
+    keys = np.asarray(keys, np.float32)
+    return select(keys, np.zeros(keys.shape[1], np.float32), k_ret, 0)
+
+
+# ---------------------------------------------------------------------------
 # packing metadata, pack and scatter (Sec. 4.2 compact execution)
 # ---------------------------------------------------------------------------
 def keep_mask(cfg, retained_per_seq):
