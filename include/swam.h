@@ -230,6 +230,19 @@ int swam_select(swam_ctx* ctx, const float* v, const float* a, int32_t* keep_idx
                 int32_t* keep_cnt, int32_t* pack_pos, int32_t* gather,
                 int32_t* cu_seqlens);
 
+/* Random-selection baseline (the component ablation compares the method
+ * with tokens chosen at random at the same per-frame budget): per scored
+ * sequence and frame, the K_c + K_s positions with the largest uniform keys
+ * (ties to the lower index), i.e. a uniformly random subset drawn
+ * independently per frame, no anchors.  The keys are the top 24 bits of word
+ * 0 of Philox4x64-10 (Salmon et al., SC 2011) at counter
+ * ((b * F + f) * N_s + j, 0, 0, 0) and key (seed, 0), times 2^-24; they
+ * replace the context's V (A is cleared).  Outputs as in swam_select; the
+ * selection is cached for sparse steps (with guidance pairs the partner
+ * shares it).  SWAM_E_UNSUPPORTED in mass-threshold mode. */
+int swam_select_random(swam_ctx* ctx, uint64_t seed, int32_t* keep_idx, int32_t* keep_cnt,
+                       int32_t* pack_pos, int32_t* gather, int32_t* cu_seqlens);
+
 /* Import a selection (int32 [B][F][k_max] ascending, -1 padded; counts
  * [B][F]; with guidance pairs B is the whole batch, partners included) and
  * rebuild the packing metadata.  Indices outside [0, N_s) are

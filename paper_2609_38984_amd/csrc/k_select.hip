@@ -621,4 +621,34 @@ hipError_t launch_copy(const void* src, void* dst, int64_t bytes, hipStream_t st
   return hipGetLastError();
 }
 
+// Random-selection baseline: one Philox4x64-10 evaluation (Salmon et al.,
+// SC 2011: ten rounds of two 64x64 -> 128-bit products crossed with the other
+// two words and a Weyl-stepped key) per (sequence, frame, position); the
+// selection then takes the largest keys per frame.
+__global__ void __launch_bounds__(256)
+random_keys_kernel(float* __restrict__ v, int64_t n, uint64_t seed) {
+  const int64_t id = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (id >= n) return;
+  uint64_t x0 = (uint64_t)id, x1 = 0, x2 = 0, x3 = 0, k0 = seed, k1 = 0;
+#pragma unroll
+  for (int r = 0; r < 10; ++r) {
+    const uint64_t lo0 = 0xD2E7470EE14C6C93ull * x0, hi0 = __umul64hi(0xD2E7470EE14C6C93ull, x0);
+    const uint64_t lo1 = 0xCA5A826395121157ull * x2, hi1 = __umul64hi(0xCA5A826395121157ull, x2);
+    x0 = hi1 ^ x1 ^ k0;
+    x1 = lo1;
+    x2 = hi0 ^ x3 ^ k1;
+    x3 = lo0;
+    k0 += 0x9E3779B97F4A7C15ull;
+    k1 += 0xBB67AE8584CAA73Bull;
+  }
+  v[id] = (float)(uint32_t)(x0 >> 40) * 0x1p-24f;
+}
+
+hipError_t launch_random_keys(float* v, int64_t n, uint64_t seed, hipStream_t st) {
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(random_keys_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, v, n,
+                     seed);
+  return hipGetLastError();
+}
+
 }  // namespace swam

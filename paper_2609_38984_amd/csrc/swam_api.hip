@@ -349,7 +349,8 @@ int read_packed_rows(swam_ctx* c) {
   return SWAM_OK;
 }
 
-int run_select(swam_ctx* c, const float* v, const float* a) {
+// k_core / k_anchor < 0: the configured budgets
+int run_select(swam_ctx* c, const float* v, const float* a, int k_core = -1, int k_anchor = -1) {
   const swam_config& cf = c->cfg;
   SelectArgs s{};
   s.v = v;
@@ -362,8 +363,8 @@ int run_select(swam_ctx* c, const float* v, const float* a) {
   s.B = (int)c->dv.n_scored;
   s.F = cf.n_frames;
   s.n_s = (int)c->dv.n_s;
-  s.k_core = cf.k_core;
-  s.k_anchor = cf.k_anchor;
+  s.k_core = k_core >= 0 ? k_core : cf.k_core;
+  s.k_anchor = k_anchor >= 0 ? k_anchor : cf.k_anchor;
   s.k_max = (int)c->dv.k_max;
   s.mass_num = c->dv.mass_num;
   s.mass_den = c->dv.mass_den;
@@ -578,6 +579,26 @@ int swam_select(swam_ctx* c, const float* v, const float* a, int32_t* keep_idx,
     a = c->ptr<float>(c->lay.a);
   }
   int rc = run_select(c, v, a);
+  if (rc != SWAM_OK) return rc;
+  return swam_export(c, nullptr, nullptr, nullptr, nullptr, keep_idx, keep_cnt, pack_pos, gather,
+                     cu_seqlens);
+}
+
+int swam_select_random(swam_ctx* c, uint64_t seed, int32_t* keep_idx, int32_t* keep_cnt,
+                       int32_t* pack_pos, int32_t* gather, int32_t* cu_seqlens) {
+  if (!c) return set_err(nullptr, SWAM_E_INVALID, "ctx is NULL");
+  if (c->dv.mass_den > 0)
+    return set_err(c, SWAM_E_UNSUPPORTED, "random selection needs fixed budgets (mass_threshold 0)");
+  const swam_config& cf = c->cfg;
+  const int64_t n = c->dv.n_scored * cf.n_frames * c->dv.n_s;
+  {
+    Timed t(c, SWAM_T_SELECT);
+    SWAM_HIP(c, launch_random_keys(c->ptr<float>(c->lay.v), n, seed, c->st), "random keys");
+    SWAM_HIP(c, hipMemsetAsync(c->ptr<float>(c->lay.a), 0, c->dv.n_scored * c->dv.n_s * 4, c->st),
+             "clear anchor keys");
+  }
+  int rc = run_select(c, c->ptr<float>(c->lay.v), c->ptr<float>(c->lay.a),
+                      cf.k_core + cf.k_anchor, 0);
   if (rc != SWAM_OK) return rc;
   return swam_export(c, nullptr, nullptr, nullptr, nullptr, keep_idx, keep_cnt, pack_pos, gather,
                      cu_seqlens);

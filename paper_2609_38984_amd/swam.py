@@ -29,7 +29,7 @@ EXPORTS = ["swam_create", "swam_destroy", "swam_set_stream", "swam_plan", "swam_
            "swam_set_selection", "swam_packed_rows", "swam_export", "swam_pack", "swam_unpack",
            "swam_block", "swam_step", "swam_step_graph", "swam_graph_clear", "swam_timer_enable",
            "swam_timer_reset", "swam_timer_read", "swam_embed", "swam_velocity",
-           "swam_sample_update", "swam_sample_step", "swam_overlap"]
+           "swam_sample_update", "swam_sample_step", "swam_overlap", "swam_select_random"]
 
 # the flow-schedule shift of the paper's backbones (App. B.2)
 SCHEDULE_SHIFT = 5.0
@@ -118,6 +118,7 @@ def load_library(path: str = LIB_PATH):
         "swam_score": [P, P, I64, I64, P, I64, I64, P, P, I64, P],
         "swam_score_reduce": [P, P, P, P, P, P],
         "swam_select": [P, P, P, P, P, P, P, P],
+        "swam_select_random": [P, C.c_uint64, P, P, P, P, P],
         "swam_set_selection": [P, P, P],
         "swam_packed_rows": [P, C.POINTER(I64)],
         "swam_export": [P, P, P, P, P, P, P, P, P, P],
@@ -272,6 +273,18 @@ class Context:
         self._ok(self.lib.swam_select(
             self.h, _ptr(v, torch.float32, self.n_scored * c.n_frames * self.n_s, "v"),
             _ptr(a, torch.float32, self.n_scored * self.n_s, "a"),
+            _ptr(keep_idx, torch.int32, c.batch * c.n_frames * self.k_max, "keep_idx"),
+            _ptr(keep_cnt, torch.int32, c.batch * c.n_frames, "keep_cnt"),
+            _ptr(pack_pos, torch.int32, self.rows_full, "pack_pos"),
+            _ptr(gather, torch.int32, self.rows_full, "gather"),
+            _ptr(cu_seqlens, torch.int32, c.batch + 1, "cu_seqlens")))
+
+    def select_random(self, seed: int, keep_idx=None, keep_cnt=None, pack_pos=None, gather=None,
+                      cu_seqlens=None):
+        """Random-selection baseline at the configured budget K_c + K_s."""
+        c = self.c_cfg
+        self._ok(self.lib.swam_select_random(
+            self.h, int(seed) & ((1 << 64) - 1),
             _ptr(keep_idx, torch.int32, c.batch * c.n_frames * self.k_max, "keep_idx"),
             _ptr(keep_cnt, torch.int32, c.batch * c.n_frames, "keep_cnt"),
             _ptr(pack_pos, torch.int32, self.rows_full, "pack_pos"),
