@@ -55,32 +55,52 @@ __device__ __forceinline__ void tile_of(int pid, int nwg, int tiles_m, int tiles
 typedef __attribute__((address_space(3))) void lds_void_t;
 typedef __attribute__((address_space(1))) void glb_void_t;
 
-// one k-stage (64) of MFMAs from a staged A/B tile pair
+// one k-stage (64) of MFMAs from a staged A/B tile pair.  The operand
+// fragments of k-step s + 1 are read from LDS while the MFMAs of k-step s
+// run (two fragment sets), and the schedule interleaves one LDS read after
+// each MFMA so the reads never queue behind a whole MFMA group.
 template <int BM, int BN, int TM, int TN, int FM, int FN>
 __device__ __forceinline__ void mma_stage(const uint4* __restrict__ as, const uint4* __restrict__ bs,
                                           int wm, int wn, int lane, f32x16 (&acc)[FM][FN]) {
+  static_assert(FM * FN >= FM + FN, "interleave needs an MFMA per fragment read");
+  constexpr int KS = GEMM_BK / 16;
   const int khalf = lane >> 5, r31 = lane & 31;
   const int sw = lds_swz(r31);   // rows differ from r31 by multiples of 32
-#pragma unroll
-  for (int s = 0; s < GEMM_BK / 16; ++s) {
+  bf16x8 af[2][FM], bfr[2][FN];
+  auto load = [&](int s, int buf) {
     const int chunk = (2 * s + khalf) ^ sw;
-    bf16x8 af[FM], bfr[FN];
 #pragma unroll
-    for (int i = 0; i < FM; ++i) {
-      const int row = wm * TM + i * 32 + r31;
-      af[i] = __builtin_bit_cast(bf16x8, as[row * 8 + chunk]);
-    }
+    for (int i = 0; i < FM; ++i)
+      af[buf][i] = __builtin_bit_cast(bf16x8, as[(wm * TM + i * 32 + r31) * 8 + chunk]);
 #pragma unroll
-    for (int j = 0; j < FN; ++j) {
-      const int row = wn * TN + j * 32 + r31;
-      bfr[j] = __builtin_bit_cast(bf16x8, bs[row * 8 + chunk]);
-    }
+    for (int j = 0; j < FN; ++j)
+      bfr[buf][j] = __builtin_bit_cast(bf16x8, bs[(wn * TN + j * 32 + r31) * 8 + chunk]);
+  };
+  load(0, 0);
+#pragma unroll
+  for (int s = 0; s < KS; ++s) {
+    if (s + 1 < KS) load(s + 1, (s + 1) & 1);
 #pragma unroll
     for (int i = 0; i < FM; ++i)
 #pragma unroll
       for (int j = 0; j < FN; ++j)
-        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[s & 1][i], bfr[s & 1][j], acc[i][j],
+                                                            0, 0, 0);
   }
+  // schedule: the first fragment set, then per k-step (MFMA, LDS read) pairs
+  // for the next set followed by the remaining MFMAs; the last k-step's MFMAs
+  __builtin_amdgcn_sched_group_barrier(0x100, FM + FN, 0);
+#pragma unroll
+  for (int s = 0; s + 1 < KS; ++s) {
+#pragma unroll
+    for (int r = 0; r < FM + FN; ++r) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+    }
+    if constexpr (FM * FN > FM + FN)
+      __builtin_amdgcn_sched_group_barrier(0x008, FM * FN - (FM + FN), 0);
+  }
+  __builtin_amdgcn_sched_group_barrier(0x008, FM * FN, 0);
 }
 
 // Stage loads go global -> LDS directly (no registers): each instruction moves
