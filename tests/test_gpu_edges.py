@@ -1,0 +1,71 @@
+"""Degenerate cases of the step on the GPU against the oracle (fp32, outputs
+1e-4 max-relative, selection bit-exact, pruned rows byte-identical): no
+retained future token, no context, a single 7-token frame, two-token frames,
+one action query per frame, a mass threshold of 1, and a zero-row block."""
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+import workload as W
+from helpers import dev, host, maxrel, model_for
+
+pytestmark = pytest.mark.gpu
+
+BASE = W.preset(1)
+CASES = {
+    "no_future_token_kept": BASE.replace(k_core=0, k_anchor=0),
+    "no_context": BASE.replace(n_ctx=0),
+    "one_frame_of_7": BASE.replace(n_frames=1, frame_h=1, frame_w=7, n_act=4, k_core=3, k_anchor=2),
+    "two_token_frames": BASE.replace(frame_h=1, frame_w=2, k_core=1, k_anchor=1),
+    "one_query_per_frame": BASE.replace(n_act=2),
+    "mass_threshold_one": BASE.replace(mass_threshold=1.0, k_core=64, k_anchor=0),
+}
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    torch.cuda.set_device(0)
+
+
+@pytest.mark.parametrize("name", list(CASES))
+def test_degenerate_schedule_matches_oracle(name):
+    from paper_2609_38984_amd import swam
+    cfg = CASES[name]
+    print(f"edge case {name}: L_full={cfg.l_full} N_s={cfg.n_s} F={cfg.n_frames} H={cfg.n_act}",
+          flush=True)
+    blocks, _, model = model_for(cfg)
+    inp = W.make_inputs(cfg, blocks[0]["w_qkv"])
+    ys, refr = O.run_schedule(cfg, blocks, inp.x, inp.temb)
+    ctx = swam.Context(cfg)
+    for tau in range(cfg.n_steps):
+        x = dev(inp.x(tau))
+        y = torch.empty_like(x)
+        kind = ctx.step(model, x, dev(inp.temb(tau)), tau, y)
+        torch.cuda.synchronize()
+        err = maxrel(host(y), ys[tau])
+        print(f"  tau {tau} kind {kind} max-rel {err:.2e}", flush=True)
+        assert err < 1e-4
+        if tau in refr:
+            pp = torch.empty(cfg.l_full, dtype=torch.int32, device="cuda:0")
+            ctx.export(pack_pos=pp)
+            torch.cuda.synchronize()
+            np.testing.assert_array_equal(pp.cpu().numpy(), refr[tau].packmap.pack_pos)
+            assert ctx.packed_rows() == int(refr[tau].packmap.cu_seqlens[-1])
+        else:
+            pruned = refr[cfg.reuse_R * (tau // cfg.reuse_R)].packmap.pack_pos < 0
+            assert y.cpu().numpy()[pruned].tobytes() == x.cpu().numpy()[pruned].tobytes()
+
+
+def test_block_with_zero_rows_is_a_no_op():
+    cfg = BASE
+    _, dblocks, _ = model_for(cfg, 1)
+    from paper_2609_38984_amd import swam
+    ctx = swam.Context(cfg)
+    x = torch.full((4, cfg.d_model), 3.0, device="cuda:0")
+    cu = torch.zeros(2, dtype=torch.int32, device="cuda:0")
+    ctx.block(dblocks[0], dev(W.timestep_embedding(cfg, 0)), x, 0, cu, 1)
+    torch.cuda.synchronize()
+    assert (x == 3.0).all()
