@@ -4,6 +4,8 @@
 //             fp32 latents, x = z W_in^T + b_in, stored in the config dtype;
 //   velocity: v = LN(y) W_v^T + b_v for every latent row, or only for the rows
 //             of the cached selection (retained future tokens and actions);
+//             bf16 on the matrix cores (16 rows per wave), fp32 one row per
+//             wave on the vector units;
 //   update  : with guidance pairs the two branch velocities of a latent row
 //             are first combined as v_u + g (v_c - v_u); a full step stores the
 //             future velocities in the cache; a sparse step uses the current
@@ -87,10 +89,10 @@ embed_kernel(const float* __restrict__ z, const T* __restrict__ w_in, const T* _
 }
 
 // c in {8, 16}: each thread keeps the W_in rows of its 8 columns in registers
-// and walks EMB_ROWS consecutive latent rows (the weights are read once per
-// thread instead of once per row; the z row is the same address across the
-// wave and 64 lanes store one contiguous kilobyte of x per row).
-constexpr int EMB_ROWS = 32;
+// and walks EMB_ROWS consecutive latent rows, four at a time (the weights are
+// read once per thread instead of once per row; the z row is the same address
+// across the wave and 64 lanes store one contiguous kilobyte of x per row).
+constexpr int EMB_ROWS = 16;
 template <typename T, int C>
 __global__ void __launch_bounds__(256)
 embed_reg_kernel(const float* __restrict__ z, const T* __restrict__ w_in, const T* __restrict__ b_in,
@@ -114,6 +116,7 @@ embed_reg_kernel(const float* __restrict__ z, const T* __restrict__ w_in, const 
     }
   load8(b_in + col, bb);
   const int64_t i1 = i0 + EMB_ROWS < n_lat_rows ? i0 + EMB_ROWS : n_lat_rows;
+#pragma unroll 4
   for (int64_t i = i0; i < i1; ++i) {
     const int64_t b = i / l_lat;
     const int64_t row = b * l_full + n_ctx + (i - b * l_lat);
@@ -235,6 +238,123 @@ velocity_kernel(const T* __restrict__ y, const int32_t* __restrict__ gather, int
   }
 }
 
+// bf16 read-out on the matrix cores: one workgroup per 16 rows, 16x16 tiles
+// of y . W_v^T by 16x16x32 MFMAs along d, the 32-column chunks of d dealt
+// round-robin to the VEL_WAVES waves (lane l feeds row l & 15 and eight
+// consecutive columns of its k-group l >> 4; W_v rows are the B operand,
+// read straight from L2).  The row sums and sums of squares and the column
+// sums of W_v come from the same fragments; the waves' partials are added
+// in LDS in a fixed order and
+//   v = rstd * (y . W_v^T - mean * sum_k W_v) + b_v,  rstd = 1/sqrt(var + eps)
+// gives LN(y) W_v^T + b_v without a second pass over the row.
+constexpr int VEL_WAVES = 4;
+template <int NT>
+__global__ void __launch_bounds__(64 * VEL_WAVES)
+velocity_mfma_kernel(const bf16_t* __restrict__ y, const int32_t* __restrict__ gather, int n_items,
+                     const bf16_t* __restrict__ w_v, const bf16_t* __restrict__ b_v,
+                     float* __restrict__ v, int l_lat, int l_full, int n_ctx, int c, int d) {
+  constexpr int NP = 5 * NT + 2;                 // partials per lane: acc, column sums, s1, s2
+  __shared__ float red[VEL_WAVES - 1][NP][64];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int r = lane & 15, kg = lane >> 4;
+  const int item = blockIdx.x * 16 + r;
+  int row = 0, lat = -1;                         // lat < 0: nothing to write for this row
+  if (item < n_items) {
+    if (gather == nullptr) {
+      const int b = item / l_lat;
+      lat = item;
+      row = b * l_full + n_ctx + (item - b * l_lat);
+    } else {
+      row = gather[item];
+      const int b = row / l_full, in_seq = row - b * l_full;
+      lat = in_seq < n_ctx ? -1 : b * l_lat + (in_seq - n_ctx);   // context rows carry no latent
+    }
+  }
+  const bf16_t* yr = y + (int64_t)row * d + 8 * kg;
+  f32x4 acc[NT];
+  float cs[NT];
+#pragma unroll
+  for (int t = 0; t < NT; ++t) {
+    acc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+    cs[t] = 0.f;
+  }
+  float s1 = 0.f, s2 = 0.f;
+#pragma unroll 2
+  for (int k0 = 32 * wave; k0 < d; k0 += 32 * VEL_WAVES) {
+    const uint4 a = *reinterpret_cast<const uint4*>(yr + k0);
+    const uint32_t aw[4] = {a.x, a.y, a.z, a.w};
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const float lo = __uint_as_float(aw[e] << 16), hi = __uint_as_float(aw[e] & 0xFFFF0000u);
+      s1 += lo + hi;
+      s2 = fmaf(lo, lo, fmaf(hi, hi, s2));
+    }
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
+      const int n = t * 16 + r;
+      uint4 w = make_uint4(0u, 0u, 0u, 0u);
+      if (n < c) w = *reinterpret_cast<const uint4*>(w_v + (int64_t)n * d + k0 + 8 * kg);
+      const uint32_t ww[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        cs[t] += __uint_as_float(ww[e] << 16) + __uint_as_float(ww[e] & 0xFFFF0000u);
+      acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a),
+                                                       __builtin_bit_cast(bf16x8, w), acc[t], 0, 0, 0);
+    }
+  }
+  // the waves' partial sums, added by wave 0 in wave order
+  if (wave > 0) {
+    float* q = &red[wave - 1][0][lane];
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) q[(4 * t + i) * 64] = acc[t][i];
+      q[(4 * NT + t) * 64] = cs[t];
+    }
+    q[(5 * NT) * 64] = s1;
+    q[(5 * NT + 1) * 64] = s2;
+  }
+  __syncthreads();
+  if (wave > 0) return;
+  for (int w = 0; w < VEL_WAVES - 1; ++w) {
+    const float* q = &red[w][0][lane];
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) acc[t][i] += q[(4 * t + i) * 64];
+      cs[t] += q[(4 * NT + t) * 64];
+    }
+    s1 += q[(5 * NT) * 64];
+    s2 += q[(5 * NT + 1) * 64];
+  }
+  // full-row statistics: the four k-groups of row r are lanes r, r+16, r+32, r+48
+  s1 += __shfl_xor(s1, 16);
+  s1 += __shfl_xor(s1, 32);
+  s2 += __shfl_xor(s2, 16);
+  s2 += __shfl_xor(s2, 32);
+  const float mean = s1 / (float)d;
+  const float rstd = rsqrtf(fmaxf(s2 / (float)d - mean * mean, 0.0f) + 1e-6f);
+#pragma unroll
+  for (int t = 0; t < NT; ++t) {
+    cs[t] += __shfl_xor(cs[t], 16);
+    cs[t] += __shfl_xor(cs[t], 32);
+  }
+  // lane l holds output rows 4 kg + i (i < 4) of column r of every tile
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int src = 4 * kg + i;
+    const float m_i = __shfl(mean, src), r_i = __shfl(rstd, src);
+    const int lat_i = __shfl(lat, src);
+    if (lat_i < 0) continue;
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
+      const int n = t * 16 + r;
+      if (n < c)
+        v[(int64_t)lat_i * c + n] = r_i * (acc[t][i] - m_i * cs[t]) + Elem<bf16_t>::load(b_v + n);
+    }
+  }
+}
+
 // one thread per latent element (of the conditional half with pairs)
 __global__ void __launch_bounds__(256)
 update_kernel(const float* __restrict__ v, float* __restrict__ v_cache, float* __restrict__ z,
@@ -313,6 +433,20 @@ hipError_t launch_velocity(int dtype, const void* y, const int32_t* gather, int6
                            const void* w_v, const void* b_v, float* v, int l_lat, int l_full,
                            int n_ctx, int c, int d, hipStream_t st) {
   if (n_items <= 0) return hipSuccess;
+  if (dtype == 1 && d % 32 == 0 && c <= 64) {
+    const dim3 grid((unsigned)((n_items + 15) / 16));
+    const int ni = (int)n_items;
+#define SWAM_VELM(NT_)                                                                        \
+  hipLaunchKernelGGL((velocity_mfma_kernel<NT_>), grid, dim3(64 * VEL_WAVES), 0, st,          \
+                     (const bf16_t*)y, gather, ni, (const bf16_t*)w_v, (const bf16_t*)b_v, v,   \
+                     l_lat, l_full, n_ctx, c, d)
+    if (c <= 16) SWAM_VELM(1);
+    else if (c <= 32) SWAM_VELM(2);
+    else if (c <= 48) SWAM_VELM(3);
+    else SWAM_VELM(4);
+#undef SWAM_VELM
+    return hipGetLastError();
+  }
   if (dtype == 1)
     return velocity_c<bf16_t>(y, gather, n_items, w_v, b_v, v, l_lat, l_full, n_ctx, c, d, st);
   return velocity_c<float>(y, gather, n_items, w_v, b_v, v, l_lat, l_full, n_ctx, c, d, st);
