@@ -499,13 +499,17 @@ def sampler_bench(args):
     print(json.dumps(out), flush=True)
 
 
-KERNEL_SOURCES = {"ATTN": ["k_attn.hip"], "GEMM_QKV": ["k_gemm.hip"], "GEMM_OUT": ["k_gemm.hip"],
-                  "GEMM_UP": ["k_gemm.hip"], "GEMM_DOWN": ["k_gemm.hip"], "SCORE": ["k_score.hip"],
-                  "PACK": ["k_select.hip"], "UNPACK": ["k_select.hip"]}
+# sources that define each kernel class (the attention kernel sees only the
+# device helpers of common.h; the others also include the launcher header)
+KERNEL_SOURCES = {"ATTN": ["k_attn.hip"],
+                  "GEMM_QKV": ["k_gemm.hip", "launchers.h"], "GEMM_OUT": ["k_gemm.hip", "launchers.h"],
+                  "GEMM_UP": ["k_gemm.hip", "launchers.h"], "GEMM_DOWN": ["k_gemm.hip", "launchers.h"],
+                  "SCORE": ["k_score.hip", "launchers.h"], "PACK": ["k_select.hip", "launchers.h"],
+                  "UNPACK": ["k_select.hip", "launchers.h"]}
 
 
 def kernel_source_hash(cls):
-    """sha256 over the sources that define a kernel class (and the shared header)."""
+    """sha256 over the sources that define a kernel class (and the device-helper header)."""
     import hashlib
     h = hashlib.sha256()
     for f in KERNEL_SOURCES[cls] + ["common.h"]:

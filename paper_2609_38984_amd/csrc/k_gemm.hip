@@ -12,7 +12,7 @@
 // Split K: when the output tiles cannot fill the 256 CUs (few rows, or a
 // narrow N), grid.y workgroups share a tile along K, store fp32 partial sums,
 // and one memory-bound pass sums them and applies the epilogue.
-#include "common.h"
+#include "launchers.h"
 
 namespace swam {
 

@@ -3,7 +3,7 @@
 //   h   = LN(x) (1 + scale) + shift       (biased variance, eps 1e-6, no affine)
 // One wavefront per output row (modulation) or per token row (LN); the row
 // stays in registers between the mean and the variance pass.
-#include "common.h"
+#include "launchers.h"
 
 namespace swam {
 

@@ -14,7 +14,7 @@
 //             with one fp32 FMA.
 // All three are memory-bound (c <= 64 latent channels against d >= 64 token
 // channels); latents, velocities and the cache are fp32.
-#include "common.h"
+#include "launchers.h"
 
 namespace swam {
 

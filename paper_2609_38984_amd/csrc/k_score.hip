@@ -20,7 +20,7 @@
 // Mode B normaliser: lambda over all keys of the sequence, per (query, head),
 // as an online max/sum split over key chunks with wavefront-shuffle
 // reductions, combined in a second pass.
-#include "common.h"
+#include "launchers.h"
 
 namespace swam {
 

@@ -11,7 +11,7 @@
 // floor(V 2^40) with a uint64 prefix scan.
 // Packing is an exclusive prefix sum of keep flags in original token order;
 // pack is a coalesced 16-byte row gather, unpack the matching scatter.
-#include "common.h"
+#include "launchers.h"
 
 namespace swam {
 

@@ -12,7 +12,7 @@
 #include <vector>
 
 #include "../../include/swam.h"
-#include "common.h"
+#include "launchers.h"
 
 #include <cmath>
 
