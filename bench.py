@@ -685,7 +685,7 @@ def main():
                     help="classifier-free guidance pairs with this scale (the batch doubles)")
     args = ap.parse_args()
     if args.gpus != 1:
-        print(json.dumps({"error": "this build runs on one GPU only: the step is single-GPU "
+        print(json.dumps({"error": "one GPU only: the step is single-GPU "
                           "data parallel work with no collectives; run with --gpus 1"}))
         sys.exit(2)
 
