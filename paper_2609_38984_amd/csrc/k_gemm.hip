@@ -53,7 +53,17 @@ __device__ __forceinline__ void tile_of(int pid, int nwg, int tiles_m, int tiles
 }
 
 typedef __attribute__((address_space(3))) void lds_void_t;
-typedef __attribute__((address_space(1))) void glb_void_t;
+
+// dword 3 of a raw buffer descriptor on gfx9-family parts (32-bit data format)
+constexpr int SWAM_BUF_DWORD3 = 0x00020000;
+
+// per-lane offset + wave-uniform step, formed at the point of use: an asm add
+// keeps the compiler from hoisting one live VGPR per slab out of the k loop
+__device__ __forceinline__ int vadd_sgpr(int v, int s) {
+  int r;
+  asm volatile("v_add_u32 %0, %1, %2" : "=v"(r) : "s"(s), "v"(v));
+  return r;
+}
 
 // one k-stage (64) of MFMAs from a staged A/B tile pair.  The operand
 // fragments of k-step s + 1 are read from LDS while the MFMAs of k-step s
@@ -103,10 +113,16 @@ __device__ __forceinline__ void mma_stage(const uint4* __restrict__ as, const ui
   __builtin_amdgcn_sched_group_barrier(0x008, FM * FN, 0);
 }
 
-// Stage loads go global -> LDS directly (no registers): each instruction moves
-// 8 rows x 128 bytes; lane i lands at slot i of the 1 KB slab, i.e. row
-// lane >> 3 and physical chunk lane & 7, so it fetches logical chunk
-// (lane & 7) ^ lds_swz(row) -- the swizzle is applied on the global side.
+// Stage loads go global -> LDS directly (no registers) as buffer loads: each
+// instruction moves 8 rows x 128 bytes; lane i lands at slot i of the 1 KB
+// slab, i.e. row lane >> 3 and physical chunk lane & 7, so it fetches logical
+// chunk (lane & 7) ^ lds_swz(row) -- the swizzle is applied on the global
+// side.  The descriptors start at the tile's first row and end at the last
+// row of the operand, so the rows of a ragged last tile read as zeros (the
+// hardware range check) and every offset stays below 2^31.  A wave's slabs
+// are 8 rows apart; only bit 3 of the row enters the swizzle, so two
+// per-lane offsets (even / odd slab) plus a wave-uniform step address them
+// all.
 template <int BM, int BN, int WM, int WN, int EPI>
 __global__ void __launch_bounds__(WM * WN * 64)
 gemm_bf16_nt(const bf16_t* __restrict__ A, int64_t lda, const bf16_t* __restrict__ B,
@@ -118,35 +134,42 @@ gemm_bf16_nt(const bf16_t* __restrict__ A, int64_t lda, const bf16_t* __restrict
   constexpr int FM = TM / 32, FN = TN / 32;
   constexpr int A_INS = BM / 8 / NW, B_INS = BN / 8 / NW;
   static_assert(A_INS * 8 * NW == BM && B_INS * 8 * NW == BN, "tile/waves mismatch");
+  static_assert(A_INS % 2 == 0 && B_INS % 2 == 0, "slab pairs");
   __shared__ uint4 lds[2 * (BM + BN) * 8];   // [stage][A rows | B rows][8 chunks]
 
   int tm, tn;
   tile_of(blockIdx.x, gridDim.x, tiles_m, tiles_n, tm, tn);
   const int m0 = tm * BM, n0 = tn * BN;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave-uniform
   const int wm = wave / WN, wn = wave % WN;
   const int lrow = lane >> 3;
-  // logical chunk fetched by this lane for an 8-row slab starting at row8
-  // (a multiple of 8): only bit 3 of the row beyond lrow enters the swizzle
-  auto lchunk = [&](int row8) { return (lane & 7) ^ lds_swz(row8 + lrow); };
 
-  auto a_src = [&](int j) {
-    const int r = (wave * A_INS + j) * 8;
-    return A + (int64_t)min(m0 + r + lrow, M - 1) * lda + 8 * lchunk(r & 8);
-  };
-  auto b_src = [&](int j) {
-    const int r = (wave * B_INS + j) * 8;
-    return B + (int64_t)min(n0 + r + lrow, N - 1) * ldb + 8 * lchunk(r & 8);
-  };
+  const __amdgpu_buffer_rsrc_t ra = __builtin_amdgcn_make_buffer_rsrc(
+      (void*)(A + (int64_t)m0 * lda), (short)0,
+      (int)min((int64_t)(M - m0) * lda * 2, (int64_t)0x7fffffff), SWAM_BUF_DWORD3);
+  const __amdgpu_buffer_rsrc_t rb = __builtin_amdgcn_make_buffer_rsrc(
+      (void*)(B + (int64_t)n0 * ldb), (short)0,
+      (int)min((int64_t)(N - n0) * ldb * 2, (int64_t)0x7fffffff), SWAM_BUF_DWORD3);
+  int va[2], vb[2];
+#pragma unroll
+  for (int p = 0; p < 2; ++p) {
+    const int ch = (lane & 7) ^ lds_swz(8 * p + lrow);
+    va[p] = (int)(((int64_t)(wave * A_INS * 8 + 8 * p + lrow) * lda + 8 * ch) * 2);
+    vb[p] = (int)(((int64_t)(wave * B_INS * 8 + 8 * p + lrow) * ldb + 8 * ch) * 2);
+  }
+  const int step_a = (int)(16 * lda * 2), step_b = (int)(16 * ldb * 2);
   auto issue = [&](uint4* as, uint4* bs, int k0) {
 #pragma unroll
     for (int j = 0; j < A_INS; ++j)
-      __builtin_amdgcn_global_load_lds((glb_void_t*)(a_src(j) + k0),
-                                       (lds_void_t*)(as + (wave * A_INS + j) * 64), 16, 0, 0);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(
+          ra, (lds_void_t*)(as + (wave * A_INS + j) * 64), 16,
+          vadd_sgpr(va[j & 1], (j >> 1) * step_a + k0 * 2), 0, 0, 0);
 #pragma unroll
     for (int j = 0; j < B_INS; ++j)
-      __builtin_amdgcn_global_load_lds((glb_void_t*)(b_src(j) + k0),
-                                       (lds_void_t*)(bs + (wave * B_INS + j) * 64), 16, 0, 0);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(
+          rb, (lds_void_t*)(bs + (wave * B_INS + j) * 64), 16,
+          vadd_sgpr(vb[j & 1], (j >> 1) * step_b + k0 * 2), 0, 0, 0);
   };
 
   f32x16 acc[FM][FN];
