@@ -127,38 +127,70 @@ attn_fwd_bf16(const bf16_t* __restrict__ qkv, bf16_t* __restrict__ out, float* _
   // carry no masking code, the ragged last one runs a copy with the key mask
   auto tile = [&](int cur, int sub, int kb, auto masked) {
     const uint4* Kt = &Ks[cur][sub * ATT_BK * 8];
-    f32x16 st[2];
+    auto scores = [&](f32x16 (&st)[2]) {
 #pragma unroll
-    for (int t = 0; t < 2; ++t) {
+      for (int t = 0; t < 2; ++t) {
 #pragma unroll
-      for (int r = 0; r < 16; ++r) st[t][r] = 0.0f;
-      const int key = 32 * t + (lane & 31);
+        for (int r = 0; r < 16; ++r) st[t][r] = 0.0f;
+        const int key = 32 * t + (lane & 31);
 #pragma unroll
-      for (int s = 0; s < 4; ++s) {
-        const int ch = 2 * s + g;
-        bf16x8 kf = __builtin_bit_cast(bf16x8, Kt[key * 8 + (ch ^ lds_swz(key))]);
-        st[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[s], st[t], 0, 0, 0);
+        for (int s = 0; s < 4; ++s) {
+          const int ch = 2 * s + g;
+          bf16x8 kf = __builtin_bit_cast(bf16x8, Kt[key * 8 + (ch ^ lds_swz(key))]);
+          st[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[s], st[t], 0, 0, 0);
+        }
       }
-    }
-    if constexpr (decltype(masked)::value) {
-      const int nvalid = s1 - kb;
+      if constexpr (decltype(masked)::value) {
+        const int nvalid = s1 - kb;
+#pragma unroll
+        for (int t = 0; t < 2; ++t)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int key = 32 * t + 8 * (r >> 2) + 4 * g + (r & 3);
+            if (key >= nvalid) st[t][r] = -INFINITY;
+          }
+      }
+    };
+    // probabilities against the running max.  Their row sum bounds every one
+    // of them, so a sum above 2^8 is the only case in which the running max
+    // must move (lazy rescaling: each p stays <= 2^8 otherwise); the scores
+    // are then recomputed (K is still staged) and the tile is redone against
+    // the new max.  The first tile of a row always takes that path (the
+    // running max starts at -1e30).
+    bf16x8 pf[2][2];
+    float psum0, psum1;
+    auto probs = [&](const f32x16 (&st)[2]) {
+      psum0 = 0.0f; psum1 = 0.0f;
 #pragma unroll
       for (int t = 0; t < 2; ++t)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int key = 32 * t + 8 * (r >> 2) + 4 * g + (r & 3);
-          if (key >= nvalid) st[t][r] = -INFINITY;
-        }
+        for (int u = 0; u < 2; ++u)
+#pragma unroll
+          for (int mm = 0; mm < 8; mm += 2) {
+            const float p0 = __builtin_amdgcn_exp2f(fmaf(st[t][8 * u + mm], sc, -m_run));
+            const float p1 = __builtin_amdgcn_exp2f(fmaf(st[t][8 * u + mm + 1], sc, -m_run));
+            // row sums from the fp32 probabilities (the exported normaliser)
+            psum0 += p0; psum1 += p1;
+            pf[t][u][mm] = (__bf16)p0; pf[t][u][mm + 1] = (__bf16)p1;
+          }
+    };
+    {
+      f32x16 st[2];
+      scores(st);
+      probs(st);
     }
-    float mx = st[0][0];
+    if (__any(!(psum0 + psum1 <= 256.0f))) {
+      // re-read K from LDS rather than keeping the first pass's fragments live
+      asm volatile("" ::: "memory");
+      f32x16 st[2];
+      scores(st);
+      float mx = st[0][0];
 #pragma unroll
-    for (int t = 0; t < 2; ++t)
+      for (int t = 0; t < 2; ++t)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) mx = fmaxf(mx, st[t][r]);
-    mx = fmaxf(mx, __shfl_xor(mx, 32));
-    const float m_tile = mx * sc;
-    if (__any(m_tile > m_run + 8.0f)) {
-      const float m_new = fmaxf(m_run, m_tile);
+        for (int r = 0; r < 16; ++r) mx = fmaxf(mx, st[t][r]);
+      mx = fmaxf(mx, __shfl_xor(mx, 32));
+      const float m_new = fmaxf(m_run, mx * sc);
       const float corr = __builtin_amdgcn_exp2f(m_run - m_new);
       m_run = m_new;
       l_run *= corr;
@@ -166,21 +198,8 @@ attn_fwd_bf16(const bf16_t* __restrict__ qkv, bf16_t* __restrict__ out, float* _
       for (int t = 0; t < 2; ++t)
 #pragma unroll
         for (int r = 0; r < 16; ++r) o[t][r] *= corr;
+      probs(st);
     }
-    bf16x8 pf[2][2];
-    float psum0 = 0.0f, psum1 = 0.0f;
-#pragma unroll
-    for (int t = 0; t < 2; ++t)
-#pragma unroll
-      for (int u = 0; u < 2; ++u)
-#pragma unroll
-        for (int mm = 0; mm < 8; mm += 2) {
-          const float p0 = __builtin_amdgcn_exp2f(fmaf(st[t][8 * u + mm], sc, -m_run));
-          const float p1 = __builtin_amdgcn_exp2f(fmaf(st[t][8 * u + mm + 1], sc, -m_run));
-          // row sums from the fp32 probabilities (the exported normaliser)
-          psum0 += p0; psum1 += p1;
-          pf[t][u][mm] = (__bf16)p0; pf[t][u][mm + 1] = (__bf16)p1;
-        }
     l_run += psum0 + psum1;
     const unsigned short* vs = reinterpret_cast<const unsigned short*>(&Vs[cur][sub * ATT_BK * 8]);
 #pragma unroll
