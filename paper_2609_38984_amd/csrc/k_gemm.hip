@@ -14,6 +14,8 @@
 // and one memory-bound pass sums them and applies the epilogue.
 #include "launchers.h"
 
+#include <algorithm>
+
 namespace swam {
 
 __device__ __forceinline__ float gelu_tanh(float u) {
@@ -379,11 +381,16 @@ static hipError_t run_bf16(const void* A, int64_t lda, const void* B, int64_t ld
 }
 
 // Tile and K-split choice: modelled time = rounds * (per-CU MFMA work of one
-// round / tile efficiency) + (split > 1) the partial-sum pass over HBM, where
-// a round places `per_cu` workgroups on each of the 256 CUs (LDS-limited),
-// the efficiencies are the measured per-tile MFMA rates of the three kernels
-// relative to a 40%-of-peak base, and the pass moves splits * M * N fp32
-// partials plus the bf16 output (and residual) at about 4 TB/s.
+// round / tile efficiency) + (split > 1) the partial-sum pass over HBM.  A
+// round places `per_cu` workgroups on each of the 256 CUs (LDS-limited).  The
+// 256x256 and 256x128 kernels fit one workgroup per CU and run in whole
+// rounds; two 128x128 workgroups share a CU and start as soon as a slot
+// frees, so their rounds count in halves once a grid spills past one slot per
+// CU.  The efficiencies are the per-CU MFMA rates of the three kernels
+// measured on the block shapes of the d = 1536 and d = 2048 workloads,
+// relative to the 256x256 kernel (whose rate, about 40% of the per-CU peak,
+// is the base); the pass moves splits * M * N fp32 partials plus the bf16
+// output (and residual) at about 4 TB/s.
 struct GemmPlan { int tile, splits; };
 static GemmPlan choose_gemm(int64_t M, int64_t N, int64_t K, int64_t ws_floats) {
   static int forced = -2, forced_split = -2;
@@ -394,7 +401,7 @@ static GemmPlan choose_gemm(int64_t M, int64_t N, int64_t K, int64_t ws_floats) 
     forced_split = f ? atoi(f) : -1;
   }
   struct Cand { int bm, bn, per_cu; double eff; };
-  const Cand c[3] = {{256, 256, 1, 1.0}, {256, 128, 1, 0.85}, {128, 128, 2, 0.75}};
+  const Cand c[3] = {{256, 256, 1, 1.0}, {256, 128, 1, 0.72}, {128, 128, 2, 0.80}};
   const int split_opts[6] = {1, 2, 3, 4, 6, 8};
   const int64_t kt = K / GEMM_BK;
   const double cu_flops = 2.5e15 / 256.0 * 0.40;        // sustained MFMA rate per CU
@@ -403,14 +410,20 @@ static GemmPlan choose_gemm(int64_t M, int64_t N, int64_t K, int64_t ws_floats) 
   for (int i = 0; i < 3; ++i) {
     if (forced >= 0 && forced <= 2 && i != forced) continue;
     const int64_t tiles = ((M + c[i].bm - 1) / c[i].bm) * ((N + c[i].bn - 1) / c[i].bn);
-    const int64_t slots = 256ll * c[i].per_cu;
     for (int s : split_opts) {
       if (forced_split >= 1 && s != forced_split) continue;
       if (s > 1 && (kt / s < 4 || (int64_t)s * M * N > ws_floats)) continue;
       const int64_t wgs = tiles * s;
-      const int64_t rounds = (wgs + slots - 1) / slots;
+      double rounds;
+      if (c[i].per_cu == 1) {
+        rounds = (double)((wgs + 255) / 256);
+      } else {
+        // whole half-rounds while one slot per CU is not yet filled
+        rounds = std::max((double)wgs / (256.0 * c[i].per_cu),
+                          (double)((wgs + 255) / 256) / c[i].per_cu);
+      }
       const double k_slice = (double)((kt + s - 1) / s) * GEMM_BK;
-      double t = (double)rounds * 2.0 * c[i].bm * c[i].bn * c[i].per_cu * k_slice /
+      double t = rounds * 2.0 * c[i].bm * c[i].bn * c[i].per_cu * k_slice /
                  (cu_flops * c[i].eff);
       if (s > 1) t += ((double)s * M * N * 4.0 + 4.0 * M * N) / 4.0e12 + 3e-6;
       if (t < best_t) { best_t = t; best = {i, s}; }
