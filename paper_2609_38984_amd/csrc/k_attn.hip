@@ -79,6 +79,7 @@ attn_fwd_bf16(const bf16_t* __restrict__ qkv, bf16_t* __restrict__ out, float* _
   const bf16_t* kbase = qkv + d + h * 64;
   const bf16_t* vbase = qkv + 2 * d + h * 64;
   constexpr int SLABS = SK / 8 / NW;             // 8-row slabs per wave and stage
+  static_assert(SLABS * 8 * NW == SK, "every wave stages whole 8-row slabs");
   int lofs[SLABS];
 #pragma unroll
   for (int j = 0; j < SLABS; ++j) {
