@@ -113,6 +113,11 @@ attn_fwd_bf16(const bf16_t* __restrict__ qkv, bf16_t* __restrict__ out, float* _
       const int hd = 32 * ht + 16 * (G & 1) + 4 * (a16 & 3);
       vofs[ht][hf] = r * 64 + 8 * ((hd >> 3) ^ lds_swz(r)) + (hd & 7);
     }
+  // K fragment (logical chunk 2 s + g of key lane & 31) offsets in a tile
+  int kofs[4];
+#pragma unroll
+  for (int s = 0; s < 4; ++s)
+    kofs[s] = (lane & 31) * 8 + ((2 * s + g) ^ lds_swz(lane & 31));
   f32x16 o[2];
 #pragma unroll
   for (int t = 0; t < 2; ++t)
@@ -133,11 +138,11 @@ attn_fwd_bf16(const bf16_t* __restrict__ qkv, bf16_t* __restrict__ out, float* _
       for (int t = 0; t < 2; ++t) {
 #pragma unroll
         for (int r = 0; r < 16; ++r) st[t][r] = 0.0f;
-        const int key = 32 * t + (lane & 31);
+        // keys 32 t + (lane & 31): the swizzle sees the same row bits for both
+        // halves, so the half is a constant offset of 32 rows
 #pragma unroll
         for (int s = 0; s < 4; ++s) {
-          const int ch = 2 * s + g;
-          bf16x8 kf = __builtin_bit_cast(bf16x8, Kt[key * 8 + (ch ^ lds_swz(key))]);
+          bf16x8 kf = __builtin_bit_cast(bf16x8, Kt[kofs[s] + t * 32 * 8]);
           st[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[s], st[t], 0, 0, 0);
         }
       }
