@@ -281,12 +281,17 @@ def measure(cfg, model, xs, tembs, steps, warmup, reps):
     qk_post = None
     if cfg.rope or cfg.qk_norm:
         n_qk, ms_qk = ctx.timer_read("QK_POST")
-        rows = [full_rows if t % cfg.reuse_R == 0 else packed_rows for t in range(n_sched)]
-        work = sum(kernel_work(cfg, "QK_POST", r) * cfg.n_blocks for r in rows)
-        gbs = work / (ms_qk * 1e-3) / 1e9
-        qk_post = {"rope": cfg.rope, "qk_norm": cfg.qk_norm, "launches": n_qk,
-                   "ms_per_step": round(ms_qk / n_sched, 4), "achieved": round(gbs, 1),
-                   "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": round(gbs / PEAK_HBM_GBS, 4)}
+        if n_qk == 0:
+            # applied inside the QKV projection's store (no pass of its own)
+            qk_post = {"rope": cfg.rope, "qk_norm": cfg.qk_norm, "launches": 0,
+                       "fused_into": "GEMM_QKV"}
+        else:
+            rows = [full_rows if t % cfg.reuse_R == 0 else packed_rows for t in range(n_sched)]
+            work = sum(kernel_work(cfg, "QK_POST", r) * cfg.n_blocks for r in rows)
+            gbs = work / (ms_qk * 1e-3) / 1e9
+            qk_post = {"rope": cfg.rope, "qk_norm": cfg.qk_norm, "launches": n_qk,
+                       "ms_per_step": round(ms_qk / n_sched, 4), "achieved": round(gbs, 1),
+                       "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": round(gbs / PEAK_HBM_GBS, 4)}
     ctx.timer_enable([], 1)
     over = sum(phase_ms[c] for c in ("SCORE", "REDUCE", "SELECT", "PACK", "UNPACK"))
     tok = cfg.batch * cfg.l_full

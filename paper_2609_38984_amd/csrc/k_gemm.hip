@@ -34,6 +34,70 @@ __device__ __forceinline__ float epi_value(float acc, float bias, float gate, fl
   return resid + gate * (acc + bias);
 }
 
+// Store of 8 consecutive QKV columns of one row with the QK-norm / rotary
+// embedding of q and k heads applied (the steps of qk_post_kernel on the
+// projection rounded to bf16).  The 8 lanes storing one row's 64 columns are
+// consecutive and aligned, and a wave's 64 columns are one head, so the head
+// norm is a 3-step exchange; every lane takes part (the store is guarded).
+__device__ __forceinline__ void qkpost_store(const float* v, const bf16_t* __restrict__ bias,
+                                             bf16_t* C, int64_t ldc, int row, int col, int col0,
+                                             int M, int N, const QkPost& qp) {
+  float x[8];
+  {
+    const float4 v0 = *reinterpret_cast<const float4*>(v);
+    const float4 v1 = *reinterpret_cast<const float4*>(v + 4);
+    const float a[8] = {v0.x, v0.y, v0.z, v0.w, v1.x, v1.y, v1.z, v1.w};
+    uint4 bw = make_uint4(0u, 0u, 0u, 0u);
+    if (col < N) bw = *reinterpret_cast<const uint4*>(bias + col);
+    const uint32_t bb[4] = {bw.x, bw.y, bw.z, bw.w};
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      // the projection is stored (rounded to bf16) before the post-processing
+      x[2 * e] = bf16_to_f32(f32_to_bf16(a[2 * e] + __uint_as_float(bb[e] << 16)));
+      x[2 * e + 1] = bf16_to_f32(f32_to_bf16(a[2 * e + 1] + __uint_as_float(bb[e] & 0xFFFF0000u)));
+    }
+  }
+  if (col0 < 2 * qp.d) {                      // q or k head (wave-uniform)
+    if (qp.qk_norm) {
+      float ss = 0.0f;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) ss = fmaf(x[e], x[e], ss);
+      ss += __shfl_xor(ss, 1);
+      ss += __shfl_xor(ss, 2);
+      ss += __shfl_xor(ss, 4);
+      const float r = rsqrtf(ss / 64.0f + 1e-6f);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) x[e] *= r;
+    }
+    if (qp.tab != nullptr) {
+      const int rr = min(row, M - 1);
+      int pos;
+      if (qp.pos_mode == 0) {
+        pos = rr % qp.l_full;
+      } else if (qp.pos_mode == 1) {
+        pos = qp.gather[rr] % qp.l_full;
+      } else {
+        int b = 0;
+        while (b + 1 < qp.n_seqs && qp.cu[b + 1] <= rr) ++b;
+        pos = rr - qp.cu[b];
+      }
+      pos = min(max(pos, 0), qp.n_pos - 1);
+      const float2* t = qp.tab + (int64_t)pos * 32 + ((col & 63) >> 1);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const float2 cs = t[e];
+        const float a = x[2 * e], b = x[2 * e + 1];
+        x[2 * e] = a * cs.x - b * cs.y;
+        x[2 * e + 1] = a * cs.y + b * cs.x;
+      }
+    }
+  }
+  if (row < M && col < N)
+    *reinterpret_cast<uint4*>(C + (int64_t)row * ldc + col) =
+        make_uint4(pack_bf16x2(x[0], x[1]), pack_bf16x2(x[2], x[3]), pack_bf16x2(x[4], x[5]),
+                   pack_bf16x2(x[6], x[7]));
+}
+
 // ---------------------------------------------------------------------------
 // bf16 MFMA kernel
 // ---------------------------------------------------------------------------
@@ -130,7 +194,7 @@ __global__ void __launch_bounds__(WM * WN * 64)
 gemm_bf16_nt(const bf16_t* __restrict__ A, int64_t lda, const bf16_t* __restrict__ B,
              int64_t ldb, const bf16_t* __restrict__ bias, const float* __restrict__ gate,
              bf16_t* C, int64_t ldc, int M, int N, int K, int tiles_m, int tiles_n,
-             float* __restrict__ part) {
+             float* __restrict__ part, const QkPost qp) {
   constexpr int NW = WM * WN;
   constexpr int TM = BM / WM, TN = BN / WN;
   constexpr int FM = TM / 32, FN = TN / 32;
@@ -205,6 +269,7 @@ gemm_bf16_nt(const bf16_t* __restrict__ A, int64_t lda, const bf16_t* __restrict
   // handles 8 consecutive columns with 16-byte loads (bias, gate, residual) and
   // a 16-byte store, so each 8 lanes write one contiguous 128-byte row run.
   constexpr int EP_LD = TN + 4;                       // fp32 row pitch of the staging slice
+  static_assert(EPI != EPI_BIAS_QKPOST || TN == 64, "a wave's columns must be one head");
   static_assert(NW * 32 * EP_LD * 4 <= (int)sizeof(lds), "epilogue staging exceeds LDS");
   float* stage = reinterpret_cast<float*>(lds) + wave * 32 * EP_LD;
   const int col0 = n0 + wn * TN;
@@ -224,6 +289,10 @@ gemm_bf16_nt(const bf16_t* __restrict__ A, int64_t lda, const bf16_t* __restrict
     for (int c = lane; c < 32 * TN / 8; c += 64) {
       const int rl = c / (TN / 8), cl = (c % (TN / 8)) * 8;
       const int row = row0 + rl, col = col0 + cl;
+      if constexpr (EPI == EPI_BIAS_QKPOST) {
+        qkpost_store(stage + rl * EP_LD + cl, bias, C, ldc, row, col, col0, M, N, qp);
+        continue;
+      }
       if (EPI == EPI_PARTIAL && row < M && col < N) {
         // fp32 partial sums of this K slice: part[slice][M][N]
         float* q = part + ((int64_t)blockIdx.y * M + row) * N + col;
@@ -360,24 +429,30 @@ gemm_f32_nt(const float* __restrict__ A, int64_t lda, const float* __restrict__ 
 template <int BM, int BN, int WM, int WN, int EPI>
 static hipError_t run_bf16(const void* A, int64_t lda, const void* B, int64_t ldb,
                            const void* bias, const float* gate, void* C, int64_t ldc, int M,
-                           int N, int K, int splits, float* part, hipStream_t st) {
+                           int N, int K, int splits, float* part, hipStream_t st,
+                           const QkPost& qp = QkPost{}) {
   const int tiles_m = (M + BM - 1) / BM, tiles_n = (N + BN - 1) / BN;
   if (splits <= 1) {
     hipLaunchKernelGGL((gemm_bf16_nt<BM, BN, WM, WN, EPI>), dim3(tiles_m * tiles_n),
                        dim3(WM * WN * 64), 0, st, (const bf16_t*)A, lda, (const bf16_t*)B, ldb,
                        (const bf16_t*)bias, gate, (bf16_t*)C, ldc, M, N, K, tiles_m, tiles_n,
-                       (float*)nullptr);
+                       (float*)nullptr, qp);
     return hipGetLastError();
   }
-  hipLaunchKernelGGL((gemm_bf16_nt<BM, BN, WM, WN, EPI_PARTIAL>), dim3(tiles_m * tiles_n, splits),
-                     dim3(WM * WN * 64), 0, st, (const bf16_t*)A, lda, (const bf16_t*)B, ldb,
-                     (const bf16_t*)bias, gate, (bf16_t*)C, ldc, M, N, K, tiles_m, tiles_n, part);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  const int64_t n = (int64_t)M * (N / 8);
-  hipLaunchKernelGGL(splitk_epilogue<EPI>, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st,
-                     part, splits, M, N, (const bf16_t*)bias, gate, (bf16_t*)C, ldc);
-  return hipGetLastError();
+  if constexpr (EPI == EPI_BIAS_QKPOST) {
+    return hipErrorNotSupported;             // no split-K store with the QK post-processing
+  } else {
+    hipLaunchKernelGGL((gemm_bf16_nt<BM, BN, WM, WN, EPI_PARTIAL>), dim3(tiles_m * tiles_n, splits),
+                       dim3(WM * WN * 64), 0, st, (const bf16_t*)A, lda, (const bf16_t*)B, ldb,
+                       (const bf16_t*)bias, gate, (bf16_t*)C, ldc, M, N, K, tiles_m, tiles_n, part,
+                       QkPost{});
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    const int64_t n = (int64_t)M * (N / 8);
+    hipLaunchKernelGGL(splitk_epilogue<EPI>, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st,
+                       part, splits, M, N, (const bf16_t*)bias, gate, (bf16_t*)C, ldc);
+    return hipGetLastError();
+  }
 }
 
 // Tile and K-split choice: modelled time = rounds * (per-CU MFMA work of one
@@ -473,6 +548,30 @@ hipError_t launch_gemm(int dtype, int epi, const void* A, int64_t lda, const voi
     case EPI_BIAS_GELU: return run_f32<EPI_BIAS_GELU>(A, lda, B, ldb, bias, gate, C, ldc, m, n, k, st);
     default: return run_f32<EPI_BIAS_GATED_RESIDUAL>(A, lda, B, ldb, bias, gate, C, ldc, m, n, k, st);
   }
+}
+
+hipError_t launch_gemm_qkv(int dtype, const void* A, int64_t lda, const void* B, int64_t ldb,
+                           const void* bias, void* C, int64_t ldc, int64_t M, int64_t N,
+                           int64_t K, const QkPost& qp, hipStream_t st, float* ws,
+                           int64_t ws_floats) {
+  if (M <= 0) return hipSuccess;
+  const bool post = qp.qk_norm || qp.tab != nullptr;
+  if (dtype == 1 && post) {
+    const GemmPlan p = choose_gemm(M, N, K, ws ? ws_floats : 0);
+    if (p.splits <= 1) {
+      const int m = (int)M, n = (int)N, k = (int)K;
+      switch (p.tile) {
+        case 0: return run_bf16<256, 256, 2, 4, EPI_BIAS_QKPOST>(A, lda, B, ldb, bias, nullptr, C, ldc, m, n, k, 1, nullptr, st, qp);
+        case 1: return run_bf16<256, 128, 4, 2, EPI_BIAS_QKPOST>(A, lda, B, ldb, bias, nullptr, C, ldc, m, n, k, 1, nullptr, st, qp);
+        default: return run_bf16<128, 128, 2, 2, EPI_BIAS_QKPOST>(A, lda, B, ldb, bias, nullptr, C, ldc, m, n, k, 1, nullptr, st, qp);
+      }
+    }
+  }
+  const hipError_t e = launch_gemm(dtype, EPI_BIAS, A, lda, B, ldb, bias, nullptr, C, ldc, M, N, K,
+                                   st, ws, ws_floats);
+  if (e != hipSuccess || !post) return e;
+  return launch_qk_post(dtype, C, M, qp.d, qp.pos_mode, qp.gather, qp.cu, qp.n_seqs, qp.l_full,
+                        qp.tab, qp.n_pos, qp.qk_norm, st);
 }
 
 }  // namespace swam

@@ -8,8 +8,22 @@ namespace swam {
 // ---------------------------------------------------------------------------
 // launchers (host side), one per kernel family; all asynchronous on `st`
 // ---------------------------------------------------------------------------
-// EPI_PARTIAL is internal to the bf16 split-K path (fp32 partial sums)
-enum Epilogue { EPI_BIAS = 0, EPI_BIAS_GELU = 1, EPI_BIAS_GATED_RESIDUAL = 2, EPI_PARTIAL = 3 };
+// EPI_PARTIAL is internal to the bf16 split-K path (fp32 partial sums);
+// EPI_BIAS_QKPOST to launch_gemm_qkv
+enum Epilogue { EPI_BIAS = 0, EPI_BIAS_GELU = 1, EPI_BIAS_GATED_RESIDUAL = 2, EPI_PARTIAL = 3,
+                EPI_BIAS_QKPOST = 4 };
+
+// QK-norm / rotary embedding of the q and k columns of a QKV projection
+// (the arguments of launch_qk_post): d = model width (q columns [0, d), k
+// columns [d, 2d)); pos_mode 0 = dense rows (position row % l_full), 1 =
+// packed rows (gather[row] % l_full), 2 = index inside the cu_seqlens
+// sequence; tab = rotary table [n_pos][32] (NULL: no rotation).
+struct QkPost {
+  int d = 0, pos_mode = 0, n_seqs = 0, l_full = 1, n_pos = 1, qk_norm = 0;
+  const int32_t* gather = nullptr;
+  const int32_t* cu = nullptr;
+  const float2* tab = nullptr;
+};
 
 // C[M][N] = epi(A[M][K] . B[N][K]^T + bias[N]); for the gated residual
 // C[m][n] = C[m][n] + gate[n] * (acc + bias[n]) (C read then written).
@@ -20,6 +34,15 @@ hipError_t launch_gemm(int dtype, int epi, const void* A, int64_t lda, const voi
                        int64_t ldb, const void* bias, const float* gate, void* C,
                        int64_t ldc, int64_t M, int64_t N, int64_t K, hipStream_t st,
                        float* ws = nullptr, int64_t ws_floats = 0);
+
+// QKV projection C = A . B^T + bias followed by the QK-norm / rotary
+// embedding of qp on its q and k columns, with the same bf16 rounding of the
+// projection as launch_gemm + launch_qk_post; fused into the GEMM's store
+// for bf16 unless the shape splits K (then the two launches).
+hipError_t launch_gemm_qkv(int dtype, const void* A, int64_t lda, const void* B, int64_t ldb,
+                           const void* bias, void* C, int64_t ldc, int64_t M, int64_t N,
+                           int64_t K, const QkPost& qp, hipStream_t st, float* ws = nullptr,
+                           int64_t ws_floats = 0);
 
 // mod[blk][6d] = W_ada[blk] SiLU(temb) + b_ada[blk] for n_blk blocks at once.
 struct AdalnArgs {

@@ -263,19 +263,26 @@ int run_block(swam_ctx* c, const swam_block_weights* w, const float* mod, void* 
     Timed t(c, SWAM_T_LNMOD);
     SWAM_HIP(c, launch_ln_mod(dt, x, h, sh1, sc1, n_rows, (int)d, st), "ln_mod");
   }
-  {
+  if (c->cfg.rope || c->cfg.qk_norm) {
+    // QKV projection with the QK-norm / rotary embedding of q and k (fused
+    // into the projection's store where the shape allows)
+    QkPost qp;
+    qp.d = (int)d;
+    qp.pos_mode = pos_mode;
+    qp.gather = c->ptr<int32_t>(c->lay.gather);
+    qp.cu = cu;
+    qp.n_seqs = n_seqs;
+    qp.l_full = (int)c->dv.l_full;
+    qp.tab = c->cfg.rope ? c->ptr<float2>(c->lay.rope) : nullptr;
+    qp.n_pos = (int)c->dv.rows_full;
+    qp.qk_norm = c->cfg.qk_norm;
+    Timed t(c, SWAM_T_GEMM_QKV);
+    SWAM_HIP(c, launch_gemm_qkv(dt, h, d, w->w_qkv, d, w->b_qkv, qkv, 3 * d, n_rows, 3 * d, d, qp,
+                                st, sk, sk_n), "gemm qkv + qk post");
+  } else {
     Timed t(c, SWAM_T_GEMM_QKV);
     SWAM_HIP(c, launch_gemm(dt, EPI_BIAS, h, d, w->w_qkv, d, w->b_qkv, nullptr, qkv, 3 * d,
                             n_rows, 3 * d, d, st, sk, sk_n), "gemm qkv");
-  }
-  if (c->cfg.rope || c->cfg.qk_norm) {
-    Timed t(c, SWAM_T_QK_POST);
-    SWAM_HIP(c, launch_qk_post(dt, qkv, n_rows, (int)d, pos_mode, c->ptr<int32_t>(c->lay.gather),
-                               cu, n_seqs, (int)c->dv.l_full,
-                               c->cfg.rope ? c->ptr<float2>(c->lay.rope) : nullptr,
-                               (int)c->dv.rows_full,
-                               c->cfg.qk_norm, st),
-             "qk post");
   }
   {
     Timed t(c, SWAM_T_ATTN);
