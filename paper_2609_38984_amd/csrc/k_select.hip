@@ -535,41 +535,42 @@ hipError_t launch_packmap(const int32_t* keep, int32_t* pack_pos, int32_t* gathe
 // ---------------------------------------------------------------------------
 // pack / unpack / copy: 16-byte chunks, one row per 64 x 16 B slice
 // ---------------------------------------------------------------------------
+// Row copies of pack / unpack: one wave per row (the row's source or target
+// index is wave-uniform), lanes striding over the row's 16-byte chunks, four
+// rows per 256-thread workgroup.
 __global__ void __launch_bounds__(256)
 pack_rows(const uint4* __restrict__ src, uint4* __restrict__ dst,
           const int32_t* __restrict__ gather, int64_t rows, int cpr) {
-  const int64_t total = rows * cpr;
-  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < total;
-       i += (int64_t)gridDim.x * 256) {
-    const int64_t r = i / cpr;
-    const int c = (int)(i - r * cpr);
-    dst[i] = src[(int64_t)gather[r] * cpr + c];
-  }
+  const int64_t r = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (r >= rows) return;
+  const int lane = threadIdx.x & 63;
+  const uint4* s_ = src + (int64_t)gather[r] * cpr;
+  uint4* d_ = dst + r * cpr;
+  for (int c = lane; c < cpr; c += 64) d_[c] = s_[c];
 }
 
 __global__ void __launch_bounds__(256)
 unpack_scatter(const uint4* __restrict__ src, uint4* __restrict__ dst,
                const int32_t* __restrict__ gather, int64_t rows, int cpr) {
-  const int64_t total = rows * cpr;
-  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < total;
-       i += (int64_t)gridDim.x * 256) {
-    const int64_t r = i / cpr;
-    const int c = (int)(i - r * cpr);
-    dst[(int64_t)gather[r] * cpr + c] = src[i];
-  }
+  const int64_t r = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (r >= rows) return;
+  const int lane = threadIdx.x & 63;
+  const uint4* s_ = src + r * cpr;
+  uint4* d_ = dst + (int64_t)gather[r] * cpr;
+  for (int c = lane; c < cpr; c += 64) d_[c] = s_[c];
 }
 
+// y row r = packed row pack_pos[r] if retained, else x row r
 __global__ void __launch_bounds__(256)
 unpack_merge(const uint4* __restrict__ yp, const uint4* __restrict__ x, uint4* __restrict__ y,
              const int32_t* __restrict__ pack_pos, int64_t rows, int cpr) {
-  const int64_t total = rows * cpr;
-  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < total;
-       i += (int64_t)gridDim.x * 256) {
-    const int64_t r = i / cpr;
-    const int c = (int)(i - r * cpr);
-    const int32_t p = pack_pos[r];
-    y[i] = p >= 0 ? yp[(int64_t)p * cpr + c] : x[i];
-  }
+  const int64_t r = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (r >= rows) return;
+  const int lane = threadIdx.x & 63;
+  const int32_t p = pack_pos[r];
+  const uint4* s_ = p >= 0 ? yp + (int64_t)p * cpr : x + r * cpr;
+  uint4* d_ = y + r * cpr;
+  for (int c = lane; c < cpr; c += 64) d_[c] = s_[c];
 }
 
 __global__ void __launch_bounds__(256)
@@ -588,7 +589,7 @@ hipError_t launch_pack(const void* x_full, void* x_packed, const int32_t* gather
                        int64_t row_bytes, hipStream_t st) {
   if (rows <= 0) return hipSuccess;
   const int cpr = (int)(row_bytes / 16);
-  hipLaunchKernelGGL(pack_rows, dim3(grid_for(rows * cpr)), dim3(256), 0, st,
+  hipLaunchKernelGGL(pack_rows, dim3((unsigned)((rows + 3) / 4)), dim3(256), 0, st,
                      (const uint4*)x_full, (uint4*)x_packed, gather, rows, cpr);
   return hipGetLastError();
 }
@@ -597,7 +598,7 @@ hipError_t launch_unpack_scatter(const void* y_packed, void* y_full, const int32
                                  int64_t rows, int64_t row_bytes, hipStream_t st) {
   if (rows <= 0) return hipSuccess;
   const int cpr = (int)(row_bytes / 16);
-  hipLaunchKernelGGL(unpack_scatter, dim3(grid_for(rows * cpr)), dim3(256), 0, st,
+  hipLaunchKernelGGL(unpack_scatter, dim3((unsigned)((rows + 3) / 4)), dim3(256), 0, st,
                      (const uint4*)y_packed, (uint4*)y_full, gather, rows, cpr);
   return hipGetLastError();
 }
@@ -607,7 +608,7 @@ hipError_t launch_unpack_merge(const void* y_packed, const void* x_full, void* y
                                hipStream_t st) {
   if (rows <= 0) return hipSuccess;
   const int cpr = (int)(row_bytes / 16);
-  hipLaunchKernelGGL(unpack_merge, dim3(grid_for(rows * cpr)), dim3(256), 0, st,
+  hipLaunchKernelGGL(unpack_merge, dim3((unsigned)((rows + 3) / 4)), dim3(256), 0, st,
                      (const uint4*)y_packed, (const uint4*)x_full, (uint4*)y_full, pack_pos,
                      rows, cpr);
   return hipGetLastError();
