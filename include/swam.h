@@ -41,6 +41,10 @@
  * Element type: activations and weights are float32 (SWAM_F32) or bf16
  *   (SWAM_BF16, raw 16-bit storage) as fixed by swam_config.dtype; scores,
  *   normalisers, timestep embeddings and all statistics are float32.
+ * Alignment: block weights (swam_block_weights), activation rows (x, x_full,
+ *   y_full, x_packed, y_packed, qkv_out) and the latent-io tensors are read
+ *   and written in 16-byte vectors and must be 16-byte aligned; the entry
+ *   points that take them return SWAM_E_INVALID otherwise.
  * Errors: every int-returning call returns SWAM_OK (0) or a negative
  *   swam_status.  Arguments are validated on the host before any launch; on
  *   error nothing is launched and swam_last_error() describes the problem.

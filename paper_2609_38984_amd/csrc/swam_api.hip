@@ -237,9 +237,16 @@ struct Timed {
   }
 };
 
-bool any_null_block(const swam_block_weights* w) {
-  return !w || !w->w_ada || !w->b_ada || !w->w_qkv || !w->b_qkv || !w->w_o || !w->b_o ||
-         !w->w_1 || !w->b_1 || !w->w_2 || !w->b_2;
+bool aligned16(const void* p) { return ((uintptr_t)p & 15) == 0; }
+
+// NULL or not 16-byte aligned (the kernels read weights in 16-byte vectors)
+bool bad_block(const swam_block_weights* w) {
+  if (!w) return true;
+  const void* p[10] = {w->w_ada, w->b_ada, w->w_qkv, w->b_qkv, w->w_o,
+                       w->b_o,   w->w_1,   w->b_1,   w->w_2,   w->b_2};
+  for (const void* q : p)
+    if (!q || !aligned16(q)) return true;
+  return false;
 }
 
 // one block in place on x [n_rows][d]; mod = this block's [6][d] modulation
@@ -665,6 +672,8 @@ int swam_export(swam_ctx* c, float* s_all, float* q, float* v, float* a, int32_t
 int swam_pack(swam_ctx* c, const void* x_full, void* x_packed) {
   if (!c) return set_err(nullptr, SWAM_E_INVALID, "ctx is NULL");
   if (!x_full || !x_packed) return set_err(c, SWAM_E_INVALID, "NULL tensor");
+  if (!aligned16(x_full) || !aligned16(x_packed))
+    return set_err(c, SWAM_E_INVALID, "tensors must be 16-byte aligned");
   if (!c->sel_valid) return set_err(c, SWAM_E_STATE, "no selection cached");
   Timed t(c, SWAM_T_PACK);
   SWAM_HIP(c, launch_pack(x_full, x_packed, c->ptr<int32_t>(c->lay.gather), c->packed_rows,
@@ -675,6 +684,8 @@ int swam_pack(swam_ctx* c, const void* x_full, void* x_packed) {
 int swam_unpack(swam_ctx* c, const void* y_packed, const void* x_full, void* y_full) {
   if (!c) return set_err(nullptr, SWAM_E_INVALID, "ctx is NULL");
   if (!y_packed || !x_full || !y_full) return set_err(c, SWAM_E_INVALID, "NULL tensor");
+  if (!aligned16(y_packed) || !aligned16(x_full) || !aligned16(y_full))
+    return set_err(c, SWAM_E_INVALID, "tensors must be 16-byte aligned");
   if (!c->sel_valid) return set_err(c, SWAM_E_STATE, "no selection cached");
   Timed t(c, SWAM_T_UNPACK);
   const int64_t rb = c->dv.d * c->dv.esz;
@@ -691,7 +702,9 @@ int swam_block(swam_ctx* c, const swam_block_weights* w, const float* temb, void
                int64_t n_rows, const int32_t* cu_seqlens, int32_t n_seqs, float* lse_out,
                void* qkv_out) {
   if (!c) return set_err(nullptr, SWAM_E_INVALID, "ctx is NULL");
-  if (any_null_block(w) || !temb || !x) return set_err(c, SWAM_E_INVALID, "NULL weight or tensor");
+  if (bad_block(w) || !temb || !x) return set_err(c, SWAM_E_INVALID, "NULL or unaligned weight, or NULL tensor");
+  if (!aligned16(x) || (qkv_out && !aligned16(qkv_out)))
+    return set_err(c, SWAM_E_INVALID, "x and qkv_out must be 16-byte aligned");
   if (n_rows < 0 || n_rows > c->dv.rows_full)
     return set_err(c, SWAM_E_SHAPE, "n_rows must be in [0, batch * l_full]");
   const int32_t* cu = cu_seqlens;
@@ -720,8 +733,11 @@ int check_step(swam_ctx* c, const swam_model* model, const void* x_full, const f
   if (!model || !model->blocks || model->n_blocks != cf.n_blocks)
     return set_err(c, SWAM_E_INVALID, "model must have config.n_blocks blocks");
   for (int l = 0; l < cf.n_blocks; ++l)
-    if (any_null_block(&model->blocks[l])) return set_err(c, SWAM_E_INVALID, "NULL block weight");
+    if (bad_block(&model->blocks[l]))
+      return set_err(c, SWAM_E_INVALID, "NULL or not 16-byte aligned block weight");
   if (!x_full || !y_full || !temb) return set_err(c, SWAM_E_INVALID, "NULL tensor");
+  if (!aligned16(x_full) || !aligned16(y_full))
+    return set_err(c, SWAM_E_INVALID, "x_full and y_full must be 16-byte aligned");
   if (tau < 0) return set_err(c, SWAM_E_INVALID, "tau < 0");
   if (flags & SWAM_STEP_FORCE_DENSE) *kind = SWAM_KIND_DENSE;
   else if ((flags & SWAM_STEP_FORCE_REFRESH) || tau % cf.reuse_R == 0) *kind = SWAM_KIND_REFRESH;
@@ -848,7 +864,6 @@ int swam_overlap(swam_ctx* c, const float* p, const float* q, int64_t n_maps, in
 
 // ------------------------------------------------------------- sampler
 
-static bool aligned16(const void* p) { return ((uintptr_t)p & 15) == 0; }
 
 static int check_io(swam_ctx* c, const swam_latent_io* io) {
   if (!io) return set_err(c, SWAM_E_INVALID, "latent io is NULL");

@@ -69,3 +69,33 @@ def test_block_with_zero_rows_is_a_no_op():
     ctx.block(dblocks[0], dev(W.timestep_embedding(cfg, 0)), x, 0, cu, 1)
     torch.cuda.synchronize()
     assert (x == 3.0).all()
+
+
+def test_misaligned_tensors_are_rejected_before_any_launch():
+    """The kernels move weights and activation rows in 16-byte vectors: a view
+    4 bytes off its allocation must come back as SWAM_E_INVALID from the host
+    checks, with nothing written."""
+    from paper_2609_38984_amd import swam
+    cfg = BASE
+    _, dblocks, model = model_for(cfg)
+    ctx = swam.Context(cfg)
+    n = cfg.l_full * cfg.d_model
+    buf = torch.zeros(2 * n + 8, dtype=torch.float32, device="cuda:0")
+    x_ok = buf[:n].view(cfg.l_full, cfg.d_model)
+    x_bad = buf[n + 1:2 * n + 1].view(cfg.l_full, cfg.d_model)
+    temb = dev(W.timestep_embedding(cfg, 0))
+    with pytest.raises(swam.SwamError) as e:
+        ctx.block(dblocks[0], temb, x_bad)
+    assert e.value.code == -1 and "aligned" in str(e.value)
+    w_bad = dict(dblocks[0])
+    wq = w_bad["w_qkv"]
+    wbuf = torch.zeros(wq.numel() + 8, dtype=wq.dtype, device="cuda:0")
+    w_bad["w_qkv"] = wbuf[1:1 + wq.numel()].view_as(wq)
+    with pytest.raises(swam.SwamError) as e:
+        ctx.block(w_bad, temb, x_ok)
+    assert e.value.code == -1 and "aligned" in str(e.value)
+    with pytest.raises(swam.SwamError) as e:
+        ctx.step(model, x_ok, temb, 0, x_bad)
+    assert e.value.code == -1 and "aligned" in str(e.value)
+    torch.cuda.synchronize()
+    assert bool((buf == 0).all())
