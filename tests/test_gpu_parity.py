@@ -92,6 +92,15 @@ def test_block_bf16_wide():
     _block_case(cfg, O.dense_cu(cfg), 2e-2, 5e-2)
 
 
+@pytest.mark.parametrize("d", [2560, 4096])
+def test_block_bf16_max_width(d):
+    # above d = 2048 rows take the 8-chunk path of the normalisation (2560 leaves
+    # lanes without a last chunk); 4096 is the largest bf16 width the library
+    # accepts.  Sequences of 130, 0 and 171 rows.
+    cfg = W.preset(2).replace(name=f"bf16-d{d}", d_model=d, n_heads=d // 64, n_blocks=1)
+    _block_case(cfg, np.array([0, 130, 130, 301]), 2e-2, 5e-2)
+
+
 # ---------------------------------------------------------------------------
 # (1) scoring
 # ---------------------------------------------------------------------------
@@ -245,6 +254,50 @@ def test_select_mass_threshold_ragged():
 def test_select_mass_threshold_with_anchors():
     _select_case(W.preset(5).replace(n_blocks=2, d_model=64, n_heads=1, batch=3, k_anchor=40,
                                      mass_threshold=0.55), 73)
+
+
+# frames at the library's maximum of 4096 tokens (the capacity of the selection
+# sort) and one below it (a 63 x 65 grid, not a power of two), in fixed-budget
+# and mass-threshold mode
+MAX_FRAME = {
+    "ns4096_fixed": W.preset(2).replace(name="ns4096-fixed", batch=2, n_blocks=8, d_model=128,
+                                        n_heads=2, n_frames=3, frame_h=64, frame_w=64, n_act=48,
+                                        k_core=900, k_anchor=300),
+    "ns4095_mass": W.preset(2).replace(name="ns4095-mass", batch=2, n_blocks=8, d_model=128,
+                                       n_heads=2, n_frames=3, frame_h=63, frame_w=65, n_act=48,
+                                       k_core=900, k_anchor=100, mass_threshold=0.6),
+}
+
+
+@pytest.mark.parametrize("name", list(MAX_FRAME))
+def test_select_bitexact_max_tokens_per_frame(name):
+    _select_case(MAX_FRAME[name], 74)
+
+
+@pytest.mark.parametrize("name", list(MAX_FRAME))
+def test_score_reduce_max_tokens_per_frame(name):
+    cfg = MAX_FRAME[name]
+    print(f"reduce case {cfg.name}", flush=True)
+    rng = np.random.default_rng(75)
+    S = _random_scores(rng, cfg.batch, cfg.n_blocks, cfg.n_frames, cfg.n_s)
+    ctx = _ctx(cfg)
+    V = torch.empty(cfg.batch * cfg.n_frames * cfg.n_s, dtype=torch.float32, device="cuda:0")
+    A = torch.empty(cfg.batch * cfg.n_s, dtype=torch.float32, device="cuda:0")
+    Q = torch.empty(cfg.batch * cfg.n_blocks, dtype=torch.float32, device="cuda:0")
+    core = torch.empty(cfg.batch * 6, dtype=torch.int32, device="cuda:0")
+    ctx.score_reduce(dev(S), V, A, Q, core)
+    torch.cuda.synchronize()
+    for b in range(cfg.batch):
+        r = O.score_reduce(S[b], cfg.k_layer, cfg.cv_penalty)
+        np.testing.assert_array_equal(host(core)[b * 6:(b + 1) * 6], r.L_core)
+        assert maxrel(host(Q)[b * cfg.n_blocks:(b + 1) * cfg.n_blocks], r.Q) < 1e-6
+        assert rowwise_maxrel(host(V).reshape(cfg.batch, cfg.n_frames, cfg.n_s)[b], r.V) < 1e-5
+        assert maxrel(host(A).reshape(cfg.batch, cfg.n_s)[b], r.A) < 1e-5
+
+
+@pytest.mark.parametrize("mode", ["A", "B"])
+def test_score_bf16_max_tokens_per_frame(mode):
+    _score_case(MAX_FRAME["ns4096_fixed"].replace(dtype="bf16"), mode)
 
 
 # ---------------------------------------------------------------------------
