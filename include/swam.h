@@ -161,6 +161,10 @@ typedef struct swam_ctx swam_ctx;
  * context; on error *out is NULL. */
 int swam_create(const swam_config* cfg, void* stream, swam_ctx** out);
 int swam_destroy(swam_ctx* ctx);
+/* Bind another stream (a hipStream_t; NULL = the null stream).  Later calls
+ * run on it after everything already queued on the previous stream: the new
+ * stream waits on an event recorded there (no host synchronisation).  Not
+ * allowed while swam_step_graph captures (SWAM_E_STATE). */
 int swam_set_stream(swam_ctx* ctx, void* stream);
 
 /* Derived sizes; validates cfg exactly as swam_create does, without a GPU. */

@@ -8,6 +8,7 @@
 
 #include <algorithm>
 #include <numeric>
+#include <new>
 #include <string>
 #include <vector>
 
@@ -179,6 +180,7 @@ struct swam_ctx {
   int device = 0;
   char* arena = nullptr;
   int32_t* host_cu = nullptr;   // pinned
+  hipEvent_t order_ev = nullptr; // orders a newly bound stream after the previous one
   bool sel_valid = false, scores_valid = false;
   int64_t packed_rows = 0;
   std::string err;
@@ -478,7 +480,8 @@ int swam_create(const swam_config* cfg, void* stream, swam_ctx** out) {
   Derived dv{};
   int rc = derive(cfg, &dv, &g_err);
   if (rc != SWAM_OK) return rc;
-  swam_ctx* c = new swam_ctx();
+  swam_ctx* c = new (std::nothrow) swam_ctx();
+  if (!c) return set_err(nullptr, SWAM_E_NOMEM, "context allocation");
   c->cfg = *cfg;
   c->dv = dv;
   c->lay = layout_for(cfg, dv);
@@ -491,6 +494,7 @@ int swam_create(const swam_config* cfg, void* stream, swam_ctx** out) {
     return e == hipErrorOutOfMemory ? SWAM_E_NOMEM : SWAM_E_HIP;
   }
   e = hipHostMalloc((void**)&c->host_cu, (cfg->batch + 1) * sizeof(int32_t), 0);
+  if (e == hipSuccess) e = hipEventCreateWithFlags(&c->order_ev, hipEventDisableTiming);
   if (e == hipSuccess) {
     float alpha[16];
     fill_alpha((int)dv.g, alpha);
@@ -522,13 +526,22 @@ int swam_destroy(swam_ctx* c) {
   for (hipEvent_t ev : c->ev) hipEventDestroy(ev);
   if (c->arena) hipFree(c->arena);
   if (c->host_cu) hipHostFree(c->host_cu);
+  if (c->order_ev) hipEventDestroy(c->order_ev);
   delete c;
   return SWAM_OK;
 }
 
 int swam_set_stream(swam_ctx* c, void* stream) {
   if (!c) return set_err(nullptr, SWAM_E_INVALID, "ctx is NULL");
-  c->st = (hipStream_t)stream;
+  if (c->capturing) return set_err(c, SWAM_E_STATE, "stream switch during graph capture");
+  const hipStream_t next = (hipStream_t)stream;
+  if (next != c->st) {
+    // work queued on the previous stream uses the same workspace: the new
+    // stream waits for it (no host synchronisation)
+    SWAM_HIP(c, hipEventRecord(c->order_ev, c->st), "order event record");
+    SWAM_HIP(c, hipStreamWaitEvent(next, c->order_ev, 0), "order event wait");
+    c->st = next;
+  }
   return SWAM_OK;
 }
 

@@ -225,6 +225,12 @@ class Context:
     def _ok(self, rc):
         _check(self.lib, self.h, rc)
 
+    def set_stream(self, stream: torch.cuda.Stream):
+        """swam_set_stream: later calls run on `stream`, after the work already
+        queued on the previous one."""
+        self._ok(self.lib.swam_set_stream(self.h, C.c_void_p(stream.cuda_stream)))
+        self.stream = stream
+
     # -- sizes -----------------------------------------------------------------
     @property
     def n_s(self):

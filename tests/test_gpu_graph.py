@@ -3,6 +3,8 @@
 Each schedule is run eagerly in one context and through swam_step_graph in
 another (on a non-default stream); every replay -- with eager work and
 synchronisations in between -- must match the eager output byte for byte.
+A context moved between two streams step by step (swam_set_stream, no host
+synchronisation) must match a one-stream run the same way.
 """
 import numpy as np
 import pytest
@@ -72,3 +74,34 @@ def test_graph_needs_non_default_stream():
     with pytest.raises(swam.SwamError) as e:
         ctx.step_graph(model, x, torch.zeros(cfg.d_temb, device="cuda:0"), 0, torch.empty_like(x))
     assert e.value.code == -4
+
+
+def test_stream_switch_orders_after_queued_work():
+    """swam_set_stream between the steps of a schedule, with no host
+    synchronisation: every sparse step on the second stream reads the
+    selection the refresh on the first stream wrote, and the outputs equal a
+    one-stream run byte for byte."""
+    from paper_2609_38984_amd import swam
+    cfg = _small()
+    blocks, _, model = model_for(cfg)
+    inp = W.make_inputs(cfg, blocks[0]["w_qkv"])
+    dt = act_dtype(cfg)
+    xs = [dev(inp.x(t), dt) for t in range(cfg.n_steps)]
+    ts = [dev(inp.temb(t)) for t in range(cfg.n_steps)]
+    ref = [torch.empty_like(x) for x in xs]
+    got = [torch.empty_like(x) for x in xs]
+    torch.cuda.synchronize()
+    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+    one = swam.Context(cfg, stream=s1)
+    for t in range(cfg.n_steps):
+        one.step(model, xs[t], ts[t], t, ref[t])
+    two = swam.Context(cfg, stream=s1)
+    kinds = []
+    for t in range(cfg.n_steps):
+        two.set_stream(s1 if t % 2 == 0 else s2)
+        kinds.append(two.step(model, xs[t], ts[t], t, got[t]))
+    torch.cuda.synchronize()
+    print(f"step kinds {kinds}", flush=True)
+    assert swam.KIND_SPARSE in kinds
+    for t in range(cfg.n_steps):
+        assert torch.equal(got[t].view(torch.int16), ref[t].view(torch.int16)), t
