@@ -31,8 +31,13 @@ def _small(**kw):
     return W.SwamConfig(**base)
 
 
+# "guided" records the partner copies of the selection (device-to-device copy
+# nodes); "rope_qknorm" the QKV projection with its fused rotary / norm store
 @pytest.mark.parametrize("cfg", [_small(), _small(mass_threshold=0.8, k_core=72, k_anchor=0),
-                                 W.preset(1).replace(n_steps=6)], ids=["fixed", "mass", "fp32"])
+                                 W.preset(1).replace(n_steps=6),
+                                 _small(cfg_pairs=1, guidance=3.0),
+                                 _small(rope=1, qk_norm=1)],
+                         ids=["fixed", "mass", "fp32", "guided", "rope_qknorm"])
 def test_graph_replays_match_eager(cfg):
     from paper_2609_38984_amd import swam
     print(f"graph case {cfg.name} mass={cfg.mass_threshold}", flush=True)
