@@ -90,6 +90,9 @@ def test_plan_rejects_bad_configs(lib, bad, code):
 def test_null_context_is_rejected(lib):
     assert lib.swam_pack(None, None, None) == -1
     assert lib.swam_step(None, None, None, None, 0, None, 0, None) == -1
+    assert lib.swam_set_stream(None, None) == -1
+    assert lib.swam_packed_rows(None, None) == -1
+    assert lib.swam_graph_clear(None) == -1
     assert lib.swam_destroy(None) == 0
 
 
