@@ -1,0 +1,141 @@
+"""The oracle's pins catch plausible mistakes: each case plants one (a dropped
+term, a wrong sign, index or order, a transposed operand, a wrong normaliser)
+into the oracle on the CPU and checks that the pin named beside it fails.
+
+Mistakes are planted by swapping one oracle function for a wrong variant
+(monkeypatch, in the package namespace and in the module the other oracle
+functions look it up in); nothing is changed on disk.
+"""
+import math
+
+import numpy as np
+import pytest
+
+import oracle as O
+import oracle.swam_oracle as SO
+import test_oracle_pins as P
+
+
+def _plant(monkeypatch, name, fn):
+    monkeypatch.setattr(SO, name, fn)
+    monkeypatch.setattr(O, name, fn)
+
+
+def _ln_uncentred(x):
+    x = np.asarray(x, np.float64)
+    return x / np.sqrt((x * x).mean(axis=-1, keepdims=True) + SO.LN_EPS)
+
+
+def _gelu_no_cubic(u):
+    u = np.asarray(u, np.float64)
+    return 0.5 * u * (1.0 + np.tanh(math.sqrt(2.0 / math.pi) * u))
+
+
+def _round_bf16_truncate(x):
+    x32 = np.ascontiguousarray(np.asarray(x, np.float64).astype(np.float32))
+    bits = x32.view(np.uint32) & np.uint32(0xFFFF0000)
+    return bits.view(np.float32).astype(np.float64)
+
+
+def _topk_high_index_ties(scores, candidates, k):
+    cand = np.asarray(sorted(int(c) for c in candidates), dtype=np.int64)
+    s = np.asarray(scores)[cand]
+    order = np.lexsort((-cand, -s.astype(np.float64)))
+    return np.sort(cand[order[:k]])
+
+
+def _mutants():
+    ln, mod, score, att = SO.layer_norm, SO.modulation, SO.score, SO.attention
+    lq, wm, ak, pm, mc = SO.layer_quality, SO.weighted_mean, SO.anchor_key, SO.pack_map, SO.mass_count
+
+    def mod_swapped(w, b, t):
+        s = mod(w, b, t)
+        return [s[1], s[0], s[2], s[4], s[3], s[5]]          # shift and scale exchanged
+
+    def score_lambda_off(q, k, lse, F, n_s, nh, alpha=None):
+        return score(q, k, np.asarray(lse) + 1.0, F, n_s, nh, alpha)
+
+    def attention_one_sequence(q, k, v, cu, nh):
+        return att(q, k, v, np.array([0, int(np.asarray(cu)[-1])]), nh)
+
+    def attention_scale_hd(q, k, v, cu, nh):
+        return att(np.asarray(q, np.float64) / 8.0, k, v, cu, nh)  # 1/hd instead of 1/sqrt(hd)
+
+    def quality_sign(S):
+        R, E, _ = lq(S)
+        return R, E, R * (1.0 + E)
+
+    def mean_unweighted(S, Q, layers):
+        return wm(S, np.ones(len(np.asarray(Q))), layers)
+
+    def anchor_no_penalty(V, c=1.0):
+        return ak(V, 0.0)
+
+    def pack_inclusive(mask, batch):
+        r = pm(mask, batch)
+        r.pack_pos[r.pack_pos >= 0] += 1
+        return r
+
+    def mass_plus_one(v, pool, theta):
+        return min(mc(v, pool, theta) + 1, len(list(pool)))
+
+    return {
+        "layer norm without centring": ("layer_norm", _ln_uncentred,
+                                        [P.test_block_matches_torch_composition]),
+        "shift and scale exchanged": ("modulation", mod_swapped,
+                                      [P.test_block_matches_torch_composition]),
+        "GELU without its cubic term": ("gelu_tanh", _gelu_no_cubic,
+                                        [P.test_block_matches_torch_composition]),
+        "attention scaled by 1/hd": ("attention", attention_scale_hd,
+                                     [P.test_attention_rows_sum_to_one_and_match_library]),
+        "attention across sequences": ("attention", attention_one_sequence,
+                                       [P.test_varlen_attention_isolates_sequences]),
+        "score normaliser off by one": ("score", score_lambda_off,
+                                        [lambda: P.test_score_equals_head_mean_attention(2, 4, 2),
+                                         P.test_score_hand_example]),
+        "uniform query weights": ("alpha_weights", lambda g: np.full(g, 1.0 / g),
+                                  [lambda: P.test_alpha_printed_values(_golden())]),
+        "quality with the entropy's sign flipped": ("layer_quality", quality_sign,
+                                                    [P.test_entropy_closed_forms]),
+        "unweighted core-layer mean": ("weighted_mean", mean_unweighted,
+                                       [P.test_weighted_mean_closed_forms]),
+        "anchor key without the CV penalty": ("anchor_key", anchor_no_penalty,
+                                              [P.test_anchor_key_closed_forms]),
+        "top-k ties to the highest index": ("topk", _topk_high_index_ties,
+                                            [P.test_topk_exhaustive_with_ties]),
+        "mass count one too many": ("mass_count", mass_plus_one,
+                                    [P.test_mass_threshold_bruteforce_and_monotone]),
+        "inclusive prefix sum in the pack map": ("pack_map", pack_inclusive,
+                                                 [P.test_pack_unpack_invariants]),
+        "bf16 storage by truncation": ("round_bf16", _round_bf16_truncate,
+                                       [P.test_storage_rounding_bf16_ties_to_even]),
+        "refresh on the last step of each interval": (
+            "is_refresh", lambda tau, R: tau % R == R - 1,
+            [P.test_refresh_is_dense_and_reuse_equals_reselection]),
+    }
+
+
+def _golden():
+    import json
+    import os
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    with open(os.path.join(root, "tests", "golden", "paper_constants.json")) as fh:
+        return json.load(fh)
+
+
+MUTANTS = _mutants()
+
+
+@pytest.mark.parametrize("name", list(MUTANTS))
+def test_pins_catch_planted_mistake(name, monkeypatch):
+    target, fn, pins = MUTANTS[name]
+    for pin in pins:
+        pin()                                   # passes on the unchanged oracle
+    _plant(monkeypatch, target, fn)
+    caught = 0
+    for pin in pins:
+        try:
+            pin()
+        except Exception:                      # a failed check, or the pin cannot run
+            caught += 1
+    assert caught > 0, f"no pin caught: {name}"
