@@ -12,11 +12,17 @@ import numpy as np
 import pytest
 
 import oracle as O
+import oracle.sampler_oracle as SA
 import oracle.swam_oracle as SO
 import test_oracle_pins as P
+import test_oracle_sampler as PS
+import test_oracle_variants as PV
 
 
 def _plant(monkeypatch, name, fn):
+    if hasattr(SA, name) and not hasattr(SO, name):
+        monkeypatch.setattr(SA, name, fn)          # sampler oracle
+        return
     monkeypatch.setattr(SO, name, fn)
     monkeypatch.setattr(O, name, fn)
 
@@ -79,6 +85,24 @@ def _mutants():
     def mass_plus_one(v, pool, theta):
         return min(mc(v, pool, theta) + 1, len(list(pool)))
 
+    sig, eul, mrg = SA.sigmas, SA.euler_update, SA.merge_velocity
+    rope, qkn = SO.apply_rope, SO.qk_rms_norm
+
+    def sigmas_unshifted(n, shift=SA.SCHEDULE_SHIFT):
+        return sig(n, 1.0)
+
+    def euler_wrong_sign(z, v, dsigma):
+        return eul(z, v, -dsigma)
+
+    def merge_swapped(v_cur, v_cached, keep):
+        return mrg(v_cur, v_cached, ~np.asarray(keep, bool))
+
+    def rope_reversed(x, positions, nh):
+        return rope(x, -np.asarray(positions), nh)
+
+    def qk_norm_sum(x, nh, eps=SO.LN_EPS):
+        return qkn(x, nh, eps) / 8.0                 # root of the sum, not the mean, of squares
+
     return {
         "layer norm without centring": ("layer_norm", _ln_uncentred,
                                         [P.test_block_matches_torch_composition]),
@@ -112,6 +136,17 @@ def _mutants():
         "refresh on the last step of each interval": (
             "is_refresh", lambda tau, R: tau % R == R - 1,
             [P.test_refresh_is_dense_and_reuse_equals_reselection]),
+        "flow schedule without its shift": ("sigmas", sigmas_unshifted,
+                                            [PS.test_sigmas_closed_form_n4]),
+        "Euler step with the wrong sign": ("euler_update", euler_wrong_sign,
+                                           [PS.test_euler_integrates_the_straight_flow_exactly]),
+        "merge takes the cache at retained rows": (
+            "merge_velocity", merge_swapped,
+            [PS.test_merge_selects_current_or_cached_rowwise]),
+        "rotary angles reversed": ("apply_rope", rope_reversed,
+                                   [PV.test_rope_closed_form_single_pair_and_identity_at_zero]),
+        "QK-norm by the root sum of squares": ("qk_rms_norm", qk_norm_sum,
+                                               [PV.test_qk_norm_gives_unit_rms_heads]),
     }
 
 
