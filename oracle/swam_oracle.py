@@ -432,30 +432,38 @@ MASS_SCALE_BITS = 40
 
 
 def threshold_fraction(theta: float) -> Fraction:
-    """Mass threshold as an exact fraction with denominator dividing 1000."""
-    return Fraction(int(round(theta * 1000)), 1000)
+    """Mass threshold as an exact fraction with denominator dividing 1000.
+
+    The threshold is a float32 configuration value; 1000 times it is formed
+    exactly (Fraction arithmetic) and rounded to the nearest integer (a float32
+    value is a dyadic rational, so 1000 theta is never halfway between
+    integers).  A numerator of 0 (theta below 0.0005) is allowed."""
+    exact = Fraction(float(np.float32(theta))) * 1000
+    num = math.floor(exact + Fraction(1, 2))
+    return Fraction(num, 1000)
+
+
+def mass_code(val) -> int:
+    """Integer code of one fp32 score for the mass rule: floor(V 2^40) of the
+    exact fp32 value, 0 for V <= 0 and 2^40 for V >= 1."""
+    val = float(np.float32(val))
+    if not val > 0.0:
+        return 0
+    if val >= 1.0:
+        return 1 << MASS_SCALE_BITS
+    return math.floor(Fraction(val) * (1 << MASS_SCALE_BITS))
 
 
 def mass_count(v_row, pool, theta):
     """Per-frame core count from a score-mass threshold (ragged extension).
 
-    q_j = floor(V(f,j) 2^40) exactly from the fp32 value (clamped to [0, 2^40]),
-    T = sum over all positions, and candidates of the pool are walked in top-k
-    order; k is the smallest count >= 1 whose prefix reaches theta * T, capped
-    at the pool size.
+    q_j = mass_code(V(f,j)), T = sum over all positions, and candidates of the
+    pool are walked in top-k order; k is the smallest count >= 1 whose prefix
+    reaches theta * T, capped at the pool size.
     """
     frac = threshold_fraction(theta)
     v32 = np.asarray(v_row, dtype=np.float32)
-
-    def code(val):
-        val = float(val)
-        if not val > 0.0:
-            return 0
-        if val >= 1.0:
-            return 1 << MASS_SCALE_BITS
-        return math.floor(Fraction(val) * (1 << MASS_SCALE_BITS))
-
-    q = [code(val) for val in v32]
+    q = [mass_code(val) for val in v32]
     T = sum(q)
     ranked = sorted((int(j) for j in pool), key=lambda j: (-float(v32[j]), j))
     run = 0

@@ -50,6 +50,20 @@ def _topk_high_index_ties(scores, candidates, k):
     return np.sort(cand[order[:k]])
 
 
+def mass_code_nearest(val):
+    val = float(np.float32(val))
+    if not val > 0.0:
+        return 0
+    if val >= 1.0:
+        return 1 << SO.MASS_SCALE_BITS
+    return round(val * (1 << SO.MASS_SCALE_BITS))
+
+
+def threshold_float64(theta):
+    from fractions import Fraction
+    return Fraction(max(1, int(round(theta * 1000))), 1000)
+
+
 def _mutants():
     ln, mod, score, att = SO.layer_norm, SO.modulation, SO.score, SO.attention
     lq, wm, ak, pm, mc = SO.layer_quality, SO.weighted_mean, SO.anchor_key, SO.pack_map, SO.mass_count
@@ -129,6 +143,11 @@ def _mutants():
                                             [P.test_topk_exhaustive_with_ties]),
         "mass count one too many": ("mass_count", mass_plus_one,
                                     [P.test_mass_threshold_bruteforce_and_monotone]),
+        "mass code rounded to nearest": ("mass_code", mass_code_nearest,
+                                         [P.test_mass_code_floors_values_off_the_grid]),
+        "threshold numerator from the float64 value, at least 1": (
+            "threshold_fraction", threshold_float64,
+            [P.test_threshold_fraction_rounds_the_float32_value]),
         "inclusive prefix sum in the pack map": ("pack_map", pack_inclusive,
                                                  [P.test_pack_unpack_invariants]),
         "bf16 storage by truncation": ("round_bf16", _round_bf16_truncate,

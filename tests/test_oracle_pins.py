@@ -340,6 +340,68 @@ def test_mass_threshold_bruteforce_and_monotone():
     assert O.mass_count(z, np.arange(6), 0.8) == 1                        # smallest k >= 1
 
 
+def _mass_bruteforce(v, pool, frac, rounding):
+    """The mass rule literally: codes rounding(V 2^40) of the exact fp32 values
+    (clamped to [0, 2^40]), the pool walked in (score desc, index asc) order,
+    the smallest k >= 1 whose prefix reaches frac * T."""
+    def q(x):
+        x = Fraction(float(x))
+        return 0 if x <= 0 else (1 << 40) if x >= 1 else rounding(x * (1 << 40))
+    codes = [q(x) for x in v]
+    T = sum(codes)
+    ranked = sorted((int(j) for j in pool), key=lambda j: (-float(v[j]), j))
+    run = 0
+    for k, j in enumerate(ranked, start=1):
+        run += codes[j]
+        if run >= frac * T:
+            return k
+    return len(ranked)
+
+
+def test_mass_code_floors_values_off_the_grid():
+    """Scores of a few 2^-40 units with fractional parts: the count must follow
+    floor(V 2^40), and the cases are chosen so that rounding to nearest or up
+    would change it somewhere."""
+    rng = np.random.default_rng(13)
+    differ_round = differ_ceil = 0
+    for _ in range(300):
+        n_s = int(rng.integers(3, 10))
+        v = (rng.uniform(0.05, 6.0, n_s) * 2.0 ** -40).astype(np.float32)
+        pool = np.arange(n_s)
+        for theta in (0.2, 0.5, 0.8, 0.95):
+            frac = O.threshold_fraction(theta)
+            want = _mass_bruteforce(v, pool, frac, math.floor)
+            assert O.mass_count(v, pool, theta) == want
+            differ_round += want != _mass_bruteforce(v, pool, frac, lambda x: math.floor(x + Fraction(1, 2)))
+            differ_ceil += want != _mass_bruteforce(v, pool, frac, math.ceil)
+        # single codes straight from the definition
+        for x in v:
+            assert O.mass_code(x) == math.floor(Fraction(float(x)) * (1 << 40))
+    assert differ_round > 0 and differ_ceil > 0
+    # codes saturate at 1 and vanish at or below 0
+    assert O.mass_code(np.float32(1.0)) == O.mass_code(np.float32(3.0)) == 1 << 40
+    assert O.mass_code(np.float32(0.0)) == O.mass_code(np.float32(-1.0)) == 0
+    assert O.mass_code(np.float32(2.0 ** -41)) == 0 and O.mass_code(np.float32(2.0 ** -40)) == 1
+
+
+def test_threshold_fraction_rounds_the_float32_value():
+    """theta = num / 1000 with num the integer nearest to 1000 times the float32
+    threshold (the value the configuration carries)."""
+    assert O.threshold_fraction(0.0125) == Fraction(13, 1000)   # float32(0.0125) > 1/80
+    assert O.threshold_fraction(0.0004) == 0                     # below 1/2000: zero
+    assert O.threshold_fraction(0.0005) == Fraction(1, 1000)     # float32(0.0005) > 1/2000
+    assert O.threshold_fraction(0.8) == Fraction(4, 5)
+    assert O.threshold_fraction(1.0) == 1
+    rng = np.random.default_rng(14)
+    for t in rng.uniform(0.0, 1.0, 2000).astype(np.float32):
+        exact = Fraction(float(t)) * 1000
+        num = O.threshold_fraction(float(t)) * 1000
+        assert num.denominator == 1 and abs(exact - num) < Fraction(1, 2)
+    # a zero numerator keeps one core token per frame
+    v = np.array([0.1, 0.5, 0.2, 0.2], np.float32)
+    assert O.mass_count(v, np.arange(4), 0.0004) == 1
+
+
 # ---------------------------------------------------------------------------
 # packing, steps, reuse
 # ---------------------------------------------------------------------------
