@@ -386,6 +386,16 @@ int swam_velocity(swam_ctx* ctx, const swam_latent_io* io, const void* y_full,
 int swam_sample_update(swam_ctx* ctx, int32_t d_latent, const float* v, float* v_cache,
                        float* z, float dsigma, int32_t kind);
 
+/* Noise levels of the sampler's flow schedule with a shift (the paper's
+ * backbones use shift 5.0, App. B.2): sigma_i = shift s / (1 + (shift - 1) s)
+ * with s = 1 - i / n_steps, for i = 0 .. n_steps, from 1 (pure noise) down to
+ * 0; the model time of step i is 1000 sigma_i and its update uses
+ * dsigma = sigma_{i+1} - sigma_i.  sigmas is a HOST array of n_steps + 1
+ * doubles owned by the caller.  Pure host arithmetic: needs no context, no
+ * GPU and no stream.  SWAM_E_INVALID for n_steps < 1, a shift that is not
+ * finite and positive, or sigmas NULL. */
+int swam_flow_sigmas(int32_t n_steps, double shift, double* sigmas);
+
 /* One closed-loop sampling step: swam_embed(z -> x_full), swam_step(x_full ->
  * y_full), swam_velocity (all latent rows after a full step, the retained
  * rows after a sparse one) and swam_sample_update with the step's kind.

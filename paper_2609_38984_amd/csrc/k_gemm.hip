@@ -189,7 +189,9 @@ __device__ __forceinline__ void mma_stage(const uint4* __restrict__ as, const ui
 // are 8 rows apart; only bit 3 of the row enters the swizzle, so two
 // per-lane offsets (even / odd slab) plus a wave-uniform step address them
 // all.
-template <int BM, int BN, int WM, int WN, int EPI>
+// ROLE (a GemmRole) only names the instantiation after the block's
+// projection, so a kernel trace tells the four projections apart.
+template <int ROLE, int BM, int BN, int WM, int WN, int EPI>
 __global__ void __launch_bounds__(WM * WN * 64)
 gemm_bf16_nt(const bf16_t* __restrict__ A, int64_t lda, const bf16_t* __restrict__ B,
              int64_t ldb, const bf16_t* __restrict__ bias, const float* __restrict__ gate,
@@ -332,7 +334,7 @@ gemm_bf16_nt(const bf16_t* __restrict__ A, int64_t lda, const bf16_t* __restrict
 
 // Sum of the split-K partials and the epilogue: one thread per 8 columns of
 // a row (16-byte bias / residual loads and stores, 32-byte partial loads).
-template <int EPI>
+template <int ROLE, int EPI>
 __global__ void __launch_bounds__(256)
 splitk_epilogue(const float* __restrict__ part, int splits, int M, int N,
                 const bf16_t* __restrict__ bias, const float* __restrict__ gate, bf16_t* C,
@@ -426,14 +428,14 @@ gemm_f32_nt(const float* __restrict__ A, int64_t lda, const float* __restrict__ 
 // ---------------------------------------------------------------------------
 // host side
 // ---------------------------------------------------------------------------
-template <int BM, int BN, int WM, int WN, int EPI>
+template <int ROLE, int BM, int BN, int WM, int WN, int EPI>
 static hipError_t run_bf16(const void* A, int64_t lda, const void* B, int64_t ldb,
                            const void* bias, const float* gate, void* C, int64_t ldc, int M,
                            int N, int K, int splits, float* part, hipStream_t st,
                            const QkPost& qp = QkPost{}) {
   const int tiles_m = (M + BM - 1) / BM, tiles_n = (N + BN - 1) / BN;
   if (splits <= 1) {
-    hipLaunchKernelGGL((gemm_bf16_nt<BM, BN, WM, WN, EPI>), dim3(tiles_m * tiles_n),
+    hipLaunchKernelGGL((gemm_bf16_nt<ROLE, BM, BN, WM, WN, EPI>), dim3(tiles_m * tiles_n),
                        dim3(WM * WN * 64), 0, st, (const bf16_t*)A, lda, (const bf16_t*)B, ldb,
                        (const bf16_t*)bias, gate, (bf16_t*)C, ldc, M, N, K, tiles_m, tiles_n,
                        (float*)nullptr, qp);
@@ -442,14 +444,14 @@ static hipError_t run_bf16(const void* A, int64_t lda, const void* B, int64_t ld
   if constexpr (EPI == EPI_BIAS_QKPOST) {
     return hipErrorNotSupported;             // no split-K store with the QK post-processing
   } else {
-    hipLaunchKernelGGL((gemm_bf16_nt<BM, BN, WM, WN, EPI_PARTIAL>), dim3(tiles_m * tiles_n, splits),
+    hipLaunchKernelGGL((gemm_bf16_nt<ROLE, BM, BN, WM, WN, EPI_PARTIAL>), dim3(tiles_m * tiles_n, splits),
                        dim3(WM * WN * 64), 0, st, (const bf16_t*)A, lda, (const bf16_t*)B, ldb,
                        (const bf16_t*)bias, gate, (bf16_t*)C, ldc, M, N, K, tiles_m, tiles_n, part,
                        QkPost{});
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     const int64_t n = (int64_t)M * (N / 8);
-    hipLaunchKernelGGL(splitk_epilogue<EPI>, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st,
+    hipLaunchKernelGGL((splitk_epilogue<ROLE, EPI>), dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st,
                        part, splits, M, N, (const bf16_t*)bias, gate, (bf16_t*)C, ldc);
     return hipGetLastError();
   }
@@ -458,14 +460,15 @@ static hipError_t run_bf16(const void* A, int64_t lda, const void* B, int64_t ld
 // Tile and K-split choice: modelled time = rounds * (per-CU MFMA work of one
 // round / tile efficiency) + (split > 1) the partial-sum pass over HBM.  A
 // round places `per_cu` workgroups on each of the 256 CUs (LDS-limited).  The
-// 256x256 and 256x128 kernels fit one workgroup per CU and run in whole
-// rounds; two 128x128 workgroups share a CU and start as soon as a slot
-// frees, so their rounds count in halves once a grid spills past one slot per
-// CU.  The efficiencies are the per-CU MFMA rates of the three kernels
-// measured on the block shapes of the d = 1536 and d = 2048 workloads,
-// relative to the 256x256 kernel (whose rate, about 40% of the per-CU peak,
-// is the base); the pass moves splits * M * N fp32 partials plus the bf16
-// output (and residual) at about 4 TB/s.
+// 256x256 kernel fits one workgroup per CU and runs in whole rounds; two
+// 128x128 workgroups share a CU and start as soon as a slot frees, so their
+// rounds count in halves once a grid spills past one slot per CU.  The
+// efficiencies are the per-CU MFMA rates of the two kernels measured on the
+// block shapes of the d = 1536 and d = 2048 workloads, relative to the
+// 256x256 kernel (whose rate, about 40% of the per-CU peak, is the base); the
+// pass moves splits * M * N fp32 partials plus the bf16 output (and
+// residual) at about 4 TB/s.  (A 256x128 tile measured at 0.72 of that rate
+// never won at any block shape from d = 256 to 4096 and was dropped.)
 struct GemmPlan { int tile, splits; };
 static GemmPlan choose_gemm(int64_t M, int64_t N, int64_t K, int64_t ws_floats) {
   static int forced = -2, forced_split = -2;
@@ -476,14 +479,14 @@ static GemmPlan choose_gemm(int64_t M, int64_t N, int64_t K, int64_t ws_floats) 
     forced_split = f ? atoi(f) : -1;
   }
   struct Cand { int bm, bn, per_cu; double eff; };
-  const Cand c[3] = {{256, 256, 1, 1.0}, {256, 128, 1, 0.72}, {128, 128, 2, 0.80}};
+  const Cand c[2] = {{256, 256, 1, 1.0}, {128, 128, 2, 0.80}};
   const int split_opts[6] = {1, 2, 3, 4, 6, 8};
   const int64_t kt = K / GEMM_BK;
   const double cu_flops = 2.5e15 / 256.0 * 0.40;        // sustained MFMA rate per CU
   GemmPlan best{0, 1};
   double best_t = 1e30;
-  for (int i = 0; i < 3; ++i) {
-    if (forced >= 0 && forced <= 2 && i != forced) continue;
+  for (int i = 0; i < 2; ++i) {
+    if (forced >= 0 && forced <= 1 && i != forced) continue;
     const int64_t tiles = ((M + c[i].bm - 1) / c[i].bm) * ((N + c[i].bn - 1) / c[i].bn);
     for (int s : split_opts) {
       if (forced_split >= 1 && s != forced_split) continue;
@@ -507,17 +510,15 @@ static GemmPlan choose_gemm(int64_t M, int64_t N, int64_t K, int64_t ws_floats) 
   return best;
 }
 
-template <int EPI>
+template <int ROLE, int EPI>
 static hipError_t dispatch_bf16(const void* A, int64_t lda, const void* B, int64_t ldb,
                                 const void* bias, const float* gate, void* C, int64_t ldc,
                                 int M, int N, int K, float* ws, int64_t ws_floats,
                                 hipStream_t st) {
   const GemmPlan p = choose_gemm(M, N, K, ws ? ws_floats : 0);
-  switch (p.tile) {
-    case 0: return run_bf16<256, 256, 2, 4, EPI>(A, lda, B, ldb, bias, gate, C, ldc, M, N, K, p.splits, ws, st);
-    case 1: return run_bf16<256, 128, 4, 2, EPI>(A, lda, B, ldb, bias, gate, C, ldc, M, N, K, p.splits, ws, st);
-    default: return run_bf16<128, 128, 2, 2, EPI>(A, lda, B, ldb, bias, gate, C, ldc, M, N, K, p.splits, ws, st);
-  }
+  if (p.tile == 0)
+    return run_bf16<ROLE, 256, 256, 2, 4, EPI>(A, lda, B, ldb, bias, gate, C, ldc, M, N, K, p.splits, ws, st);
+  return run_bf16<ROLE, 128, 128, 2, 2, EPI>(A, lda, B, ldb, bias, gate, C, ldc, M, N, K, p.splits, ws, st);
 }
 
 template <int EPI>
@@ -530,23 +531,27 @@ static hipError_t run_f32(const void* A, int64_t lda, const void* B, int64_t ldb
   return hipGetLastError();
 }
 
-hipError_t launch_gemm(int dtype, int epi, const void* A, int64_t lda, const void* B,
+hipError_t launch_gemm(int dtype, int role, const void* A, int64_t lda, const void* B,
                        int64_t ldb, const void* bias, const float* gate, void* C,
                        int64_t ldc, int64_t M, int64_t N, int64_t K, hipStream_t st,
                        float* ws, int64_t ws_floats) {
   if (M <= 0) return hipSuccess;
   const int m = (int)M, n = (int)N, k = (int)K;
   if (dtype == 1) {
-    switch (epi) {
-      case EPI_BIAS: return dispatch_bf16<EPI_BIAS>(A, lda, B, ldb, bias, gate, C, ldc, m, n, k, ws, ws_floats, st);
-      case EPI_BIAS_GELU: return dispatch_bf16<EPI_BIAS_GELU>(A, lda, B, ldb, bias, gate, C, ldc, m, n, k, ws, ws_floats, st);
-      default: return dispatch_bf16<EPI_BIAS_GATED_RESIDUAL>(A, lda, B, ldb, bias, gate, C, ldc, m, n, k, ws, ws_floats, st);
+    switch (role) {
+      case ROLE_QKV: return dispatch_bf16<ROLE_QKV, EPI_BIAS>(A, lda, B, ldb, bias, gate, C, ldc, m, n, k, ws, ws_floats, st);
+      case ROLE_UP: return dispatch_bf16<ROLE_UP, EPI_BIAS_GELU>(A, lda, B, ldb, bias, gate, C, ldc, m, n, k, ws, ws_floats, st);
+      case ROLE_OUT: return dispatch_bf16<ROLE_OUT, EPI_BIAS_GATED_RESIDUAL>(A, lda, B, ldb, bias, gate, C, ldc, m, n, k, ws, ws_floats, st);
+      case ROLE_DOWN: return dispatch_bf16<ROLE_DOWN, EPI_BIAS_GATED_RESIDUAL>(A, lda, B, ldb, bias, gate, C, ldc, m, n, k, ws, ws_floats, st);
+      default: return hipErrorInvalidValue;
     }
   }
-  switch (epi) {
-    case EPI_BIAS: return run_f32<EPI_BIAS>(A, lda, B, ldb, bias, gate, C, ldc, m, n, k, st);
-    case EPI_BIAS_GELU: return run_f32<EPI_BIAS_GELU>(A, lda, B, ldb, bias, gate, C, ldc, m, n, k, st);
-    default: return run_f32<EPI_BIAS_GATED_RESIDUAL>(A, lda, B, ldb, bias, gate, C, ldc, m, n, k, st);
+  switch (role) {
+    case ROLE_QKV: return run_f32<EPI_BIAS>(A, lda, B, ldb, bias, gate, C, ldc, m, n, k, st);
+    case ROLE_UP: return run_f32<EPI_BIAS_GELU>(A, lda, B, ldb, bias, gate, C, ldc, m, n, k, st);
+    case ROLE_OUT:
+    case ROLE_DOWN: return run_f32<EPI_BIAS_GATED_RESIDUAL>(A, lda, B, ldb, bias, gate, C, ldc, m, n, k, st);
+    default: return hipErrorInvalidValue;
   }
 }
 
@@ -560,14 +565,12 @@ hipError_t launch_gemm_qkv(int dtype, const void* A, int64_t lda, const void* B,
     const GemmPlan p = choose_gemm(M, N, K, ws ? ws_floats : 0);
     if (p.splits <= 1) {
       const int m = (int)M, n = (int)N, k = (int)K;
-      switch (p.tile) {
-        case 0: return run_bf16<256, 256, 2, 4, EPI_BIAS_QKPOST>(A, lda, B, ldb, bias, nullptr, C, ldc, m, n, k, 1, nullptr, st, qp);
-        case 1: return run_bf16<256, 128, 4, 2, EPI_BIAS_QKPOST>(A, lda, B, ldb, bias, nullptr, C, ldc, m, n, k, 1, nullptr, st, qp);
-        default: return run_bf16<128, 128, 2, 2, EPI_BIAS_QKPOST>(A, lda, B, ldb, bias, nullptr, C, ldc, m, n, k, 1, nullptr, st, qp);
-      }
+      if (p.tile == 0)
+        return run_bf16<ROLE_QKV, 256, 256, 2, 4, EPI_BIAS_QKPOST>(A, lda, B, ldb, bias, nullptr, C, ldc, m, n, k, 1, nullptr, st, qp);
+      return run_bf16<ROLE_QKV, 128, 128, 2, 2, EPI_BIAS_QKPOST>(A, lda, B, ldb, bias, nullptr, C, ldc, m, n, k, 1, nullptr, st, qp);
     }
   }
-  const hipError_t e = launch_gemm(dtype, EPI_BIAS, A, lda, B, ldb, bias, nullptr, C, ldc, M, N, K,
+  const hipError_t e = launch_gemm(dtype, ROLE_QKV, A, lda, B, ldb, bias, nullptr, C, ldc, M, N, K,
                                    st, ws, ws_floats);
   if (e != hipSuccess || !post) return e;
   return launch_qk_post(dtype, C, M, qp.d, qp.pos_mode, qp.gather, qp.cu, qp.n_seqs, qp.l_full,

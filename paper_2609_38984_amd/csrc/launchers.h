@@ -25,12 +25,16 @@ struct QkPost {
   const float2* tab = nullptr;
 };
 
+// The four projections of a block; the role fixes the epilogue:
+// QKV bias, UP bias + tanh-GELU, OUT and DOWN bias + gated residual.
+enum GemmRole { ROLE_QKV = 0, ROLE_OUT = 1, ROLE_UP = 2, ROLE_DOWN = 3 };
+
 // C[M][N] = epi(A[M][K] . B[N][K]^T + bias[N]); for the gated residual
 // C[m][n] = C[m][n] + gate[n] * (acc + bias[n]) (C read then written).
 // ws / ws_floats: fp32 workspace the bf16 path may use to split K when the
 // output tiles alone cannot fill the CUs (partial sums, then one reduce +
 // epilogue pass); NULL or too small means no split.
-hipError_t launch_gemm(int dtype, int epi, const void* A, int64_t lda, const void* B,
+hipError_t launch_gemm(int dtype, int role, const void* A, int64_t lda, const void* B,
                        int64_t ldb, const void* bias, const float* gate, void* C,
                        int64_t ldc, int64_t M, int64_t N, int64_t K, hipStream_t st,
                        float* ws = nullptr, int64_t ws_floats = 0);

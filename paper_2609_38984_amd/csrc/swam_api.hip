@@ -106,9 +106,11 @@ int derive(const swam_config* c, Derived* dv, std::string* err) {
   dv->esz = c->dtype == SWAM_BF16 ? 2 : 4;
   dv->k_eff = std::min(c->k_layer, c->n_blocks);
   if (c->mass_threshold > 0.0f) {
-    int num = (int)lrintf(c->mass_threshold * 1000.0f), den = 1000;
-    if (num < 1) num = 1;
-    const int gg = std::gcd(num, den);
+    // theta = num / 1000 with num the integer nearest to 1000 theta: the
+    // product of the float32 threshold and 1000 is exact in double and never
+    // halfway between integers; num = 0 (theta < 0.0005) keeps one core token
+    const int num = (int)llround((double)c->mass_threshold * 1000.0), den = 1000;
+    const int gg = std::gcd(num, den);   // gcd(0, 1000) = 1000 gives 0 / 1
     dv->mass_num = num / gg;
     dv->mass_den = den / gg;
     dv->k_max = n_s;
@@ -132,14 +134,14 @@ Layout layout_for(const swam_config* c, const Derived& dv) {
   };
   const int64_t R = dv.rows_full, B = c->batch, F = c->n_frames, Lb = c->n_blocks;
   const int64_t chunks = (dv.l_full + 255) / 256;
-  // one QKV / lambda slot per block: a refresh keeps every layer's projections
-  // resident and scores all layers in one launch after the last block
-  L.qkv = take(Lb * R * 3 * dv.d * dv.esz);
+  // one QKV / lambda slot: a refresh scores each layer right after its
+  // attention, before the next block overwrites the slot
+  L.qkv = take(R * 3 * dv.d * dv.esz);
   L.h = take(R * dv.d * dv.esz);
   L.o = take(R * dv.d * dv.esz);
   L.u = take(R * dv.hidden * dv.esz);
   L.xp = take(R * dv.d * dv.esz);
-  L.lse = take(Lb * R * c->n_heads * 4);
+  L.lse = take(R * c->n_heads * 4);
   L.mod = take(Lb * 6 * dv.d * 4);
   L.alpha = take(16 * 4);
   // positions up to batch * l_full - 1: a cu_seqlens sequence of swam_block may
@@ -253,10 +255,12 @@ bool bad_block(const swam_block_weights* w) {
 
 // one block in place on x [n_rows][d]; mod = this block's [6][d] modulation
 // pos_mode (rope only): 0 = dense layout, 1 = packed rows of the cached
-// selection (original positions), 2 = index inside the cu_seqlens sequence
+// selection (original positions), 2 = index inside the cu_seqlens sequence.
+// score (refresh only): this layer's action-to-future scores, launched right
+// after the attention while the layer's q, k and lambda are fresh in cache
 int run_block(swam_ctx* c, const swam_block_weights* w, const float* mod, void* x,
               int64_t n_rows, const int32_t* cu, int n_seqs, float* lse_out, void* qkv,
-              int pos_mode) {
+              int pos_mode, const ScoreArgs* score = nullptr) {
   const int dt = c->cfg.dtype;
   const int64_t d = c->dv.d, hid = c->dv.hidden;
   void* h = c->ptr<char>(c->lay.h);
@@ -290,7 +294,7 @@ int run_block(swam_ctx* c, const swam_block_weights* w, const float* mod, void* 
                                 st, sk, sk_n), "gemm qkv + qk post");
   } else {
     Timed t(c, SWAM_T_GEMM_QKV);
-    SWAM_HIP(c, launch_gemm(dt, EPI_BIAS, h, d, w->w_qkv, d, w->b_qkv, nullptr, qkv, 3 * d,
+    SWAM_HIP(c, launch_gemm(dt, ROLE_QKV, h, d, w->w_qkv, d, w->b_qkv, nullptr, qkv, 3 * d,
                             n_rows, 3 * d, d, st, sk, sk_n), "gemm qkv");
   }
   {
@@ -298,9 +302,13 @@ int run_block(swam_ctx* c, const swam_block_weights* w, const float* mod, void* 
     SWAM_HIP(c, launch_attention(dt, qkv, o, lse_out, cu, n_seqs, n_rows, c->cfg.n_heads, st),
              "attention");
   }
+  if (score) {
+    Timed t(c, SWAM_T_SCORE);
+    SWAM_HIP(c, launch_score(dt, *score, st), "score");
+  }
   {
     Timed t(c, SWAM_T_GEMM_OUT);
-    SWAM_HIP(c, launch_gemm(dt, EPI_BIAS_GATED_RESIDUAL, o, d, w->w_o, d, w->b_o, g1, x, d,
+    SWAM_HIP(c, launch_gemm(dt, ROLE_OUT, o, d, w->w_o, d, w->b_o, g1, x, d,
                             n_rows, d, d, st, sk, sk_n), "gemm out");
   }
   {
@@ -309,12 +317,12 @@ int run_block(swam_ctx* c, const swam_block_weights* w, const float* mod, void* 
   }
   {
     Timed t(c, SWAM_T_GEMM_UP);
-    SWAM_HIP(c, launch_gemm(dt, EPI_BIAS_GELU, h, d, w->w_1, d, w->b_1, nullptr, u, hid, n_rows,
+    SWAM_HIP(c, launch_gemm(dt, ROLE_UP, h, d, w->w_1, d, w->b_1, nullptr, u, hid, n_rows,
                             hid, d, st, sk, sk_n), "gemm up");
   }
   {
     Timed t(c, SWAM_T_GEMM_DOWN);
-    SWAM_HIP(c, launch_gemm(dt, EPI_BIAS_GATED_RESIDUAL, u, hid, w->w_2, hid, w->b_2, g2, x, d,
+    SWAM_HIP(c, launch_gemm(dt, ROLE_DOWN, u, hid, w->w_2, hid, w->b_2, g2, x, d,
                             n_rows, d, hid, st, sk, sk_n), "gemm down");
   }
   return SWAM_OK;
@@ -775,21 +783,12 @@ int enqueue_step(swam_ctx* c, const swam_model* model, const void* x_full, const
       SWAM_HIP(c, launch_copy(x_full, y_full, c->dv.rows_full * d * c->dv.esz, c->st), "copy");
     }
     const bool score = kind == SWAM_KIND_REFRESH;
-    const int64_t qkv_slot = c->dv.rows_full * 3 * d * c->dv.esz;      // bytes per layer
-    const int64_t lse_slot = c->dv.rows_full * cf.n_heads;             // floats per layer
-    for (int l = 0; l < cf.n_blocks; ++l) {
-      rc = run_block(c, &model->blocks[l], mod + (int64_t)l * 6 * d, y_full, c->dv.rows_full,
-                     c->ptr<int32_t>(c->lay.cu_dense), cf.batch,
-                     score ? c->ptr<float>(c->lay.lse) + l * lse_slot : nullptr,
-                     score ? (void*)((char*)qkv + l * qkv_slot) : qkv, 0);
-      if (rc != SWAM_OK) return rc;
-    }
+    // scores of layer l from its q, k (in the QKV slot) and lambda, written
+    // into S_all[b][l]; the slot is reused by the next block
+    ScoreArgs a{};
     if (score) {
-      // every layer's action-to-future scores from its stored q, k and lambda
-      Timed t(c, SWAM_T_SCORE);
       const int64_t ld = 3 * d, es = c->dv.esz;
       const int64_t act0 = cf.n_ctx + (int64_t)cf.n_frames * c->dv.n_s;
-      ScoreArgs a{};
       a.q = (const char*)qkv + act0 * ld * es;
       a.q_seq = c->dv.l_full * ld;
       a.q_row = ld;
@@ -798,7 +797,6 @@ int enqueue_step(swam_ctx* c, const swam_model* model, const void* x_full, const
       a.k_row = ld;
       a.lse = c->ptr<float>(c->lay.lse) + act0 * cf.n_heads;
       a.lse_seq = c->dv.l_full * cf.n_heads;
-      a.s_out = c->ptr<float>(c->lay.s_all);
       a.s_seq = (int64_t)cf.n_blocks * cf.n_frames * c->dv.n_s;
       a.alpha = c->ptr<float>(c->lay.alpha);
       a.B = (int)c->dv.n_scored;
@@ -806,12 +804,15 @@ int enqueue_step(swam_ctx* c, const swam_model* model, const void* x_full, const
       a.n_s = (int)c->dv.n_s;
       a.H = cf.n_act;
       a.n_heads = cf.n_heads;
-      a.n_layers = cf.n_blocks;
-      a.q_lay = c->dv.rows_full * ld;
-      a.k_lay = c->dv.rows_full * ld;
-      a.lse_lay = lse_slot;
-      a.s_lay = (int64_t)cf.n_frames * c->dv.n_s;
-      SWAM_HIP(c, launch_score(cf.dtype, a, c->st), "score");
+      a.n_layers = 1;
+    }
+    for (int l = 0; l < cf.n_blocks; ++l) {
+      a.s_out = c->ptr<float>(c->lay.s_all) + (int64_t)l * cf.n_frames * c->dv.n_s;
+      rc = run_block(c, &model->blocks[l], mod + (int64_t)l * 6 * d, y_full, c->dv.rows_full,
+                     c->ptr<int32_t>(c->lay.cu_dense), cf.batch,
+                     score ? c->ptr<float>(c->lay.lse) : nullptr, qkv, 0,
+                     score ? &a : nullptr);
+      if (rc != SWAM_OK) return rc;
     }
     if (score) {
       c->scores_valid = true;
@@ -951,6 +952,16 @@ int swam_sample_update(swam_ctx* c, int32_t d_latent, const float* v, float* v_c
   if (!c) return set_err(nullptr, SWAM_E_INVALID, "ctx is NULL");
   if (d_latent < 1 || d_latent > 64) return set_err(c, SWAM_E_SHAPE, "d_latent must be in [1, 64]");
   return sample_update(c, d_latent, v, v_cache, z, dsigma, kind);
+}
+
+int swam_flow_sigmas(int32_t n_steps, double shift, double* sigmas) {
+  if (n_steps < 1 || !sigmas || !std::isfinite(shift) || !(shift > 0.0))
+    return set_err(nullptr, SWAM_E_INVALID, "need n_steps >= 1, a finite shift > 0 and sigmas");
+  for (int32_t i = 0; i <= n_steps; ++i) {
+    const double s = 1.0 - (double)i / n_steps;
+    sigmas[i] = shift * s / (1.0 + (shift - 1.0) * s);
+  }
+  return SWAM_OK;
 }
 
 int swam_sample_step(swam_ctx* c, const swam_model* model, const swam_latent_io* io, float* z,

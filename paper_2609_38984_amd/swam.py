@@ -29,20 +29,20 @@ EXPORTS = ["swam_create", "swam_destroy", "swam_set_stream", "swam_plan", "swam_
            "swam_set_selection", "swam_packed_rows", "swam_export", "swam_pack", "swam_unpack",
            "swam_block", "swam_step", "swam_step_graph", "swam_graph_clear", "swam_timer_enable",
            "swam_timer_reset", "swam_timer_read", "swam_embed", "swam_velocity",
-           "swam_sample_update", "swam_sample_step", "swam_overlap", "swam_select_random"]
+           "swam_sample_update", "swam_sample_step", "swam_overlap", "swam_select_random",
+           "swam_flow_sigmas"]
 
 # the flow-schedule shift of the paper's backbones (App. B.2)
 SCHEDULE_SHIFT = 5.0
 
 
 def flow_sigmas(n_steps: int, shift: float = SCHEDULE_SHIFT) -> list[float]:
-    """Host helper: sigma_i = shift s / (1 + (shift - 1) s) with s = 1 - i / N,
-    i = 0..N, the shifted flow schedule from 1 (noise) to 0."""
-    out = []
-    for i in range(n_steps + 1):
-        s = 1.0 - i / n_steps
-        out.append(shift * s / (1.0 + (shift - 1.0) * s))
-    return out
+    """The n_steps + 1 noise levels of the shifted flow schedule, computed by
+    swam_flow_sigmas in the library (a host call, no GPU needed)."""
+    lib = load_library()
+    out = (C.c_double * (n_steps + 1))()
+    _check(lib, None, lib.swam_flow_sigmas(int(n_steps), float(shift), out))
+    return list(out)
 
 
 class SwamError(RuntimeError):
@@ -130,6 +130,7 @@ def load_library(path: str = LIB_PATH):
         "swam_timer_enable": [P, C.c_uint32, I32], "swam_timer_reset": [P],
         "swam_timer_read": [P, I32, C.POINTER(I64), C.POINTER(C.c_double)],
         "swam_overlap": [P, P, P, I64, I64, P],
+        "swam_flow_sigmas": [I32, C.c_double, C.POINTER(C.c_double)],
         "swam_embed": [P, C.POINTER(LatentIOStruct), P, P],
         "swam_velocity": [P, C.POINTER(LatentIOStruct), P, I32, P],
         "swam_sample_update": [P, I32, P, P, P, F, I32],

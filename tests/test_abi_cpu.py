@@ -28,7 +28,7 @@ def _declared():
 def test_every_declared_symbol_is_exported(lib):
     from paper_2609_38984_amd import swam
     names = _declared()
-    assert len(names) == 27
+    assert len(names) == 28
     assert sorted(swam.EXPORTS) == names
     for n in names:
         assert hasattr(lib, n), n
@@ -108,8 +108,29 @@ def test_sampler_entry_points_reject_bad_arguments_without_a_gpu(lib):
                                 0.1, 0, None) == -1
 
 
-def test_flow_sigmas_host_helper():
+def test_flow_sigmas_host_call(lib):
     from paper_2609_38984_amd import swam
     s = swam.flow_sigmas(4)
     assert s[0] == 1.0 and s[-1] == 0.0
     assert abs(s[2] - 5.0 / 6.0) < 1e-15 and all(a > b for a, b in zip(s, s[1:]))
+    assert swam.flow_sigmas(3, 1.0) == [1.0 - i / 3.0 for i in range(4)]   # shift 1: linear
+    out = (C.c_double * 5)()
+    assert lib.swam_flow_sigmas(0, 5.0, out) == -1
+    assert lib.swam_flow_sigmas(4, 0.0, out) == -1
+    assert lib.swam_flow_sigmas(4, float("inf"), out) == -1
+    assert lib.swam_flow_sigmas(4, 5.0, None) == -1
+
+
+def test_workspace_does_not_grow_with_block_depth(lib):
+    """A refresh scores each layer right after its attention, so one QKV and one
+    normaliser slot serve every block: the workspace grows with the block count
+    only by the per-block modulation (6 d floats), the per-layer scores
+    (F N_s floats per scored sequence) and two per-layer statistics."""
+    from paper_2609_38984_amd import swam
+    cfg = W.preset(3)
+    w28 = swam.plan(cfg).workspace_bytes
+    w1 = swam.plan(cfg.replace(n_blocks=1)).workspace_bytes
+    per_block = 6 * cfg.d_model * 4 + cfg.n_scored * (cfg.n_frames * cfg.n_s * 4 + 4 + 8 + 2 * 8 * cfg.n_frames)
+    assert w28 - w1 <= 27 * per_block + 16 * 256
+    # one QKV slot of the 10,160-token, d = 1536 workload is 93.6 MB; 28 of them were 2.6 GB
+    assert w28 < 512 << 20

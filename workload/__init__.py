@@ -219,11 +219,17 @@ def rng_for(cfg: SwamConfig, *stream: int) -> np.random.Generator:
 
 
 def _to_bf16_grid(x: np.ndarray) -> np.ndarray:
-    """Round float32 values to the nearest bf16 value (ties to even)."""
-    x = np.ascontiguousarray(x, dtype=np.float32)
+    """Round float32 values to the nearest bf16 value (ties to even), on a copy.
+
+    In uint32 arithmetic: for every finite float32 the bit pattern plus
+    0x7FFF + 1 stays below 2^32, so nothing wraps."""
+    x = np.array(x, dtype=np.float32, order="C")
     u = x.view(np.uint32)
-    r = ((u.astype(np.uint64) + 0x7FFF + ((u >> 16) & 1)) & 0xFFFF0000).astype(np.uint32)
-    return r.view(np.float32)
+    lsb = (u >> 16) & np.uint32(1)
+    u += np.uint32(0x7FFF)
+    u += lsb
+    u &= np.uint32(0xFFFF0000)
+    return x
 
 
 def _storage(cfg: SwamConfig, x: np.ndarray) -> np.ndarray:
