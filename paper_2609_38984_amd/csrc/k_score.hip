@@ -5,8 +5,9 @@
 // against a stream of keys), so it is bound by the single read of the future
 // keys; MFMA only keeps the dot products off the VALU.
 //
-// One launch may score several layers (the refresh step scores all of them
-// after its last block, from per-layer q/k/lambda kept resident in HBM).
+// One launch may score several layers (layer strides in ScoreArgs); the
+// refresh step launches one layer at a time, right after that layer's
+// attention, while its q, k and lambda are fresh.
 //
 // bf16: workgroup = 4 waves on 16 keys of one frame.  Each wave takes every
 // 4th head: two 16x16x32 MFMAs per head with the keys as the A operand

@@ -535,42 +535,88 @@ hipError_t launch_packmap(const int32_t* keep, int32_t* pack_pos, int32_t* gathe
 // ---------------------------------------------------------------------------
 // pack / unpack / copy: 16-byte chunks, one row per 64 x 16 B slice
 // ---------------------------------------------------------------------------
-// Row copies of pack / unpack: one wave per row (the row's source or target
-// index is wave-uniform), lanes striding over the row's 16-byte chunks, four
-// rows per 256-thread workgroup.
+// Row copies of pack / unpack: each wave moves ROWS rows (their source or
+// target indices wave-uniform and read up front), every lane loading its
+// 16-byte chunks of all of them before storing any, so one wave keeps
+// ROWS x ceil(chunks / 64) x 16 B per lane in flight; four waves per
+// 256-thread workgroup.  The copies are a few to a few tens of MB: what
+// bounds them is how much is in flight, not the bandwidth.
+constexpr int COPY_ROWS = 2;     // rows per wave
+constexpr int COPY_CH = 4;       // 16-byte chunks per lane and row in flight per pass (4 KB rows)
+
+// The row map gives the source and destination row pointers of row r.  Loads
+// are unconditional (a row past the end repeats the last row, a chunk past
+// the row end repeats the last chunk: always in bounds) so they all issue
+// before the first store; only the stores are predicated.
+template <typename RowMap>
+__device__ __forceinline__ void copy_rows(const uint4* __restrict__ src_a,
+                                          const uint4* __restrict__ src_b, uint4* __restrict__ dst,
+                                          int64_t rows, int cpr, RowMap map) {
+  const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
+  const int64_t r0 = ((int64_t)blockIdx.x * 4 + wave) * COPY_ROWS;
+  if (r0 >= rows) return;
+  const int lane = threadIdx.x & 63;
+  const uint4* sp[COPY_ROWS];
+  uint4* dp[COPY_ROWS];
+#pragma unroll
+  for (int i = 0; i < COPY_ROWS; ++i) map(min(r0 + i, rows - 1), src_a, src_b, dst, cpr, sp[i], dp[i]);
+  for (int base = 0; base < cpr; base += 64 * COPY_CH) {
+    const int c0 = base + lane;
+    uint4 v[COPY_ROWS][COPY_CH];
+#pragma unroll
+    for (int i = 0; i < COPY_ROWS; ++i)
+#pragma unroll
+      for (int k = 0; k < COPY_CH; ++k) v[i][k] = sp[i][min(c0 + 64 * k, cpr - 1)];
+    // keep every load ahead of the predicated stores (the compiler would
+    // otherwise sink each load into its store's branch, one round trip each)
+#pragma unroll
+    for (int i = 0; i < COPY_ROWS; ++i)
+#pragma unroll
+      for (int k = 0; k < COPY_CH; ++k) {
+        typedef int i32x4 __attribute__((ext_vector_type(4)));
+        asm volatile("" ::"v"(__builtin_bit_cast(i32x4, v[i][k])));
+      }
+#pragma unroll
+    for (int i = 0; i < COPY_ROWS; ++i)
+#pragma unroll
+      for (int k = 0; k < COPY_CH; ++k)
+        if (r0 + i < rows && c0 + 64 * k < cpr) dp[i][c0 + 64 * k] = v[i][k];
+  }
+}
+
 __global__ void __launch_bounds__(256)
 pack_rows(const uint4* __restrict__ src, uint4* __restrict__ dst,
           const int32_t* __restrict__ gather, int64_t rows, int cpr) {
-  const int64_t r = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (r >= rows) return;
-  const int lane = threadIdx.x & 63;
-  const uint4* s_ = src + (int64_t)gather[r] * cpr;
-  uint4* d_ = dst + r * cpr;
-  for (int c = lane; c < cpr; c += 64) d_[c] = s_[c];
+  copy_rows(src, nullptr, dst, rows, cpr,
+            [gather](int64_t r, const uint4* a, const uint4*, uint4* d, int cpr_,
+                     const uint4*& s_, uint4*& d_) {
+              s_ = a + (int64_t)gather[r] * cpr_;
+              d_ = d + r * cpr_;
+            });
 }
 
 __global__ void __launch_bounds__(256)
 unpack_scatter(const uint4* __restrict__ src, uint4* __restrict__ dst,
                const int32_t* __restrict__ gather, int64_t rows, int cpr) {
-  const int64_t r = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (r >= rows) return;
-  const int lane = threadIdx.x & 63;
-  const uint4* s_ = src + r * cpr;
-  uint4* d_ = dst + (int64_t)gather[r] * cpr;
-  for (int c = lane; c < cpr; c += 64) d_[c] = s_[c];
+  copy_rows(src, nullptr, dst, rows, cpr,
+            [gather](int64_t r, const uint4* a, const uint4*, uint4* d, int cpr_,
+                     const uint4*& s_, uint4*& d_) {
+              s_ = a + r * cpr_;
+              d_ = d + (int64_t)gather[r] * cpr_;
+            });
 }
 
 // y row r = packed row pack_pos[r] if retained, else x row r
 __global__ void __launch_bounds__(256)
 unpack_merge(const uint4* __restrict__ yp, const uint4* __restrict__ x, uint4* __restrict__ y,
              const int32_t* __restrict__ pack_pos, int64_t rows, int cpr) {
-  const int64_t r = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (r >= rows) return;
-  const int lane = threadIdx.x & 63;
-  const int32_t p = pack_pos[r];
-  const uint4* s_ = p >= 0 ? yp + (int64_t)p * cpr : x + r * cpr;
-  uint4* d_ = y + r * cpr;
-  for (int c = lane; c < cpr; c += 64) d_[c] = s_[c];
+  copy_rows(yp, x, y, rows, cpr,
+            [pack_pos](int64_t r, const uint4* a, const uint4* b, uint4* d, int cpr_,
+                       const uint4*& s_, uint4*& d_) {
+              const int32_t p = pack_pos[r];
+              s_ = p >= 0 ? a + (int64_t)p * cpr_ : b + r * cpr_;
+              d_ = d + r * cpr_;
+            });
 }
 
 __global__ void __launch_bounds__(256)
@@ -589,7 +635,7 @@ hipError_t launch_pack(const void* x_full, void* x_packed, const int32_t* gather
                        int64_t row_bytes, hipStream_t st) {
   if (rows <= 0) return hipSuccess;
   const int cpr = (int)(row_bytes / 16);
-  hipLaunchKernelGGL(pack_rows, dim3((unsigned)((rows + 3) / 4)), dim3(256), 0, st,
+  hipLaunchKernelGGL(pack_rows, dim3((unsigned)((rows + 4 * COPY_ROWS - 1) / (4 * COPY_ROWS))), dim3(256), 0, st,
                      (const uint4*)x_full, (uint4*)x_packed, gather, rows, cpr);
   return hipGetLastError();
 }
@@ -598,7 +644,7 @@ hipError_t launch_unpack_scatter(const void* y_packed, void* y_full, const int32
                                  int64_t rows, int64_t row_bytes, hipStream_t st) {
   if (rows <= 0) return hipSuccess;
   const int cpr = (int)(row_bytes / 16);
-  hipLaunchKernelGGL(unpack_scatter, dim3((unsigned)((rows + 3) / 4)), dim3(256), 0, st,
+  hipLaunchKernelGGL(unpack_scatter, dim3((unsigned)((rows + 4 * COPY_ROWS - 1) / (4 * COPY_ROWS))), dim3(256), 0, st,
                      (const uint4*)y_packed, (uint4*)y_full, gather, rows, cpr);
   return hipGetLastError();
 }
@@ -608,7 +654,7 @@ hipError_t launch_unpack_merge(const void* y_packed, const void* x_full, void* y
                                hipStream_t st) {
   if (rows <= 0) return hipSuccess;
   const int cpr = (int)(row_bytes / 16);
-  hipLaunchKernelGGL(unpack_merge, dim3((unsigned)((rows + 3) / 4)), dim3(256), 0, st,
+  hipLaunchKernelGGL(unpack_merge, dim3((unsigned)((rows + 4 * COPY_ROWS - 1) / (4 * COPY_ROWS))), dim3(256), 0, st,
                      (const uint4*)y_packed, (const uint4*)x_full, (uint4*)y_full, pack_pos,
                      rows, cpr);
   return hipGetLastError();

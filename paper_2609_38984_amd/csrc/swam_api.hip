@@ -43,6 +43,18 @@ int fail(std::string* err, int code, const std::string& msg) {
   return code;
 }
 
+// theta = num / den reduced from num / 1000, num the integer nearest to
+// 1000 theta: the product of the float32 threshold and 1000 is exact in
+// double and never halfway between integers; num = 0 (theta < 0.0005) keeps
+// one core token per frame (gcd(0, 1000) = 1000 gives 0 / 1, den > 0 still
+// marks mass-threshold mode)
+void mass_fraction(float theta, int* num, int* den) {
+  const int n = (int)llround((double)theta * 1000.0);
+  const int gg = std::gcd(n, 1000);
+  *num = n / gg;
+  *den = 1000 / gg;
+}
+
 int derive(const swam_config* c, Derived* dv, std::string* err) {
   if (!c) return fail(err, SWAM_E_INVALID, "config is NULL");
   if (c->dtype != SWAM_F32 && c->dtype != SWAM_BF16)
@@ -106,13 +118,7 @@ int derive(const swam_config* c, Derived* dv, std::string* err) {
   dv->esz = c->dtype == SWAM_BF16 ? 2 : 4;
   dv->k_eff = std::min(c->k_layer, c->n_blocks);
   if (c->mass_threshold > 0.0f) {
-    // theta = num / 1000 with num the integer nearest to 1000 theta: the
-    // product of the float32 threshold and 1000 is exact in double and never
-    // halfway between integers; num = 0 (theta < 0.0005) keeps one core token
-    const int num = (int)llround((double)c->mass_threshold * 1000.0), den = 1000;
-    const int gg = std::gcd(num, den);   // gcd(0, 1000) = 1000 gives 0 / 1
-    dv->mass_num = num / gg;
-    dv->mass_den = den / gg;
+    mass_fraction(c->mass_threshold, &dv->mass_num, &dv->mass_den);
     dv->k_max = n_s;
     dv->t_pack_fixed = -1;
   } else {
@@ -183,6 +189,11 @@ struct swam_ctx {
   char* arena = nullptr;
   int32_t* host_cu = nullptr;   // pinned
   hipEvent_t order_ev = nullptr; // orders a newly bound stream after the previous one
+  // a refresh scores layer l on `side` while the context stream runs the rest
+  // of block l; the next block's QKV projection waits for it (ev_score)
+  hipStream_t side = nullptr;
+  hipEvent_t ev_attn = nullptr, ev_score = nullptr;
+  bool score_pending = false;
   bool sel_valid = false, scores_valid = false;
   int64_t packed_rows = 0;
   std::string err;
@@ -225,21 +236,32 @@ int hip_check(swam_ctx* c, hipError_t e, const char* what) {
     if (rc_ != SWAM_OK) return rc_;                      \
   } while (0)
 
-// brackets one launch (or phase) of a timed class with events on the stream
+// brackets one launch (or phase) of a timed class with events on a stream
+// (the context stream unless given)
 struct Timed {
   swam_ctx* c;
+  hipStream_t s;
   int slot = -1;
-  Timed(swam_ctx* ctx, int cls) : c(ctx) {
+  Timed(swam_ctx* ctx, int cls) : Timed(ctx, cls, ctx->st) {}
+  Timed(swam_ctx* ctx, int cls, hipStream_t on) : c(ctx), s(on) {
     if (!c->capturing && ((c->tmask >> cls) & 1u) && c->tused < c->tcap) {
       slot = c->tused++;
       c->ev_cls[slot] = cls;
-      hipEventRecord(c->ev[2 * slot], c->st);
+      (void)hipEventRecord(c->ev[2 * slot], s);
     }
   }
   ~Timed() {
-    if (slot >= 0) hipEventRecord(c->ev[2 * slot + 1], c->st);
+    if (slot >= 0) (void)hipEventRecord(c->ev[2 * slot + 1], s);
   }
 };
+
+// the context stream waits for the scoring launched on the side stream
+int join_score(swam_ctx* c) {
+  if (!c->score_pending) return SWAM_OK;
+  c->score_pending = false;
+  SWAM_HIP(c, hipStreamWaitEvent(c->st, c->ev_score, 0), "join scoring");
+  return SWAM_OK;
+}
 
 bool aligned16(const void* p) { return ((uintptr_t)p & 15) == 0; }
 
@@ -276,6 +298,9 @@ int run_block(swam_ctx* c, const swam_block_weights* w, const float* mod, void* 
     Timed t(c, SWAM_T_LNMOD);
     SWAM_HIP(c, launch_ln_mod(dt, x, h, sh1, sc1, n_rows, (int)d, st), "ln_mod");
   }
+  // the previous layer's scoring (side stream) still reads the QKV slot and
+  // the normalisers: this block's projection and attention overwrite them
+  if (int rc = join_score(c)) return rc;
   if (c->cfg.rope || c->cfg.qk_norm) {
     // QKV projection with the QK-norm / rotary embedding of q and k (fused
     // into the projection's store where the shape allows)
@@ -303,8 +328,16 @@ int run_block(swam_ctx* c, const swam_block_weights* w, const float* mod, void* 
              "attention");
   }
   if (score) {
-    Timed t(c, SWAM_T_SCORE);
-    SWAM_HIP(c, launch_score(dt, *score, st), "score");
+    // fork: the scores of this layer run on the side stream, concurrently
+    // with the rest of the block (memory-bound next to MFMA-bound GEMMs)
+    SWAM_HIP(c, hipEventRecord(c->ev_attn, st), "fork scoring");
+    SWAM_HIP(c, hipStreamWaitEvent(c->side, c->ev_attn, 0), "fork scoring");
+    {
+      Timed t(c, SWAM_T_SCORE, c->side);
+      SWAM_HIP(c, launch_score(dt, *score, c->side), "score");
+    }
+    SWAM_HIP(c, hipEventRecord(c->ev_score, c->side), "scoring done");
+    c->score_pending = true;
   }
   {
     Timed t(c, SWAM_T_GEMM_OUT);
@@ -503,6 +536,10 @@ int swam_create(const swam_config* cfg, void* stream, swam_ctx** out) {
   }
   e = hipHostMalloc((void**)&c->host_cu, (cfg->batch + 1) * sizeof(int32_t), 0);
   if (e == hipSuccess) e = hipEventCreateWithFlags(&c->order_ev, hipEventDisableTiming);
+  if (e == hipSuccess) e = hipEventCreateWithFlags(&c->ev_attn, hipEventDisableTiming);
+  if (e == hipSuccess) e = hipEventCreateWithFlags(&c->ev_score, hipEventDisableTiming);
+  // default priority (no priority argument): the side stream of the scoring
+  if (e == hipSuccess) e = hipStreamCreateWithFlags(&c->side, hipStreamNonBlocking);
   if (e == hipSuccess) {
     float alpha[16];
     fill_alpha((int)dv.g, alpha);
@@ -529,12 +566,16 @@ int swam_create(const swam_config* cfg, void* stream, swam_ctx** out) {
 
 int swam_destroy(swam_ctx* c) {
   if (!c) return SWAM_OK;
-  if (c->st || c->arena) hipStreamSynchronize(c->st);
+  if (c->st || c->arena) (void)hipStreamSynchronize(c->st);
+  if (c->side) (void)hipStreamSynchronize(c->side);
   for (auto& g : c->graphs) hipGraphExecDestroy(g.exec);
   for (hipEvent_t ev : c->ev) hipEventDestroy(ev);
   if (c->arena) hipFree(c->arena);
   if (c->host_cu) hipHostFree(c->host_cu);
   if (c->order_ev) hipEventDestroy(c->order_ev);
+  if (c->ev_attn) hipEventDestroy(c->ev_attn);
+  if (c->ev_score) hipEventDestroy(c->ev_score);
+  if (c->side) hipStreamDestroy(c->side);
   delete c;
   return SWAM_OK;
 }
@@ -814,6 +855,7 @@ int enqueue_step(swam_ctx* c, const swam_model* model, const void* x_full, const
                      score ? &a : nullptr);
       if (rc != SWAM_OK) return rc;
     }
+    if ((rc = join_score(c)) != SWAM_OK) return rc;
     if (score) {
       c->scores_valid = true;
       if ((rc = run_reduce(c, c->ptr<float>(c->lay.s_all))) != SWAM_OK) return rc;
