@@ -20,9 +20,11 @@ from __future__ import annotations
 import argparse
 import json
 import os
+import re
 import statistics
 import sys
 import time
+from concurrent.futures import ThreadPoolExecutor
 
 import numpy as np
 
@@ -78,8 +80,13 @@ def kernel_work(cfg, cls, rows_per_seq):
         # one read of the future keys, the action queries and normalisers; S written
         return float(cfg.batch * (cfg.n_fut * d * esz + cfg.n_act * d * esz
                                   + cfg.n_act * cfg.n_heads * 4 + cfg.n_fut * 4))
-    if cls in ("PACK", "UNPACK"):
+    if cls == "PACK":
+        # the retained rows read once and written once
         return 2.0 * m * d * esz
+    if cls == "UNPACK":
+        # out of place (the step's y_full is not x_full): every row of y_full
+        # written once from its source, the packed row or the input row
+        return 2.0 * cfg.batch * cfg.l_full * d * esz
     if cls == "QK_POST":
         # q and k of every row read and written once (the rotation table is L2-resident)
         return 4.0 * m * d * esz
@@ -96,17 +103,75 @@ def step_flops(cfg, rows):
     return 24.0 * d * d * rows + 4.0 * d * rows * rows
 
 
-def cpu_baseline(cfg, kinds, blocks_np, inp):
-    """The oracle timed on a bounded sample of the workload: one packed block,
-    one layer's scoring and one score-reduce + selection are measured; a dense
-    block is extrapolated from the packed one by the flop model; the total is
-    scaled to the timed schedule."""
-    import oracle as O
+def host_description():
+    """CPU model of the host and the BLAS numpy links (threadpoolctl)."""
+    model = None
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    blas = []
     try:
         from threadpoolctl import threadpool_info
+        for i in threadpool_info():
+            blas.append(f"{i.get('internal_api')} {i.get('version')} "
+                        f"({i.get('threading_layer', '?')}, {i.get('num_threads')} threads)")
+    except Exception:
+        pass
+    return model, blas
+
+
+def cpu_baseline(cfg, kinds, blocks_np, inp):
+    """The oracle (plain float64 numpy, never tuned) timed on this host:
+
+    * the 1-block fp32 workload's whole schedule, with every BLAS thread and
+      with one;
+    * the 8-block d = 1024 workload: one refresh step and one sparse step
+      measured whole, its 10-step schedule composed from them;
+    * the benched workload on a bounded sample: one packed block, one layer's
+      scoring, one reduce + select and (on a fast host) one dense block, scaled
+      to the timed schedule (a whole step is hours of numpy).
+    `value` is the benched workload's rate; the others are context."""
+    import oracle as O
+    import workload as W
+    try:
+        from threadpoolctl import threadpool_info, threadpool_limits
         cores = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
     except Exception:
+        threadpool_limits = None
         cores = len(os.sched_getaffinity(0))
+    cpu_model, blas = host_description()
+
+    # workload 1 in full
+    c1 = W.preset(1)
+    b1 = [W.block_weights(c1, l) for l in range(c1.n_blocks)]
+    i1 = W.make_inputs(c1, b1[0]["w_qkv"])
+    t0 = time.perf_counter()
+    O.run_schedule(c1, b1, i1.x, i1.temb)
+    t1_n = time.perf_counter() - t0
+    t1_1 = None
+    if threadpool_limits is not None:
+        with threadpool_limits(1):
+            t0 = time.perf_counter()
+            O.run_schedule(c1, b1, i1.x, i1.temb)
+            t1_1 = time.perf_counter() - t0
+    # workload 2: one refresh and one sparse step, whole
+    c2 = W.preset(2)
+    b2 = [W.block_weights(c2, l) for l in range(c2.n_blocks)]
+    i2 = W.make_inputs(c2, b2[0]["w_qkv"])
+    t0 = time.perf_counter()
+    r2 = O.refresh_step(i2.x(0), b2, i2.temb(0), c2)
+    t2_f = time.perf_counter() - t0
+    t0 = time.perf_counter()
+    O.sparse_step(i2.x(1), b2, i2.temb(1), c2, r2.packmap)
+    t2_s = time.perf_counter() - t0
+    n2_f = sum(1 for t in range(c2.n_steps) if t % c2.reuse_R == 0)
+    t2 = n2_f * t2_f + (c2.n_steps - n2_f) * t2_s
+
+    # the benched workload, sampled
     x = inp.x(0)
     temb = inp.temb(0)
     w = blocks_np[0]
@@ -147,56 +212,147 @@ def cpu_baseline(cfg, kinds, blocks_np, inp):
                        f"{how}; scaled to {cfg.n_blocks} blocks x {len(kinds)} steps "
                        f"({n_ref} refresh, {n_sp} sparse)"),
             "sample_seconds": round(t_sparse_block + t_score + t_select
-                                    + (t_dense_block if how.startswith("one") else 0.0), 2)}
+                                    + (t_dense_block if how.startswith("one") else 0.0), 2),
+            "cpu_model": cpu_model, "blas": blas,
+            "workload1_full_schedule": {
+                "workload": c1.name, "steps": c1.n_steps, "seconds": round(t1_n, 4),
+                "tokens_per_s": round(c1.n_steps * c1.l_full / t1_n, 1),
+                "seconds_single_thread": round(t1_1, 4) if t1_1 is not None else None,
+                "tokens_per_s_single_thread": (round(c1.n_steps * c1.l_full / t1_1, 1)
+                                               if t1_1 else None)},
+            "workload2_schedule": {
+                "workload": c2.name, "steps": c2.n_steps, "refresh_step_s": round(t2_f, 3),
+                "sparse_step_s": round(t2_s, 3), "schedule_s": round(t2, 2),
+                "tokens_per_s": round(c2.n_steps * c2.l_full / t2, 1),
+                "how": f"{n2_f} refresh + {c2.n_steps - n2_f} sparse steps, each kind measured whole once"}}
 
 
-KERNEL_OF_CLASS = {"ATTN": ("attn_fwd", None), "GEMM_QKV": ("gemm", ", 0>"),
-                   "GEMM_UP": ("gemm", ", 1>"), "GEMM_OUT": ("gemm", ", 2>"),
-                   "GEMM_DOWN": ("gemm", ", 2>"), "SCORE": ("score_", None),
-                   "PACK": ("pack_rows", None), "UNPACK": ("unpack_", None)}
+GEMM_CLASSES = ("GEMM_QKV", "GEMM_OUT", "GEMM_UP", "GEMM_DOWN")   # index = the ROLE template argument
+MFMA_CLASSES = ("ATTN",) + GEMM_CLASSES
+
+
+def kernel_class(name):
+    """Timer class of a kernel from its name in a trace: the bf16 GEMM and
+    split-K epilogue instantiations carry their projection as the first
+    template argument."""
+    m = re.search(r"(?:gemm_bf16_nt|splitk_epilogue)<(\d+)", name)
+    if m:
+        return GEMM_CLASSES[int(m.group(1))]
+    for sub, cls in (("attn_fwd", "ATTN"), ("score_bf16", "SCORE"), ("score_f32", "SCORE"),
+                     ("pack_rows", "PACK"), ("unpack_", "UNPACK")):
+        if sub in name:
+            return cls
+    return None
+
+
+def class_units(rows, cls):
+    """Launch units of one class in stream order from (id, name, duration) rows:
+    [duration, [ids]], a split-K partial launch and its epilogue being one unit
+    (one projection)."""
+    units = []
+    for rid, name, dur in rows:
+        if kernel_class(name) != cls:
+            continue
+        if "splitk_epilogue" in name and units:
+            units[-1][0] += dur
+            units[-1][1].append(rid)
+        else:
+            units.append([dur, [rid]])
+    return units
+
+
+def warmup_kinds(res):
+    """Step kinds of the untimed warm-up steps (tau = 0 .. warmup - 1)."""
+    R = res["config"]["reuse_R"]
+    return [1 if t % R == 0 else 2 for t in range(res["warmup"])]
+
+
+def timed_window(res, cls, units):
+    """The units of `cls` issued by exactly the K timed steps, with the step
+    kind of each: ATTN and GEMM classes run once per block of every step,
+    SCORE once per block of a refresh, PACK / UNPACK once per sparse step."""
+    nb = res["config"]["n_blocks"]
+
+    def per_step(kind):
+        if cls == "SCORE":
+            return nb if kind == 1 else 0
+        if cls in ("PACK", "UNPACK"):
+            return 1 if kind == 2 else 0
+        return nb
+
+    skip = sum(per_step(k) for k in warmup_kinds(res))
+    out, i = [], skip
+    for k in res["config"]["schedule_kinds"]:
+        for _ in range(per_step(k)):
+            if i < len(units):
+                out.append((k, units[i]))
+            i += 1
+    return out
 
 
 def summarize_rocprof(db_path, bench_json):
-    """Per-kernel table of a rocprofv3 kernel trace of this benchmark, plus the
-    average duration of the dominant class over exactly the timed steps."""
+    """Per-kernel table of a rocprofv3 kernel trace of this benchmark, the
+    per-class rooflines over exactly the timed steps (dense-layout launches
+    of refresh steps and packed launches of sparse steps apart), and the
+    dominant class's average against the bench's live HIP-event average."""
     import sqlite3
     res = json.load(open(bench_json))
+    cfg = workload_from_json(res["config"])
     con = sqlite3.connect(db_path)
-    rows = con.execute("select name, start, end from kernels order by start").fetchall()
+    rows = con.execute("select dispatch_id, name, start, end from kernels order by start").fetchall()
     agg = {}
-    for name, a, b in rows:
+    for _, name, a, b in rows:
         short = name.split("(")[0].replace("void ", "")
         n, t = agg.get(short, (0, 0))
         agg[short] = (n + 1, t + (b - a))
     lines = [f"{'calls':>7} {'avg_us':>10} {'total_ms':>10}  kernel"]
     for k, (n, t) in sorted(agg.items(), key=lambda kv: -kv[1][1]):
         lines.append(f"{n:7d} {t / n / 1e3:10.2f} {t / 1e6:10.2f}  {k}")
+    trows = [(rid, name, b - a) for rid, name, a, b in rows]
+    full = [cfg.l_full] * cfg.batch
+    packed = res["config"]["packed_per_seq"]
+    lines += ["", "timed steps, per class and step kind (algorithmic work per launch unit / "
+              "average unit duration; a split-K projection is its partial GEMM + epilogue):",
+              f"{'class':10s} {'kind':8s} {'units':>6s} {'avg_us':>9s} {'achieved':>10s} {'unit':8s} {'%_of_peak':>9s}"]
+    avgs = {}
+    for cls in MFMA_CLASSES + ("SCORE", "PACK", "UNPACK"):
+        win = timed_window(res, cls, class_units(trows, cls))
+        for kind, name in ((1, "refresh"), (2, "sparse")):
+            sel = [u for k, u in win if k == kind]
+            if not sel:
+                continue
+            us = sum(u[0] for u in sel) / len(sel) / 1e3
+            work = kernel_work(cfg, cls, full if kind == 1 else packed)
+            if BOUND[cls] == "mfma":
+                ach, unit, peak = work / (us * 1e-6) / 1e12, "TFLOP/s", PEAK_BF16_TFLOPS
+            else:
+                ach, unit, peak = work / (us * 1e-6) / 1e9, "GB/s", PEAK_HBM_GBS
+            lines.append(f"{cls:10s} {name:8s} {len(sel):6d} {us:9.2f} {ach:10.1f} {unit:8s} "
+                         f"{100.0 * ach / peak:9.1f}")
+        if win:
+            avgs[cls] = sum(u[0] for _, u in win) / len(win) / 1e3
     rf = res["roofline"]
     cls = rf["kernel"]
-    sub, epi = KERNEL_OF_CLASS[cls]
-    seq = [(a, b) for name, a, b in rows if sub in name and (epi is None or epi in name)]
-    if cls in ("GEMM_OUT", "GEMM_DOWN"):
-        seq = seq[0::2] if cls == "GEMM_OUT" else seq[1::2]
-    per_step = res["config"]["n_blocks"]
-    skip = res["warmup"] * per_step
-    win = seq[skip: skip + rf["launches"]]
-    avg = sum(b - a for a, b in win) / max(len(win), 1) / 1e3
     lines.append("")
-    lines.append(f"timed window: {cls} launches {skip}..{skip + len(win) - 1}: "
-                 f"avg {avg:.2f} us (bench live HIP-event average {rf['avg_launch_us']:.2f} us)")
+    lines.append(f"timed window: {cls} {len(timed_window(res, cls, class_units(trows, cls)))} launch units, "
+                 f"avg {avgs.get(cls, float('nan')):.2f} us (bench live HIP-event average "
+                 f"{rf['avg_launch_us']:.2f} us)")
     return "\n".join(lines)
 
 
 def load_model(cfg, dev, adt):
+    """Seeded block weights (every block has its own random stream, so drawing
+    them on a thread pool gives the same arrays), copied to the device."""
     import torch
     import workload as W
     from paper_2609_38984_amd import swam
     blocks_np, dblocks = [], []
-    for l in range(cfg.n_blocks):
-        b = W.block_weights(cfg, l)
-        if l == 0:
-            blocks_np.append(b)
-        dblocks.append({k: torch.from_numpy(v).to(dev, adt) for k, v in b.items()})
+    workers = max(1, min(8, len(os.sched_getaffinity(0))))
+    with ThreadPoolExecutor(workers) as ex:
+        for l, b in enumerate(ex.map(lambda i: W.block_weights(cfg, i), range(cfg.n_blocks))):
+            if l == 0:
+                blocks_np.append(b)
+            dblocks.append({k: torch.from_numpy(v).to(dev, adt) for k, v in b.items()})
     return blocks_np, swam.Model(dblocks, adt)
 
 
@@ -273,6 +429,21 @@ def measure(cfg, model, xs, tembs, steps, warmup, reps):
     t_refresh = median_ms(swam.FORCE_REFRESH, 0)
     run(0)                                       # a fresh selection for the sparse medians
     t_sparse = median_ms(0, 1) if cfg.reuse_R > 1 else float("nan")
+
+    def class_times(flags, tau, n=3):
+        """(launches, ms) per class and step, every class bracketed by events."""
+        ctx.timer_enable(swam.TIMERS, capacity=1 << 14)
+        for _ in range(n):
+            run(tau, flags)
+        got = {c: ctx.timer_read(c) for c in swam.TIMERS}
+        ctx.timer_enable([], 1)
+        return {c: (k / n, ms / n) for c, (k, ms) in got.items() if k}
+
+    per_kind = {"dense": class_times(swam.FORCE_DENSE, 0), "refresh": class_times(swam.FORCE_REFRESH, 0)}
+    if cfg.reuse_R > 1:
+        run(0)
+        per_kind["sparse"] = class_times(0, 1)
+    by_class = class_rooflines(cfg, per_kind, full_rows, packed_rows)
     ctx.timer_enable(swam.TIMERS, capacity=1 << 15)
     for t in range(n_sched):
         run(t)
@@ -294,6 +465,11 @@ def measure(cfg, model, xs, tembs, steps, warmup, reps):
                        "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": round(gbs / PEAK_HBM_GBS, 4)}
     ctx.timer_enable([], 1)
     over = sum(phase_ms[c] for c in ("SCORE", "REDUCE", "SELECT", "PACK", "UNPACK"))
+    # what the overhead costs the schedule: a refresh step's excess over the
+    # dense step (scoring overlaps the blocks on a side stream) plus pack and
+    # unpack of the sparse steps, per schedule step
+    n_ref = sum(1 for t in range(n_sched) if t % cfg.reuse_R == 0)
+    exposed = (max(0.0, t_refresh - t_dense) * n_ref / n_sched + phase_ms["PACK"] + phase_ms["UNPACK"])
     tok = cfg.batch * cfg.l_full
     sched_ms = elapsed * 1e3 / steps
     return {
@@ -307,9 +483,48 @@ def measure(cfg, model, xs, tembs, steps, warmup, reps):
         "speedup_sparse_vs_dense": round(t_dense / t_sparse, 3) if t_sparse == t_sparse else None,
         "speedup_schedule_vs_dense": round(t_dense / sched_ms, 3),
         "overhead_pct_of_dense": round(100.0 * over / t_dense, 3),
+        "overhead_exposed_pct_of_dense": round(100.0 * exposed / t_dense, 3),
         "overhead_pct_of_schedule_step": round(100.0 * over / sched_ms, 3),
         "phase_ms_per_step": phase_ms, "roofline": roofline, "qk_post": qk_post,
+        "roofline_by_class": by_class,
     }
+
+
+def class_rooflines(cfg, per_kind, full_rows, packed_rows):
+    """Per kernel class: average launch time from on-stream HIP events and the
+    fraction of its roofline.  MFMA classes (attention and the four
+    projections; a split-K projection counts its partial GEMM and epilogue)
+    against the bf16 peak, separately for the dense layout (refresh / dense
+    steps) and the packed one (sparse steps); scoring, pack and unpack against
+    8 TB/s of HBM; reduce and select (latency-bound, at most 2 MB) in us."""
+    peak_mfma = PEAK_BF16_TFLOPS if cfg.dtype == "bf16" else PEAK_FP32_TFLOPS
+    out = {}
+    for kind, rows in (("dense", full_rows), ("sparse", packed_rows)):
+        if kind not in per_kind:
+            continue
+        d = {}
+        for cls in MFMA_CLASSES:
+            n, ms = per_kind[kind].get(cls, (0, 0.0))
+            if not n:
+                continue
+            us = ms * 1e3 / n
+            tf = kernel_work(cfg, cls, rows) / (us * 1e-6) / 1e12
+            d[cls] = {"us": round(us, 2), "TFLOP/s": round(tf, 1), "frac": round(tf / peak_mfma, 4)}
+        out[kind + "_mfma"] = d
+    mem = {}
+    for kind, cls, rows in (("refresh", "SCORE", full_rows), ("sparse", "PACK", packed_rows),
+                            ("sparse", "UNPACK", packed_rows)):
+        n, ms = per_kind.get(kind, {}).get(cls, (0, 0.0))
+        if not n:
+            continue
+        us = ms * 1e3 / n
+        gbs = kernel_work(cfg, cls, rows) / (us * 1e-6) / 1e9
+        mem[cls] = {"us": round(us, 2), "launches_per_step": round(n, 2), "GB/s": round(gbs, 1),
+                    "frac": round(gbs / PEAK_HBM_GBS, 4)}
+    out["hbm"] = mem
+    out["latency_us_per_refresh"] = {c: round(per_kind["refresh"].get(c, (0, 0.0))[1] * 1e3, 1)
+                                     for c in ("REDUCE", "SELECT")}
+    return out
 
 
 def measure_graph(cfg, model, xs, tembs, steps, reps):
@@ -411,6 +626,38 @@ def sweep(args):
     _, xs, tembs = inputs_for(cfg, blocks_np, dev, torch.bfloat16)
     emit(cfg, "mass 0.8", measure(cfg, model, xs, tembs, cfg.n_steps, 2, args.sweep_reps), model, xs,
          tembs)
+
+
+def second_point(dev, reps):
+    """The 2048-wide workload (17,472 tokens, 28 blocks, 32 heads) at 25% + 64
+    retention with reuse R = 2: dense / refresh / sparse medians, score+pack
+    overhead and per-class rooflines, from the same measurement as the main
+    line (two schedule steps of inputs, tau = 0 and 1)."""
+    import torch
+    import workload as W
+    cfg = W.preset(4, percent=25, reuse_R=2)
+    log(f"[bench] second point {cfg.name}: L_full={cfg.l_full} d={cfg.d_model}")
+    t0 = time.perf_counter()
+    blocks_np, model = load_model(cfg, dev, torch.bfloat16)
+    inp = W.make_inputs(cfg, blocks_np[0]["w_qkv"])
+    xs = [torch.from_numpy(inp.x(t)).to(dev, torch.bfloat16) for t in range(2)]
+    tembs = [torch.from_numpy(inp.temb(t)).to(dev) for t in range(2)]
+    log(f"[bench] second point resident ({time.perf_counter() - t0:.1f}s)")
+    m = measure(cfg, model, xs, tembs, 4, 2, reps)
+    n_f = sum(1 for t in range(cfg.n_steps) if t % cfg.reuse_R == 0)
+    sched = (n_f * m["refresh_step_ms"] + (cfg.n_steps - n_f) * m["sparse_step_ms"]) / cfg.n_steps
+    out = {"workload": cfg.name, "l_full": cfg.l_full, "packed_rows": m["packed_rows"],
+           "k_core": cfg.k_core, "k_anchor": cfg.k_anchor, "reuse_R": cfg.reuse_R,
+           "schedule_steps": cfg.n_steps,
+           "schedule_step_ms_from_medians": round(sched, 4),
+           "schedule_tokens_per_s_from_medians": round(cfg.l_full / sched * 1e3, 1)}
+    for k in ("dense_step_ms", "refresh_step_ms", "sparse_step_ms", "dense_tokens_per_s",
+              "sparse_tokens_per_s", "speedup_sparse_vs_dense", "overhead_pct_of_dense",
+              "overhead_exposed_pct_of_dense", "roofline_by_class"):
+        out[k] = m[k]
+    del model, xs
+    torch.cuda.empty_cache()
+    return out
 
 
 def overlap_diagnostic(cfg, model, xs, tembs):
@@ -528,51 +775,81 @@ def traffic_file(cls, workload):
 
 
 def summarize_traffic(fetch_db, write_db, bench_json):
-    """HBM bytes per launch of the dominant kernel from FETCH_SIZE / WRITE_SIZE
-    counter runs, each scaled by its reading for the library's plain copy kernel
-    (copy_chunks: rows_full * d * elem bytes read and written per launch)."""
+    """HBM bytes per launch unit from FETCH_SIZE / WRITE_SIZE counter runs, each
+    scaled by its reading for the library's plain copy kernel (copy_chunks:
+    rows_full * d * elem bytes read and written per launch), over exactly the
+    timed steps, per class and step kind; the dominant class's average over
+    all its timed units is what the bench line reports as traffic."""
     import sqlite3
     res = json.load(open(bench_json))
-    cfg = res["config"]
+    cfgj = res["config"]
+    cfg = workload_from_json(cfgj)
     esz = 2 if res["dtype"] == "bf16" else 4
-    copy_bytes = cfg["batch"] * cfg["l_full"] * cfg["d_model"] * esz
+    copy_bytes = cfgj["batch"] * cfgj["l_full"] * cfgj["d_model"] * esz
 
     def per_dispatch(db, counter):
         con = sqlite3.connect(db)
-        return con.execute("select name, value from (select name, dispatch_id, sum(counter_value) as value "
-                           "from pmc_events where counter_name = ? group by dispatch_id) order by dispatch_id",
+        return con.execute("select dispatch_id, name, sum(counter_value) from pmc_events "
+                           "where counter_name = ? group by dispatch_id order by dispatch_id",
                            (counter,)).fetchall()
 
     fetch = per_dispatch(fetch_db, "FETCH_SIZE")
     write = per_dispatch(write_db, "WRITE_SIZE")
-    cal_f = [v for n, v in fetch if "copy_chunks" in n]
-    cal_w = [v for n, v in write if "copy_chunks" in n]
+    cal_f = [v for _, n, v in fetch if "copy_chunks" in n]
+    cal_w = [v for _, n, v in write if "copy_chunks" in n]
     f_fac = copy_bytes / (1024.0 * sum(cal_f) / len(cal_f))
     w_fac = copy_bytes / (1024.0 * sum(cal_w) / len(cal_w))
-    rf = res["roofline"]
-    cls = rf["kernel"]
-    sub, epi = KERNEL_OF_CLASS[cls]
-
-    def window(rows):
-        seq = [v for n, v in rows if sub in n and (epi is None or epi in n)]
-        if cls in ("GEMM_OUT", "GEMM_DOWN"):
-            seq = seq[0::2] if cls == "GEMM_OUT" else seq[1::2]
-        skip = res["warmup"] * res["config"]["n_blocks"]
-        return seq[skip: skip + rf["launches"]]
-
-    wf, ww = window(fetch), window(write)
-    n = min(len(wf), len(ww))
-    per_launch = sum(wf[i] * 1024.0 * f_fac + ww[i] * 1024.0 * w_fac for i in range(n)) / max(n, 1)
+    full = [cfg.l_full] * cfg.batch
+    packed = cfgj["packed_per_seq"]
     lines = [f"calibration: copy_chunks moves {copy_bytes} bytes each way per launch; "
              f"FETCH_SIZE reads {sum(cal_f) / len(cal_f):.1f} KiB (factor {f_fac:.4f}), "
              f"WRITE_SIZE reads {sum(cal_w) / len(cal_w):.1f} KiB (factor {w_fac:.4f})",
-             f"{cls} timed window: {n} launches, avg FETCH {sum(wf[:n]) / max(n, 1):.1f} KiB, "
-             f"avg WRITE {sum(ww[:n]) / max(n, 1):.1f} KiB per launch (raw)",
-             f"traffic_per_launch_bytes: {int(per_launch)}",
-             f"kernel_class: {cls}",
-             f"workload: {cfg['workload']}",
-             f"source_sha256_16: {kernel_source_hash(cls)}"]
+             "",
+             "timed steps, HBM bytes per launch unit (FETCH + WRITE, calibrated) against the "
+             "algorithmic bytes (MFMA classes: operands read once, outputs written once):",
+             f"{'class':10s} {'kind':8s} {'units':>6s} {'MB':>9s} {'alg_MB':>9s} {'ratio':>6s}"]
+    dom = res["roofline"]["kernel"]
+    dom_avg = None
+    for cls in MFMA_CLASSES + ("SCORE", "PACK", "UNPACK"):
+        wf = timed_window(res, cls, class_units(fetch, cls))
+        ww = timed_window(res, cls, class_units(write, cls))
+        n = min(len(wf), len(ww))
+        if not n:
+            continue
+        tot = [wf[i][1][0] * 1024.0 * f_fac + ww[i][1][0] * 1024.0 * w_fac for i in range(n)]
+        for kind, name in ((1, "refresh"), (2, "sparse")):
+            sel = [t for i, t in enumerate(tot) if wf[i][0] == kind]
+            if not sel:
+                continue
+            rows = full if kind == 1 else packed
+            alg = algorithmic_bytes(cfg, cls, rows)
+            mb = sum(sel) / len(sel) / 1e6
+            lines.append(f"{cls:10s} {name:8s} {len(sel):6d} {mb:9.2f} {alg / 1e6:9.2f} {mb * 1e6 / alg:6.2f}")
+        if cls == dom:
+            dom_avg = sum(tot) / n
+    lines += ["",
+              f"traffic_per_launch_bytes: {int(dom_avg) if dom_avg else 0}",
+              f"kernel_class: {dom}",
+              f"workload: {cfgj['workload']}",
+              f"source_sha256_16: {kernel_source_hash(dom)}"]
     return "\n".join(lines)
+
+
+def algorithmic_bytes(cfg, cls, rows_per_seq):
+    """Bytes a launch must move at least: memory-bound classes their
+    kernel_work; MFMA classes their operands read once and result written once
+    (attention: q, k, v and o of every row, lambda; projections: A, B, bias, C,
+    and the residual for the gated ones)."""
+    if BOUND[cls] == "hbm":
+        return kernel_work(cfg, cls, rows_per_seq)
+    d, hid, m = cfg.d_model, cfg.mlp_ratio * cfg.d_model, sum(rows_per_seq)
+    esz = 2 if cfg.dtype == "bf16" else 4
+    if cls == "ATTN":
+        return m * 4 * d * esz + m * cfg.n_heads * 4
+    n_k = {"GEMM_QKV": (3 * d, d), "GEMM_OUT": (d, d), "GEMM_UP": (hid, d), "GEMM_DOWN": (d, hid)}[cls]
+    n, k = n_k
+    resid = 2 if cls in ("GEMM_OUT", "GEMM_DOWN") else 1
+    return (m * k + n * k + n + resid * m * n) * esz
 
 
 def read_traffic(cls, workload):
@@ -594,53 +871,48 @@ def read_traffic(cls, workload):
 
 
 def summarize_mfma(db_path, bench_json):
-    """MFMA-busy share per MFMA kernel class over the timed steps, from one
-    `rocprofv3 --kernel-trace --pmc SQ_VALU_MFMA_BUSY_CYCLES SQ_BUSY_CYCLES
-    GRBM_GUI_ACTIVE SQ_INSTS_VALU_MFMA_MOPS_BF16` run of this benchmark.
-    SQ_VALU_MFMA_BUSY_CYCLES counts SIMD-cycles with the matrix core busy; it
-    is divided by the launch time x 2.4 GHz x 1024 SIMDs (the clock of the
-    2.5 PFLOP/s peak).  SQ_INSTS_VALU_MFMA_MOPS_BF16 x 512 is the flops the
-    matrix cores executed (padding of ragged tiles included).  GRBM_GUI_ACTIVE
-    / 8 XCDs / launch time is shown as the clock the GPU ran at (approximate
-    for short launches, whose counts include dispatch overhead)."""
+    """MFMA-busy share per MFMA kernel class and step kind over the timed
+    steps, from one `rocprofv3 --kernel-trace --pmc SQ_VALU_MFMA_BUSY_CYCLES
+    SQ_BUSY_CYCLES GRBM_GUI_ACTIVE SQ_INSTS_VALU_MFMA_MOPS_BF16` run of this
+    benchmark.  SQ_VALU_MFMA_BUSY_CYCLES counts SIMD-cycles with the matrix
+    core busy; it is divided by the launch time x 2.4 GHz x 1024 SIMDs (the
+    clock of the 2.5 PFLOP/s peak).  SQ_INSTS_VALU_MFMA_MOPS_BF16 x 512 is the
+    flops the matrix cores executed (padding of ragged tiles included).
+    GRBM_GUI_ACTIVE / 8 XCDs / launch time is the clock the GPU ran at
+    (approximate for short launches).  A split-K projection counts its
+    partial GEMM and its epilogue."""
     import sqlite3
     res = json.load(open(bench_json))
     cfgj = res["config"]
+    cfg = workload_from_json(cfgj)
     con = sqlite3.connect(db_path)
-    rows = con.execute("select dispatch_id, name, counter_name, sum(counter_value) from pmc_events "
-                       "group by dispatch_id, counter_name").fetchall()
     cnt, names = {}, {}
-    for did, name, c, v in rows:
+    for did, name, c, v in con.execute("select dispatch_id, name, counter_name, sum(counter_value) "
+                                       "from pmc_events group by dispatch_id, counter_name"):
         cnt.setdefault(did, {})[c] = v
         names[did] = name
     dur = {did: b - a for did, a, b in con.execute("select dispatch_id, start, end from kernels")}
-    cfg = workload_from_json(cfgj)
-    packed = cfgj["packed_rows"]
-    lines = [f"{'class':10s} {'launches':>8s} {'avg_us':>8s} {'MFMA_busy_%':>11s} {'alg_TFLOP/s':>11s} "
-             f"{'%_of_2.5PF':>10s} {'exec/alg_flops':>14s} {'GRBM_clock_GHz':>14s}"]
-    skip = res["warmup"] * cfgj["n_blocks"]
-    for cls in ("ATTN", "GEMM_QKV", "GEMM_OUT", "GEMM_UP", "GEMM_DOWN"):
-        sub, epi = KERNEL_OF_CLASS[cls]
-        seq = [did for did in sorted(cnt) if sub in names[did] and (epi is None or epi in names[did])]
-        if cls in ("GEMM_OUT", "GEMM_DOWN"):
-            seq = seq[0::2] if cls == "GEMM_OUT" else seq[1::2]
-        win = seq[skip: skip + len(res["config"]["schedule_kinds"]) * cfgj["n_blocks"]]
-        if not win:
-            continue
-        kinds = res["config"]["schedule_kinds"]
-        alg = 0.0
-        for i, _ in enumerate(win):
-            k = kinds[i // cfgj["n_blocks"]]
-            rows_k = [cfgj["l_full"]] * cfgj["batch"] if k != 2 else [packed]
-            alg += kernel_work(cfg, cls, rows_k)
-        t = sum(dur.get(d, 0) for d in win) * 1e-9
-        gui = sum(cnt[d].get("GRBM_GUI_ACTIVE", 0) for d in win) / 8.0
-        busy = sum(cnt[d].get("SQ_VALU_MFMA_BUSY_CYCLES", 0) for d in win)
-        mops = sum(cnt[d].get("SQ_INSTS_VALU_MFMA_MOPS_BF16", 0) for d in win)
-        lines.append(f"{cls:10s} {len(win):8d} {t / len(win) * 1e6:8.1f} "
-                     f"{100.0 * busy / (t * 2.4e9 * 1024):11.1f} {alg / t / 1e12:11.1f} "
-                     f"{100.0 * alg / t / 1e12 / PEAK_BF16_TFLOPS:10.1f} {mops * 512 / alg:14.3f} "
-                     f"{gui / t / 1e9:14.2f}")
+    trows = [(did, names[did], dur.get(did, 0)) for did in sorted(cnt)]
+    full = [cfg.l_full] * cfg.batch
+    packed = cfgj["packed_per_seq"]
+    lines = [f"{'class':10s} {'kind':8s} {'units':>6s} {'avg_us':>8s} {'MFMA_busy_%':>11s} "
+             f"{'alg_TFLOP/s':>11s} {'%_of_2.5PF':>10s} {'exec/alg_flops':>14s} {'GRBM_clock_GHz':>14s}"]
+    for cls in MFMA_CLASSES:
+        win = timed_window(res, cls, class_units(trows, cls))
+        for kind, kname in ((1, "refresh"), (2, "sparse")):
+            sel = [u for k, u in win if k == kind]
+            if not sel:
+                continue
+            ids = [i for u in sel for i in u[1]]
+            t = sum(u[0] for u in sel) * 1e-9
+            alg = kernel_work(cfg, cls, full if kind == 1 else packed) * len(sel)
+            gui = sum(cnt[i].get("GRBM_GUI_ACTIVE", 0) for i in ids) / 8.0
+            busy = sum(cnt[i].get("SQ_VALU_MFMA_BUSY_CYCLES", 0) for i in ids)
+            mops = sum(cnt[i].get("SQ_INSTS_VALU_MFMA_MOPS_BF16", 0) for i in ids)
+            lines.append(f"{cls:10s} {kname:8s} {len(sel):6d} {t / len(sel) * 1e6:8.1f} "
+                         f"{100.0 * busy / (t * 2.4e9 * 1024):11.1f} {alg / t / 1e12:11.1f} "
+                         f"{100.0 * alg / t / 1e12 / PEAK_BF16_TFLOPS:10.1f} {mops * 512 / alg:14.3f} "
+                         f"{gui / t / 1e9:14.2f}")
     return "\n".join(lines)
 
 
@@ -679,6 +951,8 @@ def main():
                     help="timed repetitions per step kind for the medians (after 5 untimed)")
     ap.add_argument("--sweep-reps", type=int, default=5, help="the same, per sweep workload")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-second-point", action="store_true",
+                    help="skip the 2048-wide 25%% / R = 2 point of the default line")
     ap.add_argument("--sweep", action="store_true", help="markdown table over all workloads")
     ap.add_argument("--sampler", action="store_true",
                     help="closed-loop sampling with the cached-velocity merge (own JSON line)")
@@ -728,16 +1002,22 @@ def main():
                    "mass_threshold": cfg.mass_threshold, "reuse_R": cfg.reuse_R,
                    "rope": cfg.rope, "qk_norm": cfg.qk_norm, "cfg_pairs": cfg.cfg_pairs,
                    "guidance": cfg.guidance if cfg.cfg_pairs else None,
-                   "packed_rows": m["packed_rows"], "schedule_kinds": m["kinds"]},
+                   "packed_rows": m["packed_rows"], "packed_per_seq": m["packed_per_seq"],
+                   "schedule_kinds": m["kinds"]},
     }
     for k in ("dense_step_ms", "refresh_step_ms", "sparse_step_ms", "dense_tokens_per_s",
               "sparse_tokens_per_s", "refresh_tokens_per_s", "speedup_sparse_vs_dense",
-              "speedup_schedule_vs_dense", "overhead_pct_of_dense", "overhead_pct_of_schedule_step",
-              "phase_ms_per_step", "roofline"):
+              "speedup_schedule_vs_dense", "overhead_pct_of_dense", "overhead_exposed_pct_of_dense",
+              "overhead_pct_of_schedule_step", "phase_ms_per_step", "roofline", "roofline_by_class"):
         out[k] = m[k]
     if m["qk_post"] is not None:
         out["qk_post"] = m["qk_post"]
     out["selection_overlap"] = overlap_diagnostic(cfg, model, xs, tembs)
+    if args.config == 3 and not args.no_second_point and not (args.rope or args.qk_norm
+                                                              or args.guidance is not None):
+        del model, xs
+        torch.cuda.empty_cache()
+        out["point_d2048_r25_R2"] = second_point(dev, args.reps)
     if not args.no_cpu_baseline:
         log("[bench] timing the CPU oracle on a bounded sample")
         out["cpu_baseline"] = cpu_baseline(cfg, m["kinds"], blocks_np, inp)
