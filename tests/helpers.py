@@ -47,3 +47,22 @@ def model_for(cfg, n_blocks=None):
     blocks = [W.block_weights(cfg, l) for l in range(n)]
     dblocks = device_blocks(cfg, blocks)
     return blocks, dblocks, swam.Model(dblocks, act_dtype(cfg))
+
+
+def lse_from_qkv(qkv, cu, rows, n_heads):
+    """lambda[r][h] = log sum_j exp(q_h(r) . k_h(j) / 8) over every key j of the
+    sequence that holds row r, in float64 from a QKV buffer [rows][3][N_h][64]
+    (the normaliser the attention kernel exports, recomputed from the very q
+    and k it read)."""
+    qkv = np.asarray(qkv, np.float64)
+    d = n_heads * 64
+    cu = np.asarray(cu, np.int64)
+    out = np.empty((len(rows), n_heads))
+    for i, r in enumerate(rows):
+        b = int(np.searchsorted(cu, r, side="right") - 1)
+        k = qkv[cu[b]:cu[b + 1], d:2 * d].reshape(-1, n_heads, 64)
+        q = qkv[r, :d].reshape(n_heads, 64)
+        x = np.einsum("he,jhe->hj", q, k) / 8.0
+        m = x.max(axis=1, keepdims=True)
+        out[i] = (m[:, 0] + np.log(np.exp(x - m).sum(axis=1)))
+    return out

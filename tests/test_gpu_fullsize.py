@@ -12,7 +12,8 @@ import torch
 
 import oracle as O
 import workload as W
-from helpers import act_dtype, dev, host, maxrel, model_for
+from helpers import act_dtype, dev, host, lse_from_qkv, maxrel, model_for
+from test_oracle_blob import blob_centres
 
 pytestmark = pytest.mark.gpu
 
@@ -46,14 +47,19 @@ def _sampled_block(cfg, cu, x, per_seq=24):
     ctx = _ctx(cfg)
     xd = dev(x[:n_rows], act_dtype(cfg))
     lse = torch.empty(n_rows, cfg.n_heads, dtype=torch.float32, device="cuda:0")
-    ctx.block(dblocks[0], dev(temb), xd, n_rows, dev(np.asarray(cu, np.int32)), len(cu) - 1, lse)
+    qkv = torch.empty(n_rows, 3 * cfg.d_model, dtype=act_dtype(cfg), device="cuda:0")
+    ctx.block(dblocks[0], dev(temb), xd, n_rows, dev(np.asarray(cu, np.int32)), len(cu) - 1, lse,
+              qkv)
     torch.cuda.synchronize()
     rows = _sample_rows(cu, per_seq, np.random.default_rng(5))
     y_ref, l_ref = O.block_rows(x[:n_rows], blocks[0], temb, cu, rows, cfg.n_heads, cfg.dtype)
     e_y = maxrel(host(xd)[rows], y_ref)
     e_l = float(np.abs(host(lse)[rows] - l_ref).max())
-    print(f"  sampled {len(rows)} rows: y max-rel {e_y:.2e}, lambda abs {e_l:.2e}", flush=True)
-    assert e_y < 2e-2 and e_l < 5e-2
+    # the kernel's normaliser against the log-sum-exp of its own q and k (every head)
+    e_own = float(np.abs(host(lse)[rows] - lse_from_qkv(host(qkv), cu, rows, cfg.n_heads)).max())
+    print(f"  sampled {len(rows)} rows: y max-rel {e_y:.2e}, lambda abs {e_l:.2e}, "
+          f"lambda abs on own qkv {e_own:.2e}", flush=True)
+    assert e_y < 2e-2 and e_l < 5e-2 and e_own < 1e-5
 
 
 def test_block_wam_dense_10160_sampled():
@@ -75,6 +81,17 @@ def test_block_ragged_batch_sampled():
     cu = np.concatenate([[0], np.cumsum(lens)])
     x = W.make_inputs(cfg, W.block_weights(cfg, 0)["w_qkv"]).x(0)
     _sampled_block(cfg, cu, x, per_seq=6)
+
+
+def test_block_2048_packed_3744_sampled():
+    """The packed sequence of the d = 2048 workload at 10% + 64 retention
+    (3,744 rows, 32 heads): the shape that runs the 4-wave attention kernel
+    at four waves per SIMD, the 128x128 QKV tile and the down projection
+    split along K in two."""
+    cfg = W.preset(4, percent=10).replace(n_blocks=1)
+    assert cfg.t_pack_fixed == 3744
+    x = W.make_inputs(cfg, W.block_weights(cfg, 0)["w_qkv"]).x(0)
+    _sampled_block(cfg, np.array([0, cfg.t_pack_fixed]), x, per_seq=24)
 
 
 def test_block_2048_dense_sampled():
@@ -131,6 +148,21 @@ def test_step_wam_fullsize_properties():
     cuh = cu.cpu().numpy()
     assert cuh[-1] == cfg.t_pack_fixed == ctx.packed_rows()
     _check_selection(cfg, ki.cpu().numpy(), kc.cpu().numpy(), pp.cpu().numpy(), ga.cpu().numpy(), cuh)
+    # the planted action-relevant blob: its centre is a core token of every
+    # frame (the oracle's select on the kernel's V and A reproduces the
+    # kernel's selection bit for bit, so its core sets are the kernel's)
+    Vd = torch.empty(F * n_s, dtype=torch.float32, device="cuda:0")
+    Ad = torch.empty(n_s, dtype=torch.float32, device="cuda:0")
+    ctx.export(v=Vd, a=Ad)
+    torch.cuda.synchronize()
+    Vh = Vd.cpu().numpy().reshape(F, n_s)
+    sel = O.select(Vh, Ad.cpu().numpy(), cfg.k_core, cfg.k_anchor)
+    kih = ki.cpu().numpy().reshape(F, -1)
+    for f, centres in enumerate(blob_centres(inp, cfg, 0, 0)):
+        for j in centres:
+            rank = int((Vh[f] > Vh[f, j]).sum())
+            print(f"  frame {f}: blob centre {j} ranks {rank} of {n_s}", flush=True)
+            assert j in set(int(i) for i in sel.core[f]) and j in set(int(i) for i in kih[f])
     # reuse: re-selecting on the exported scores in a fresh context gives the cached selection
     ctx2 = _ctx(cfg)
     V = torch.empty(F * n_s, dtype=torch.float32, device="cuda:0")

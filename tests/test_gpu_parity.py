@@ -13,7 +13,7 @@ import torch
 
 import oracle as O
 import workload as W
-from helpers import act_dtype, dev, host, maxrel, model_for, rowwise_maxrel
+from helpers import act_dtype, dev, host, lse_from_qkv, maxrel, model_for, rowwise_maxrel
 
 pytestmark = pytest.mark.gpu
 
@@ -62,8 +62,12 @@ def _block_case(cfg, cu, tol, lse_tol):
     for a, b in zip(cu[:-1], cu[1:]):
         valid[a:b] = True
     e_l = float(np.abs(host(lse)[valid] - tr.lse[valid]).max())
-    print(f"  y {e_y:.2e} qkv {e_q:.2e} lse-abs {e_l:.2e}", flush=True)
-    assert e_q < tol and e_y < tol and e_l < lse_tol
+    # the exported normaliser against the log-sum-exp of the kernel's own q and
+    # k: every valid row, every head (App. A.2 reuses it as the score's normaliser)
+    rows = np.nonzero(valid)[0]
+    e_own = float(np.abs(host(lse)[rows] - lse_from_qkv(host(qkv), cu, rows, cfg.n_heads)).max())
+    print(f"  y {e_y:.2e} qkv {e_q:.2e} lse-abs {e_l:.2e} lse-abs on own qkv {e_own:.2e}", flush=True)
+    assert e_q < tol and e_y < tol and e_l < lse_tol and e_own < 1e-5
 
 
 def test_block_fp32_dense():
@@ -254,6 +258,13 @@ def test_select_mass_threshold_ragged():
 def test_select_mass_threshold_with_anchors():
     _select_case(W.preset(5).replace(n_blocks=2, d_model=64, n_heads=1, batch=3, k_anchor=40,
                                      mass_threshold=0.55), 73)
+
+
+@pytest.mark.parametrize("theta", [0.0125, 0.0004])
+def test_select_mass_threshold_small_thetas(theta):
+    # 1000 theta of the float32 threshold is 12.5000002 (numerator 13) and 0.4
+    # (numerator 0: one core token per frame)
+    _select_case(W.preset(5).replace(n_blocks=2, d_model=64, n_heads=1, mass_threshold=theta), 76)
 
 
 # frames at the library's maximum of 4096 tokens (the capacity of the selection
