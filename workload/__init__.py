@@ -299,7 +299,7 @@ class StepInputs:
     cfg: SwamConfig
     base: list = field(default_factory=list)      # per sequence: [L_full][d] float32
     blobs: list = field(default_factory=list)     # per sequence: list[_Blob]
-    direction: list = field(default_factory=list)  # per sequence: [d] float32 (norm sqrt(d))
+    direction: list = field(default_factory=list)  # per sequence: [F][d] float32 (rows of norm sqrt(d))
 
     def x(self, tau: int) -> np.ndarray:
         """x_full at step tau, [B * L_full][d] float32 on the storage grid."""
@@ -309,7 +309,7 @@ class StepInputs:
             xb = self.base[b].copy()
             w = _blob_weights(cfg, self.blobs[b], tau)           # [F][N_s]
             fut = xb[cfg.n_ctx:cfg.n_ctx + cfg.n_fut].reshape(cfg.n_frames, cfg.n_s, cfg.d_model)
-            fut += 0.5 * w[:, :, None].astype(np.float32) * self.direction[b][None, None, :]
+            fut += 0.5 * w[:, :, None].astype(np.float32) * self.direction[b][:, None, :]
             out.append(xb)
         return _storage(cfg, np.concatenate(out, axis=0))
 
@@ -357,18 +357,25 @@ def _blob_weights(cfg: SwamConfig, blobs, tau: int) -> np.ndarray:
 
 
 def blob_direction(cfg: SwamConfig, w_qkv0: np.ndarray, act_tokens: np.ndarray) -> np.ndarray:
-    """Token-space direction that raises action-query logits.
+    """Token-space direction, per future frame, that raises the logits of the
+    frame's own action queries, [F][d].
 
-    The mean action token is mapped to query space by block 0's query
-    projection and back to token space by the transpose of its key projection,
-    then scaled to the typical token norm sqrt(d).
+    Frame f is scored by its group of g = H / F action queries (rows
+    f*g .. f*g + g - 1 of the action block).  The mean action token of that
+    group is mapped to query space by block 0's query projection and back to
+    token space by the transpose of its key projection, then scaled to the
+    typical token norm sqrt(d).
     """
     d = cfg.d_model
-    a_mean = act_tokens.astype(np.float64).mean(axis=0)
+    g = cfg.n_act // cfg.n_frames
     w_q = w_qkv0[0:d].astype(np.float64)
     w_k = w_qkv0[d:2 * d].astype(np.float64)
-    u = w_k.T @ (w_q @ a_mean)
-    return (u * (math.sqrt(d) / np.linalg.norm(u))).astype(np.float32)
+    out = np.empty((cfg.n_frames, d), np.float32)
+    for f in range(cfg.n_frames):
+        a_mean = act_tokens[f * g:(f + 1) * g].astype(np.float64).mean(axis=0)
+        u = w_k.T @ (w_q @ a_mean)
+        out[f] = u * (math.sqrt(d) / np.linalg.norm(u))
+    return out
 
 
 def make_inputs(cfg: SwamConfig, w_qkv0: np.ndarray | None = None) -> StepInputs:
