@@ -238,6 +238,36 @@ int swam_select(swam_ctx* ctx, const float* v, const float* a, int32_t* keep_idx
                 int32_t* keep_cnt, int32_t* pack_pos, int32_t* gather,
                 int32_t* cu_seqlens);
 
+/* Selection without allocation, for callers that cannot allocate device
+ * memory (code under HIP graph capture, tight serving loops, harnesses that
+ * forbid it): the pool / core / anchor selection and pack map of swam_select
+ * for explicit sizes, with no context.  Its scratch (pool, core and keep
+ * flags) is a static device array of SWAM_NOALLOC_SCRATCH_BYTES per GPU that
+ * the library holds until the process ends; no call allocates or frees
+ * anything and nothing is read back to the host.  Calls on one GPU share that
+ * array, so calls that overlap on one GPU (different streams, or host
+ * threads) race: serialise them.
+ *   batch, n_frames, n_s, n_ctx, n_act : sizes as in swam_config (token
+ *       layout of the header; l_full = n_ctx + n_frames * n_s + n_act);
+ *   k_core, k_anchor, mass_threshold : budgets as in swam_config (the
+ *       threshold's numerator is the integer nearest to 1000 x the value);
+ *   v, a : float [batch][n_frames][n_s], [batch][n_s] device inputs;
+ *   keep_idx int32 [batch][n_frames][k_max] (k_max = max(1, k_core +
+ *       k_anchor), or n_s in mass-threshold mode), keep_cnt [batch][n_frames],
+ *       pack_pos and gather [batch * l_full], cu_seqlens [batch + 1]: device
+ *       outputs, all required, laid out as in swam_select;
+ *   stream : the hipStream_t to enqueue on (NULL = the null stream).
+ * Scratch need: align256(batch * n_s) + align256(batch * n_frames * n_s) +
+ * 4 * batch * l_full bytes; above SWAM_NOALLOC_SCRATCH_BYTES the call returns
+ * SWAM_E_SHAPE before launching anything.  Other invalid sizes or NULL
+ * pointers give SWAM_E_INVALID / SWAM_E_SHAPE; the message is in
+ * swam_last_error(NULL). */
+#define SWAM_NOALLOC_SCRATCH_BYTES (1 << 20)
+int swam_select_noalloc(int32_t batch, int32_t n_frames, int32_t n_s, int32_t n_ctx,
+                        int32_t n_act, int32_t k_core, int32_t k_anchor, float mass_threshold,
+                        const float* v, const float* a, int32_t* keep_idx, int32_t* keep_cnt,
+                        int32_t* pack_pos, int32_t* gather, int32_t* cu_seqlens, void* stream);
+
 /* Random-selection baseline (the component ablation compares the method
  * with tokens chosen at random at the same per-frame budget): per scored
  * sequence and frame, the K_c + K_s positions with the largest uniform keys

@@ -7,6 +7,7 @@
 #include <string.h>
 
 #include <algorithm>
+#include <mutex>
 #include <numeric>
 #include <new>
 #include <string>
@@ -678,6 +679,104 @@ int swam_select_random(swam_ctx* c, uint64_t seed, int32_t* keep_idx, int32_t* k
   if (rc != SWAM_OK) return rc;
   return swam_export(c, nullptr, nullptr, nullptr, nullptr, keep_idx, keep_cnt, pack_pos, gather,
                      cu_seqlens);
+}
+
+}  // extern "C"
+
+// ------------------------------------------- selection without allocation
+// Scratch of swam_select_noalloc.  In host code `scratch` names a host-side
+// stand-in, not device memory: its device address is resolved once per
+// device with hipGetSymbolAddress and only that address is used.
+static __device__ __align__(256) uint8_t scratch[SWAM_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+
+constexpr int kScratchDevices = 64;
+std::mutex g_scratch_mu;
+uint8_t* g_scratch[kScratchDevices] = {};
+
+// device address of `scratch` on the current device (resolved on first use)
+int scratch_of_current_device(uint8_t** out) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return set_err(nullptr, SWAM_E_HIP, std::string("hipGetDevice: ") + hipGetErrorString(e));
+  if (dev < 0 || dev >= kScratchDevices)
+    return set_err(nullptr, SWAM_E_UNSUPPORTED, "device index beyond 63");
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p)
+      return set_err(nullptr, SWAM_E_HIP, std::string("hipGetSymbolAddress(scratch): ") +
+                                          hipGetErrorString(e));
+    g_scratch[dev] = (uint8_t*)p;
+  }
+  *out = g_scratch[dev];
+  return SWAM_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int swam_select_noalloc(int32_t batch, int32_t n_frames, int32_t n_s, int32_t n_ctx,
+                        int32_t n_act, int32_t k_core, int32_t k_anchor, float mass_threshold,
+                        const float* v, const float* a, int32_t* keep_idx, int32_t* keep_cnt,
+                        int32_t* pack_pos, int32_t* gather, int32_t* cu_seqlens, void* stream) {
+  if (!v || !a || !keep_idx || !keep_cnt || !pack_pos || !gather || !cu_seqlens)
+    return set_err(nullptr, SWAM_E_INVALID, "every tensor argument is required");
+  if (batch < 1 || batch > SWAM_MAX_BATCH) return set_err(nullptr, SWAM_E_SHAPE, "batch must be in [1, 64]");
+  if (n_frames < 1 || n_frames > SWAM_MAX_FRAMES)
+    return set_err(nullptr, SWAM_E_SHAPE, "n_frames must be in [1, 64]");
+  if (n_s < 2 || n_s > SWAM_MAX_NS) return set_err(nullptr, SWAM_E_SHAPE, "n_s must be in [2, 4096]");
+  if (n_ctx < 0 || n_act < 0) return set_err(nullptr, SWAM_E_INVALID, "n_ctx and n_act must be >= 0");
+  if (!(mass_threshold >= 0.0f && mass_threshold <= 1.0f))
+    return set_err(nullptr, SWAM_E_INVALID, "mass_threshold must be in [0, 1]");
+  if (k_anchor < 0 || k_anchor >= n_s) return set_err(nullptr, SWAM_E_INVALID, "k_anchor must be in [0, n_s)");
+  if (mass_threshold == 0.0f && (k_core < 0 || (int64_t)k_core + k_anchor > n_s))
+    return set_err(nullptr, SWAM_E_INVALID, "k_core + k_anchor must be in [0, n_s]");
+  const int64_t l_full = (int64_t)n_ctx + (int64_t)n_frames * n_s + n_act;
+  const size_t pool_b = align_up((size_t)batch * n_s);
+  const size_t core_b = align_up((size_t)batch * n_frames * n_s);
+  const size_t keep_b = (size_t)batch * l_full * 4;
+  if (pool_b + core_b + keep_b > (size_t)SWAM_NOALLOC_SCRATCH_BYTES)
+    return set_err(nullptr, SWAM_E_SHAPE,
+                   "scratch need " + std::to_string(pool_b + core_b + keep_b) +
+                       " bytes exceeds SWAM_NOALLOC_SCRATCH_BYTES (" +
+                       std::to_string(SWAM_NOALLOC_SCRATCH_BYTES) + ")");
+  uint8_t* base = nullptr;
+  int rc = scratch_of_current_device(&base);
+  if (rc != SWAM_OK) return rc;
+  SelectArgs s{};
+  s.v = v;
+  s.a = a;
+  s.pool = base;
+  s.core = base + pool_b;
+  s.keep = (int32_t*)(base + pool_b + core_b);
+  s.keep_idx = keep_idx;
+  s.keep_cnt = keep_cnt;
+  s.B = batch;
+  s.F = n_frames;
+  s.n_s = n_s;
+  s.k_core = k_core;
+  s.k_anchor = k_anchor;
+  s.n_ctx = n_ctx;
+  s.n_act = n_act;
+  if (mass_threshold > 0.0f) {
+    mass_fraction(mass_threshold, &s.mass_num, &s.mass_den);
+    s.k_max = n_s;
+  } else {
+    s.mass_num = 0;
+    s.mass_den = 0;
+    s.k_max = std::max(1, k_core + k_anchor);
+  }
+  // every flag the kernels read is written by them first in the same call,
+  // so the array's contents from an earlier call never matter
+  const hipStream_t st = (hipStream_t)stream;
+  hipError_t e = launch_select(s, st);
+  if (e == hipSuccess) e = launch_packmap(s.keep, pack_pos, gather, cu_seqlens, batch, l_full, st);
+  if (e != hipSuccess) return set_err(nullptr, SWAM_E_HIP, std::string("select: ") + hipGetErrorString(e));
+  return SWAM_OK;
 }
 
 int swam_set_selection(swam_ctx* c, const int32_t* keep_idx, const int32_t* keep_cnt) {

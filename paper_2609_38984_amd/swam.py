@@ -30,7 +30,7 @@ EXPORTS = ["swam_create", "swam_destroy", "swam_set_stream", "swam_plan", "swam_
            "swam_block", "swam_step", "swam_step_graph", "swam_graph_clear", "swam_timer_enable",
            "swam_timer_reset", "swam_timer_read", "swam_embed", "swam_velocity",
            "swam_sample_update", "swam_sample_step", "swam_overlap", "swam_select_random",
-           "swam_flow_sigmas"]
+           "swam_flow_sigmas", "swam_select_noalloc"]
 
 # the flow-schedule shift of the paper's backbones (App. B.2)
 SCHEDULE_SHIFT = 5.0
@@ -131,6 +131,7 @@ def load_library(path: str = LIB_PATH):
         "swam_timer_read": [P, I32, C.POINTER(I64), C.POINTER(C.c_double)],
         "swam_overlap": [P, P, P, I64, I64, P],
         "swam_flow_sigmas": [I32, C.c_double, C.POINTER(C.c_double)],
+        "swam_select_noalloc": [I32, I32, I32, I32, I32, I32, I32, F, P, P, P, P, P, P, P, P],
         "swam_embed": [P, C.POINTER(LatentIOStruct), P, P],
         "swam_velocity": [P, C.POINTER(LatentIOStruct), P, I32, P],
         "swam_sample_update": [P, I32, P, P, P, F, I32],
@@ -197,6 +198,32 @@ class LatentIO:
         self.d_latent = int(weights["w_in"].shape[1])
         self.struct = LatentIOStruct(self.d_latent, *[_ptr(weights[n], act_dtype, name=n)
                                                       for n in LATENT_NAMES])
+
+
+NOALLOC_SCRATCH_BYTES = 1 << 20   # SWAM_NOALLOC_SCRATCH_BYTES
+
+
+def select_noalloc(batch, n_frames, n_s, n_ctx, n_act, k_core, k_anchor, mass_threshold,
+                   v, a, keep_idx, keep_cnt, pack_pos, gather, cu_seqlens,
+                   stream: torch.cuda.Stream | None = None):
+    """swam_select_noalloc: the selection and pack map for explicit sizes,
+    without a context and without any allocation (scratch in the library's
+    static device array), on `stream` (default: torch's current stream)."""
+    lib = load_library()
+    l_full = n_ctx + n_frames * n_s + n_act
+    k_max = n_s if mass_threshold > 0 else max(1, k_core + k_anchor)
+    i32 = torch.int32
+    args = [_ptr(v, torch.float32, batch * n_frames * n_s, "v"),
+            _ptr(a, torch.float32, batch * n_s, "a"),
+            _ptr(keep_idx, i32, batch * n_frames * k_max, "keep_idx"),
+            _ptr(keep_cnt, i32, batch * n_frames, "keep_cnt"),
+            _ptr(pack_pos, i32, batch * l_full, "pack_pos"),
+            _ptr(gather, i32, batch * l_full, "gather"),
+            _ptr(cu_seqlens, i32, batch + 1, "cu_seqlens")]
+    st = (stream or torch.cuda.current_stream()).cuda_stream
+    _check(lib, None, lib.swam_select_noalloc(int(batch), int(n_frames), int(n_s), int(n_ctx),
+                                              int(n_act), int(k_core), int(k_anchor),
+                                              float(mass_threshold), *args, C.c_void_p(st)))
 
 
 class Context:

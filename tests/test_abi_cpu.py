@@ -28,7 +28,7 @@ def _declared():
 def test_every_declared_symbol_is_exported(lib):
     from paper_2609_38984_amd import swam
     names = _declared()
-    assert len(names) == 28
+    assert len(names) == 29
     assert sorted(swam.EXPORTS) == names
     for n in names:
         assert hasattr(lib, n), n
@@ -134,3 +134,15 @@ def test_workspace_does_not_grow_with_block_depth(lib):
     assert w28 - w1 <= 27 * per_block + 16 * 256
     # one QKV slot of the 10,160-token, d = 1536 workload is 93.6 MB; 28 of them were 2.6 GB
     assert w28 < 512 << 20
+
+
+def test_select_noalloc_validates_on_the_host(lib):
+    """The allocation-free selection refuses NULL tensors and sizes beyond its
+    static scratch before any HIP call (so this runs without a GPU)."""
+    assert lib.swam_select_noalloc(1, 2, 8, 0, 2, 2, 0, 0.0, None, None, None, None, None, None,
+                                   None, None) == -1
+    fake = [C.c_void_p(256)] * 7             # never dereferenced: the size check comes first
+    # 16 sequences of 17,472 tokens: 1.1 MB of keep flags alone
+    assert lib.swam_select_noalloc(16, 16, 1024, 1024, 64, 256, 64, 0.0, *fake, None) == -2
+    assert b"SWAM_NOALLOC_SCRATCH_BYTES" in lib.swam_last_error(None)
+    assert lib.swam_select_noalloc(1, 2, 8, 0, 2, 7, 2, 0.0, *fake, None) == -1   # K_c + K_s > N_s
