@@ -444,6 +444,7 @@ def measure(cfg, model, xs, tembs, steps, warmup, reps):
         run(0)
         per_kind["sparse"] = class_times(0, 1)
     by_class = class_rooflines(cfg, per_kind, full_rows, packed_rows)
+    by_class["hbm"]["SCORE_isolated"] = score_isolated(cfg, ctx)
     ctx.timer_enable(swam.TIMERS, capacity=1 << 15)
     for t in range(n_sched):
         run(t)
@@ -488,6 +489,40 @@ def measure(cfg, model, xs, tembs, steps, warmup, reps):
         "phase_ms_per_step": phase_ms, "roofline": roofline, "qk_post": qk_post,
         "roofline_by_class": by_class,
     }
+
+
+def score_isolated(cfg, ctx, n=None):
+    """One layer's scoring per launch, alone on the context stream (swam_score,
+    mode A) over a QKV buffer and normalisers of the workload's shape: the
+    scorer's own launch time and HBM fraction (in a refresh step the same
+    launches overlap the projections on the side stream, which stretches
+    them).  Values are random (the work does not depend on them)."""
+    import torch
+    from paper_2609_38984_amd import swam
+    n = n or cfg.n_blocks
+    dev = torch.device("cuda:0")
+    adt = torch.bfloat16 if cfg.dtype == "bf16" else torch.float32
+    d, L = cfg.d_model, cfg.l_full
+    g = torch.Generator(device=dev)
+    g.manual_seed(0)
+    qkv = torch.randn(cfg.batch * L, 3 * d, device=dev, generator=g).to(adt)
+    lse = torch.full((cfg.n_scored, cfg.n_act, cfg.n_heads), 8.0, device=dev)
+    s = torch.empty(cfg.n_scored * cfg.n_frames * cfg.n_s, device=dev)
+    ld = 3 * d
+    flat = qkv.view(-1)
+    q_act = flat[(cfg.n_ctx + cfg.n_fut) * ld:]
+    k_fut = flat[cfg.n_ctx * ld + d:]
+    for _ in range(3):
+        ctx.score(q_act, L * ld, ld, k_fut, L * ld, ld, s, lse_act=lse)
+    ctx.timer_enable(["SCORE"], capacity=4 * n)
+    for _ in range(n):
+        ctx.score(q_act, L * ld, ld, k_fut, L * ld, ld, s, lse_act=lse)
+    k, ms = ctx.timer_read("SCORE")
+    ctx.timer_enable([], 1)
+    us = ms * 1e3 / max(k, 1)
+    gbs = kernel_work(cfg, "SCORE", [cfg.l_full] * cfg.batch) / (us * 1e-6) / 1e9
+    return {"us": round(us, 2), "launches": int(k), "GB/s": round(gbs, 1),
+            "frac": round(gbs / PEAK_HBM_GBS, 4)}
 
 
 def class_rooflines(cfg, per_kind, full_rows, packed_rows):
