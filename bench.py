@@ -81,12 +81,13 @@ def kernel_work(cfg, cls, rows_per_seq):
         return float(cfg.batch * (cfg.n_fut * d * esz + cfg.n_act * d * esz
                                   + cfg.n_act * cfg.n_heads * 4 + cfg.n_fut * 4))
     if cls == "PACK":
-        # the retained rows read once and written once
-        return 2.0 * m * d * esz
+        # the gather-pack fused into block 0's first LayerNorm: the retained
+        # rows read once, written once packed and once modulated
+        return 3.0 * m * d * esz
     if cls == "UNPACK":
-        # out of place (the step's y_full is not x_full): every row of y_full
-        # written once from its source, the packed row or the input row
-        return 2.0 * cfg.batch * cfg.l_full * d * esz
+        # the packed (retained) rows read once and scattered once; the pruned
+        # rows are copied on the side stream while the blocks run
+        return 2.0 * m * d * esz
     if cls == "QK_POST":
         # q and k of every row read and written once (the rotation table is L2-resident)
         return 4.0 * m * d * esz
@@ -238,8 +239,10 @@ def kernel_class(name):
     m = re.search(r"(?:gemm_bf16_nt|splitk_epilogue)<(\d+)", name)
     if m:
         return GEMM_CLASSES[int(m.group(1))]
+    if re.search(r"ln_mod_bf16<\d+, true>", name) or "pack_rows" in name:
+        return "PACK"
     for sub, cls in (("attn_fwd", "ATTN"), ("score_bf16", "SCORE"), ("score_f32", "SCORE"),
-                     ("pack_rows", "PACK"), ("unpack_", "UNPACK")):
+                     ("unpack_", "UNPACK")):
         if sub in name:
             return cls
     return None

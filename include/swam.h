@@ -29,7 +29,13 @@
  *   the cached scores/selection.  No call other than swam_create /
  *   swam_timer_enable allocates.
  * Streams: every call is asynchronous on the stream given to swam_create
- *   (or swam_set_stream).  Nothing synchronises except where stated:
+ *   (or swam_set_stream).  Inside a step the context also uses a second
+ *   stream of its own (default priority): a refresh scores each layer there
+ *   while the block continues, and an out-of-place sparse step copies the
+ *   pruned rows there while the blocks run; both are forked from and joined
+ *   back into the context stream with events (also under graph capture), so
+ *   a step's work is complete when the context stream's is.  Nothing
+ *   synchronises except where stated:
  *   swam_select / swam_step in mass-threshold mode and swam_set_selection read
  *   the packed lengths back to the host once; swam_timer_read synchronises.
  * Token layout: row-major [T][d].  One sequence is

@@ -72,17 +72,21 @@ hipError_t launch_adaln(int dtype, const AdalnArgs& a, int n_blk, const float* t
   return hipGetLastError();
 }
 
-// bf16 rows: 16-byte chunks of 8 elements, up to CH chunks per lane (d <= 512 CH)
-template <int CH>
+// bf16 rows: 16-byte chunks of 8 elements, up to CH chunks per lane (d <= 512 CH).
+// GATHER: output row r reads input row gather[r] and also stores it unchanged
+// to xp row r (the gather-pack of a sparse step fused into its first LN).
+template <int CH, bool GATHER>
 __global__ void __launch_bounds__(256)
 ln_mod_bf16(const bf16_t* __restrict__ x, bf16_t* __restrict__ h,
             const float* __restrict__ shift, const float* __restrict__ scale, int64_t rows,
-            int d) {
-  const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+            int d, const int32_t* __restrict__ gather, bf16_t* __restrict__ xp) {
+  const int64_t row =
+      (int64_t)blockIdx.x * 4 + __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
   const int lane = threadIdx.x & 63;
   if (row >= rows) return;
   const int nch = d >> 3;
-  const uint4* xr = (const uint4*)(x + row * d);
+  const int64_t src = GATHER ? (int64_t)gather[row] : row;
+  const uint4* xr = (const uint4*)(x + src * d);
   float v[CH][8];
   float s = 0.0f;
 #pragma unroll
@@ -90,6 +94,7 @@ ln_mod_bf16(const bf16_t* __restrict__ x, bf16_t* __restrict__ h,
     const int ci = lane + 64 * c;
     if (ci < nch) {
       const uint4 w = xr[ci];
+      if (GATHER) ((uint4*)(xp + row * d))[ci] = w;
       const uint32_t p[4] = {w.x, w.y, w.z, w.w};
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
@@ -127,16 +132,21 @@ ln_mod_bf16(const bf16_t* __restrict__ x, bf16_t* __restrict__ h,
   }
 }
 
-// fp32 rows: two passes over global memory (rows are L1/L2 resident)
+// fp32 rows: two passes over global memory (rows are L1/L2 resident);
+// gather != NULL: as the bf16 GATHER variant
 __global__ void __launch_bounds__(256)
 ln_mod_f32(const float* __restrict__ x, float* __restrict__ h, const float* __restrict__ shift,
-           const float* __restrict__ scale, int64_t rows, int d) {
+           const float* __restrict__ scale, int64_t rows, int d,
+           const int32_t* __restrict__ gather, float* __restrict__ xp) {
   const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
   if (row >= rows) return;
-  const float* xr = x + row * d;
+  const float* xr = x + (gather ? (int64_t)gather[row] : row) * d;
   float s = 0.0f;
-  for (int c = lane; c < d; c += 64) s += xr[c];
+  for (int c = lane; c < d; c += 64) {
+    s += xr[c];
+    if (gather) xp[row * d + c] = xr[c];
+  }
   const float mean = warp_sum(s) / d;
   float q = 0.0f;
   for (int c = lane; c < d; c += 64) { const float t = xr[c] - mean; q += t * t; }
@@ -145,25 +155,41 @@ ln_mod_f32(const float* __restrict__ x, float* __restrict__ h, const float* __re
     h[row * d + c] = (xr[c] - mean) * rstd * (1.0f + scale[c]) + shift[c];
 }
 
-hipError_t launch_ln_mod(int dtype, const void* x, void* h, const float* shift,
-                         const float* scale, int64_t rows, int d, hipStream_t st) {
+template <bool GATHER>
+static hipError_t ln_mod_any(int dtype, const void* x, void* h, const float* shift,
+                             const float* scale, int64_t rows, int d, const int32_t* gather,
+                             void* xp, hipStream_t st) {
   if (rows <= 0) return hipSuccess;
   dim3 grid((unsigned)((rows + 3) / 4));
   if (dtype == 1) {
+    const bf16_t* xb = (const bf16_t*)x;
+    bf16_t* hb = (bf16_t*)h;
+    bf16_t* pb = (bf16_t*)xp;
     if (d <= 1024)
-      hipLaunchKernelGGL(ln_mod_bf16<2>, grid, dim3(256), 0, st, (const bf16_t*)x, (bf16_t*)h,
-                         shift, scale, rows, d);
+      hipLaunchKernelGGL((ln_mod_bf16<2, GATHER>), grid, dim3(256), 0, st, xb, hb, shift, scale,
+                         rows, d, gather, pb);
     else if (d <= 2048)
-      hipLaunchKernelGGL(ln_mod_bf16<4>, grid, dim3(256), 0, st, (const bf16_t*)x, (bf16_t*)h,
-                         shift, scale, rows, d);
+      hipLaunchKernelGGL((ln_mod_bf16<4, GATHER>), grid, dim3(256), 0, st, xb, hb, shift, scale,
+                         rows, d, gather, pb);
     else
-      hipLaunchKernelGGL(ln_mod_bf16<8>, grid, dim3(256), 0, st, (const bf16_t*)x, (bf16_t*)h,
-                         shift, scale, rows, d);
+      hipLaunchKernelGGL((ln_mod_bf16<8, GATHER>), grid, dim3(256), 0, st, xb, hb, shift, scale,
+                         rows, d, gather, pb);
   } else {
     hipLaunchKernelGGL(ln_mod_f32, grid, dim3(256), 0, st, (const float*)x, (float*)h, shift,
-                       scale, rows, d);
+                       scale, rows, d, GATHER ? gather : nullptr, (float*)xp);
   }
   return hipGetLastError();
+}
+
+hipError_t launch_ln_mod(int dtype, const void* x, void* h, const float* shift,
+                         const float* scale, int64_t rows, int d, hipStream_t st) {
+  return ln_mod_any<false>(dtype, x, h, shift, scale, rows, d, nullptr, nullptr, st);
+}
+
+hipError_t launch_ln_mod_gather(int dtype, const void* x_full, const int32_t* gather, void* xp,
+                                void* h, const float* shift, const float* scale, int64_t rows,
+                                int d, hipStream_t st) {
+  return ln_mod_any<true>(dtype, x_full, h, shift, scale, rows, d, gather, xp, st);
 }
 
 // ---------------------------------------------------------------------------

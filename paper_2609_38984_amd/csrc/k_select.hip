@@ -580,7 +580,7 @@ __device__ __forceinline__ void copy_rows(const uint4* __restrict__ src_a,
     for (int i = 0; i < COPY_ROWS; ++i)
 #pragma unroll
       for (int k = 0; k < COPY_CH; ++k)
-        if (r0 + i < rows && c0 + 64 * k < cpr) dp[i][c0 + 64 * k] = v[i][k];
+        if (r0 + i < rows && dp[i] && c0 + 64 * k < cpr) dp[i][c0 + 64 * k] = v[i][k];
   }
 }
 
@@ -616,6 +616,20 @@ unpack_merge(const uint4* __restrict__ yp, const uint4* __restrict__ x, uint4* _
               const int32_t p = pack_pos[r];
               s_ = p >= 0 ? a + (int64_t)p * cpr_ : b + r * cpr_;
               d_ = d + r * cpr_;
+            });
+}
+
+// y row r = x row r for the pruned rows (pack_pos[r] < 0) only
+__global__ void __launch_bounds__(256)
+copy_pruned_rows(const uint4* __restrict__ x, uint4* __restrict__ y,
+                 const int32_t* __restrict__ pack_pos, int64_t rows, int cpr) {
+  copy_rows(x, nullptr, y, rows, cpr,
+            [pack_pos](int64_t r, const uint4* a, const uint4*, uint4* d, int cpr_,
+                       const uint4*& s_, uint4*& d_) {
+              // a retained row is loaded (in bounds) but not stored: its output
+              // row comes from the scatter of the packed rows
+              s_ = a + r * cpr_;
+              d_ = pack_pos[r] < 0 ? d + r * cpr_ : nullptr;
             });
 }
 
@@ -657,6 +671,15 @@ hipError_t launch_unpack_merge(const void* y_packed, const void* x_full, void* y
   hipLaunchKernelGGL(unpack_merge, dim3((unsigned)((rows + 4 * COPY_ROWS - 1) / (4 * COPY_ROWS))), dim3(256), 0, st,
                      (const uint4*)y_packed, (const uint4*)x_full, (uint4*)y_full, pack_pos,
                      rows, cpr);
+  return hipGetLastError();
+}
+
+hipError_t launch_copy_pruned(const void* x_full, void* y_full, const int32_t* pack_pos,
+                              int64_t rows, int64_t row_bytes, hipStream_t st) {
+  if (rows <= 0) return hipSuccess;
+  const int cpr = (int)(row_bytes / 16);
+  hipLaunchKernelGGL(copy_pruned_rows, dim3((unsigned)((rows + 4 * COPY_ROWS - 1) / (4 * COPY_ROWS))),
+                     dim3(256), 0, st, (const uint4*)x_full, (uint4*)y_full, pack_pos, rows, cpr);
   return hipGetLastError();
 }
 

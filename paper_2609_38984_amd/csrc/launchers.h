@@ -59,6 +59,11 @@ hipError_t launch_adaln(int dtype, const AdalnArgs& a, int n_blk, const float* t
 // h[r] = LN(x[r]) (1 + scale) + shift
 hipError_t launch_ln_mod(int dtype, const void* x, void* h, const float* shift,
                          const float* scale, int64_t rows, int d, hipStream_t st);
+// the same on gathered rows: xp[r] = x_full[gather[r]] (the gather-pack) and
+// h[r] = LN(xp[r]) (1 + scale) + shift, in one pass
+hipError_t launch_ln_mod_gather(int dtype, const void* x_full, const int32_t* gather, void* xp,
+                                void* h, const float* shift, const float* scale, int64_t rows,
+                                int d, hipStream_t st);
 
 // backbone variants: rotary table and QK-norm / RoPE of the stored q and k
 hipError_t launch_rope_table(float2* tab, int n_pos, hipStream_t st);
@@ -157,5 +162,8 @@ hipError_t launch_sample_update(const float* v, float* v_cache, float* z, const 
                                 int n_ctx, int n_fut, int c, int pairs, float guidance,
                                 hipStream_t st);
 hipError_t launch_copy(const void* src, void* dst, int64_t bytes, hipStream_t st);
+// y_full row r = x_full row r where pack_pos[r] < 0 (the pruned rows)
+hipError_t launch_copy_pruned(const void* x_full, void* y_full, const int32_t* pack_pos,
+                              int64_t rows, int64_t row_bytes, hipStream_t st);
 
 }  // namespace swam

@@ -191,7 +191,9 @@ struct swam_ctx {
   int32_t* host_cu = nullptr;   // pinned
   hipEvent_t order_ev = nullptr; // orders a newly bound stream after the previous one
   // a refresh scores layer l on `side` while the context stream runs the rest
-  // of block l; the next block's QKV projection waits for it (ev_score)
+  // of block l; the next block's QKV projection waits for it (ev_score).  An
+  // out-of-place sparse step copies the pruned rows on `side` during the
+  // blocks and joins it (ev_score) before the scatter of the packed rows.
   hipStream_t side = nullptr;
   hipEvent_t ev_attn = nullptr, ev_score = nullptr;
   bool score_pending = false;
@@ -281,9 +283,11 @@ bool bad_block(const swam_block_weights* w) {
 // selection (original positions), 2 = index inside the cu_seqlens sequence.
 // score (refresh only): this layer's action-to-future scores, launched right
 // after the attention while the layer's q, k and lambda are fresh in cache
+// pack_src (first block of a sparse step): x is filled from the gather-pack of
+// pack_src (the full latent) by the block's first LayerNorm kernel itself
 int run_block(swam_ctx* c, const swam_block_weights* w, const float* mod, void* x,
               int64_t n_rows, const int32_t* cu, int n_seqs, float* lse_out, void* qkv,
-              int pos_mode, const ScoreArgs* score = nullptr) {
+              int pos_mode, const ScoreArgs* score = nullptr, const void* pack_src = nullptr) {
   const int dt = c->cfg.dtype;
   const int64_t d = c->dv.d, hid = c->dv.hidden;
   void* h = c->ptr<char>(c->lay.h);
@@ -295,7 +299,11 @@ int run_block(swam_ctx* c, const swam_block_weights* w, const float* mod, void* 
   const float *sh1 = mod, *sc1 = mod + d, *g1 = mod + 2 * d;
   const float *sh2 = mod + 3 * d, *sc2 = mod + 4 * d, *g2 = mod + 5 * d;
   if (n_rows <= 0) return SWAM_OK;
-  {
+  if (pack_src) {
+    Timed t(c, SWAM_T_PACK);
+    SWAM_HIP(c, launch_ln_mod_gather(dt, pack_src, c->ptr<int32_t>(c->lay.gather), x, h, sh1, sc1,
+                                     n_rows, (int)d, st), "pack + ln_mod");
+  } else {
     Timed t(c, SWAM_T_LNMOD);
     SWAM_HIP(c, launch_ln_mod(dt, x, h, sh1, sc1, n_rows, (int)d, st), "ln_mod");
   }
@@ -962,14 +970,35 @@ int enqueue_step(swam_ctx* c, const swam_model* model, const void* x_full, const
         return rc;
     }
   } else {
+    // out of place, the pruned rows of y_full are x_full's whatever the blocks
+    // compute: they are copied on the side stream while the blocks run
+    const int64_t rb = d * c->dv.esz;
+    const bool fork = y_full != x_full;
+    if (fork) {
+      SWAM_HIP(c, hipEventRecord(c->ev_attn, c->st), "fork pruned-row copy");
+      SWAM_HIP(c, hipStreamWaitEvent(c->side, c->ev_attn, 0), "fork pruned-row copy");
+      {
+        Timed t(c, SWAM_T_COPY, c->side);
+        SWAM_HIP(c, launch_copy_pruned(x_full, y_full, c->ptr<int32_t>(c->lay.pack_pos),
+                                       c->dv.rows_full, rb, c->side), "pruned-row copy");
+      }
+      SWAM_HIP(c, hipEventRecord(c->ev_score, c->side), "pruned-row copy done");
+    }
+    // the gather-pack of x_full runs inside block 0's first LayerNorm kernel
     void* xp = c->ptr<char>(c->lay.xp);
-    if ((rc = swam_pack(c, x_full, xp)) != SWAM_OK) return rc;
     for (int l = 0; l < cf.n_blocks; ++l) {
       rc = run_block(c, &model->blocks[l], mod + (int64_t)l * 6 * d, xp, c->packed_rows,
-                     c->ptr<int32_t>(c->lay.cu_packed), cf.batch, nullptr, qkv, 1);
+                     c->ptr<int32_t>(c->lay.cu_packed), cf.batch, nullptr, qkv, 1, nullptr,
+                     l == 0 ? x_full : nullptr);
       if (rc != SWAM_OK) return rc;
     }
-    if ((rc = swam_unpack(c, xp, x_full, y_full)) != SWAM_OK) return rc;
+    if (fork) SWAM_HIP(c, hipStreamWaitEvent(c->st, c->ev_score, 0), "join pruned-row copy");
+    {
+      // scatter of the packed rows (the retained ones) into y_full
+      Timed t(c, SWAM_T_UNPACK);
+      SWAM_HIP(c, launch_unpack_scatter(xp, y_full, c->ptr<int32_t>(c->lay.gather),
+                                        c->packed_rows, rb, c->st), "unpack");
+    }
   }
   return SWAM_OK;
 }
