@@ -88,12 +88,12 @@ def test_variant_block_fp32_ragged():
 
 def test_variant_block_bf16_ragged_tails():
     cfg = _small_bf16(batch=4, rope=1, qk_norm=1)
-    _block_case(cfg, np.array([0, 37, 37, 237, 366, 367]), 2e-2, 5e-2)
+    _block_case(cfg, np.array([0, 37, 37, 237, 366, 367]), 2e-2, 1e-2)
 
 
 def test_variant_block_bf16_dense_layout():
     cfg = _small_bf16(batch=2, rope=1, qk_norm=1)
-    _block_case(cfg, O.dense_cu(cfg), 2e-2, 5e-2, dense_layout=True)
+    _block_case(cfg, O.dense_cu(cfg), 2e-2, 1e-2, dense_layout=True)
 
 
 @pytest.mark.parametrize("rope,qk_norm", [(1, 0), (1, 1)])
@@ -182,4 +182,4 @@ def test_variant_block_wam_packed_sampled():
     e_y = maxrel(host(xd)[rows], y_ref)
     e_l = float(np.abs(host(lse)[rows] - l_ref).max())
     print(f"  sampled {len(rows)} rows: y max-rel {e_y:.2e}, lambda abs {e_l:.2e}", flush=True)
-    assert e_y < 2e-2 and e_l < 5e-2
+    assert e_y < 2e-2 and e_l < 1e-2
