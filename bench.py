@@ -626,9 +626,10 @@ def sweep(args):
     rows = []
     head = ("| workload | retention | R | packed rows | dense ms | refresh ms | sparse ms | "
             "schedule ms/step | sparse/dense | schedule/dense | score+pack % of dense | "
-            "dominant kernel | MFMA frac | graph dense ms | graph sparse ms | graph schedule ms/step |")
+            "exposed % of dense | dominant kernel | MFMA frac | graph dense ms | graph sparse ms | "
+            "graph schedule ms/step |")
     print(head)
-    print("|" + "---|" * 16)
+    print("|" + "---|" * 17)
 
     def emit(cfg, ret, m, model, xs, tembs):
         g = measure_graph(cfg, model, xs, tembs, cfg.n_steps, args.sweep_reps)
@@ -636,7 +637,8 @@ def sweep(args):
         line = (f"| {cfg.name} | {ret} | {cfg.reuse_R} | {m['packed_rows']} | {m['dense_step_ms']:.2f} | "
                 f"{m['refresh_step_ms']:.2f} | {m['sparse_step_ms']:.2f} | {m['schedule_step_ms']:.2f} | "
                 f"{m['speedup_sparse_vs_dense']} | {m['speedup_schedule_vs_dense']} | "
-                f"{m['overhead_pct_of_dense']:.3f} | {rf['kernel']} | {rf['frac']:.3f} | "
+                f"{m['overhead_pct_of_dense']:.3f} | {m['overhead_exposed_pct_of_dense']:.3f} | "
+                f"{rf['kernel']} | {rf['frac']:.3f} | "
                 f"{g['dense_step_ms']:.3f} | {g['sparse_step_ms']:.3f} | {g['schedule_step_ms']:.3f} |")
         print(line, flush=True)
 

@@ -2,13 +2,16 @@
 //
 // Reduction (layer quality, core layers, core score V, anchor key A) sums in
 // float64 in a fixed order and rounds once to float32.
-// Selection sorts composite 64-bit keys in LDS with a bitonic network:
+// Selection orders positions by the composite key
 //   key = (~ord(score) << 32) | index
 // where ord() maps float bits to an order-preserving uint32 (signed zeros
 // merged), so ascending keys are score-descending with the lowest index first
-// on ties: every top-k is deterministic and bit-exact.  Non-candidates get
-// the all-ones key.  The mass-threshold count uses exact integer codes
-// floor(V 2^40) with a uint64 prefix scan.
+// on ties: every top-k is deterministic and bit-exact.  Fixed budgets take
+// the first k keys by a radix select (8-bit digit histograms of ~ord in LDS,
+// ties at the k-th value resolved lowest index first); the mass threshold,
+// which walks the pool in that order, sorts the keys in LDS with a bitonic
+// network and counts with exact integer codes floor(V 2^40) and a uint64
+// prefix scan.
 // Packing is an exclusive prefix sum of keep flags in original token order;
 // pack is a coalesced 16-byte row gather, unpack the matching scatter.
 #include "launchers.h"
@@ -95,6 +98,87 @@ __device__ __forceinline__ int next_pow2(int n) {
   int p = 1;
   while (p < n) p <<= 1;
   return p;
+}
+
+// ---------------------------------------------------------------------------
+// block-wide top-k by radix select (blockDim.x == SEL_THREADS)
+// ---------------------------------------------------------------------------
+constexpr int SEL_EPT = SWAM_SEL_MAXNP / SEL_THREADS;   // positions per thread
+
+struct SelScratch {
+  uint32_t hist[256];
+  int ws[SEL_THREADS / 64 + 1];
+  int pick[2];
+};
+
+// Thread t owns positions [t * SEL_EPT, (t + 1) * SEL_EPT).  Among the
+// candidate positions, sel[] marks the k that come first in the order (ok
+// ascending, then position ascending), where ok = ~float_order(score) puts
+// higher scores first: the same set as sorting the composite keys
+// (ok << 32 | j) and taking the first k.  Four passes of 8-bit digit
+// histograms (LDS atomics) narrow down the ok value of the k-th key; its
+// ties are then taken lowest position first by an exclusive scan in
+// position order.
+__device__ void block_topk(const uint32_t (&ok)[SEL_EPT], const bool (&cand)[SEL_EPT], int k,
+                           bool (&sel)[SEL_EPT], SelScratch& sc) {
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  int mine = 0;
+#pragma unroll
+  for (int e = 0; e < SEL_EPT; ++e) mine += cand[e];
+  int total;
+  block_excl_scan(mine, sc.ws, &total);
+  if (k >= total || k <= 0) {
+#pragma unroll
+    for (int e = 0; e < SEL_EPT; ++e) sel[e] = k > 0 && cand[e];
+    return;
+  }
+  uint32_t prefix = 0, pmask = 0;
+  int need = k;                                 // keys still to take at or after `prefix`
+  for (int shift = 24; shift >= 0; shift -= 8) {
+    for (int i = tid; i < 256; i += blockDim.x) sc.hist[i] = 0;
+    __syncthreads();
+#pragma unroll
+    for (int e = 0; e < SEL_EPT; ++e)
+      if (cand[e] && (ok[e] & pmask) == prefix) atomicAdd(&sc.hist[(ok[e] >> shift) & 255u], 1u);
+    __syncthreads();
+    if (wave == 0) {
+      // the digit bucket that holds the need-th key: scan of the 256 counts
+      uint32_t c[4], s = 0;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) { c[q] = sc.hist[4 * lane + q]; s += c[q]; }
+      uint32_t x = s;
+#pragma unroll
+      for (int o = 1; o < 64; o <<= 1) {
+        const uint32_t y = __shfl_up(x, o);
+        if (lane >= o) x += y;
+      }
+      const uint32_t before = x - s;
+      if (before < (uint32_t)need && (uint32_t)need <= x) {
+        uint32_t run = before;
+        int q = 0;
+        while (run + c[q] < (uint32_t)need) run += c[q++];
+        sc.pick[0] = 4 * lane + q;
+        sc.pick[1] = (int)run;
+      }
+    }
+    __syncthreads();
+    prefix |= (uint32_t)sc.pick[0] << shift;
+    pmask |= 255u << shift;
+    need -= sc.pick[1];
+    __syncthreads();                            // pick is rewritten by the next pass
+  }
+  // prefix is now the k-th key's ok value; take `need` of its ties
+  int t = 0;
+#pragma unroll
+  for (int e = 0; e < SEL_EPT; ++e) t += cand[e] && ok[e] == prefix;
+  int tt;
+  int rank = block_excl_scan(t, sc.ws, &tt);
+#pragma unroll
+  for (int e = 0; e < SEL_EPT; ++e) {
+    const bool tie = cand[e] && ok[e] == prefix;
+    sel[e] = cand[e] && (ok[e] < prefix || (tie && rank < need));
+    rank += tie;
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -300,24 +384,27 @@ hipError_t launch_score_reduce(const ReduceArgs& a, hipStream_t st) {
 __global__ void __launch_bounds__(SEL_THREADS)
 select_pool(const float* __restrict__ v, int F, int n_s, int k_anchor,
             uint8_t* __restrict__ pool) {
-  __shared__ uint64_t keys[SWAM_SEL_MAXNP];
+  __shared__ SelScratch sc;
   const int b = blockIdx.x;
-  const int np = next_pow2(n_s);
   const float* vb = v + (int64_t)b * F * n_s;
-  for (int j = threadIdx.x; j < np; j += blockDim.x) {
-    uint64_t key = ~0ull;
-    if (j < n_s) {
+  uint32_t ok[SEL_EPT];
+  bool cand[SEL_EPT], sel[SEL_EPT];
+  const int j0 = threadIdx.x * SEL_EPT;
+#pragma unroll
+  for (int e = 0; e < SEL_EPT; ++e) {
+    const int j = j0 + e;
+    cand[e] = j < n_s;
+    ok[e] = ~0u;
+    if (cand[e]) {
       float m = vb[j];
       for (int f = 1; f < F; ++f) m = fmaxf(m, vb[(int64_t)f * n_s + j]);
-      key = sel_key(m, j);
-      pool[(int64_t)b * n_s + j] = 0;
+      ok[e] = ~float_order(m);
     }
-    keys[j] = key;
   }
-  __syncthreads();
-  bitonic_sort(keys, np);
-  for (int r = threadIdx.x; r < n_s - k_anchor; r += blockDim.x)
-    pool[(int64_t)b * n_s + (int)(keys[r] & 0xFFFFFFFFu)] = 1;
+  block_topk(ok, cand, n_s - k_anchor, sel, sc);
+#pragma unroll
+  for (int e = 0; e < SEL_EPT; ++e)
+    if (j0 + e < n_s) pool[(int64_t)b * n_s + j0 + e] = sel[e];
 }
 
 __device__ __forceinline__ uint64_t mass_code(float x) {
@@ -341,12 +428,32 @@ select_core(const float* __restrict__ v, const uint8_t* __restrict__ pool, int F
   __shared__ uint64_t keys[SWAM_SEL_MAXNP];
   __shared__ uint64_t ws64[SEL_THREADS / 64 + 1];
   __shared__ int fails;
+  __shared__ SelScratch sc;
   const int bf = blockIdx.x;               // b * F + f
   const int b = bf / F;
   const int np = next_pow2(n_s);
   const float* vr = v + (int64_t)bf * n_s;
   const uint8_t* pb = pool + (int64_t)b * n_s;
   uint8_t* cr = core + (int64_t)bf * n_s;
+  if (mass_den == 0) {
+    // fixed budget: the top K_c of the pool by radix select
+    uint32_t ok[SEL_EPT];
+    bool cand[SEL_EPT], sel[SEL_EPT];
+    const int j0 = threadIdx.x * SEL_EPT;
+#pragma unroll
+    for (int e = 0; e < SEL_EPT; ++e) {
+      const int j = j0 + e;
+      cand[e] = j < n_s && pb[j];
+      ok[e] = cand[e] ? ~float_order(vr[j]) : ~0u;
+    }
+    block_topk(ok, cand, k_core, sel, sc);
+#pragma unroll
+    for (int e = 0; e < SEL_EPT; ++e)
+      if (j0 + e < n_s) cr[j0 + e] = sel[e];
+    if (threadIdx.x == 0) kcount[bf] = min(k_core, n_s - k_anchor);
+    return;
+  }
+  // mass threshold: the pool in TopK order (full sort), walked with the codes
   for (int j = threadIdx.x; j < np; j += blockDim.x) {
     uint64_t key = ~0ull;
     if (j < n_s) {
@@ -393,45 +500,51 @@ select_anchor(const float* __restrict__ a, const uint8_t* __restrict__ core, int
               int k_anchor, int k_max, int n_ctx, int n_act, int64_t l_full,
               int32_t* __restrict__ keep_idx, int32_t* __restrict__ keep_cnt,
               int32_t* __restrict__ keep) {
-  __shared__ uint64_t keys[SWAM_SEL_MAXNP];
+  __shared__ SelScratch sc;
   __shared__ uint8_t anchor[SWAM_MAX_NS_DEV];
-  __shared__ int ws[SEL_THREADS / 64 + 1];
   const int b = blockIdx.x;
-  const int np = next_pow2(n_s);
   const uint8_t* cb = core + (int64_t)b * F * n_s;
-  for (int j = threadIdx.x; j < np; j += blockDim.x) {
-    uint64_t key = ~0ull;
-    if (j < n_s) {
-      bool used = false;
-      for (int f = 0; f < F; ++f) used |= cb[(int64_t)f * n_s + j] != 0;
-      if (!used) key = sel_key(a[(int64_t)b * n_s + j], j);
-      anchor[j] = 0;
+  {
+    // anchors: the top K_s of A over the positions no frame's core took
+    uint32_t ok[SEL_EPT];
+    bool cand[SEL_EPT], sel[SEL_EPT];
+    const int j0 = threadIdx.x * SEL_EPT;
+#pragma unroll
+    for (int e = 0; e < SEL_EPT; ++e) {
+      const int j = j0 + e;
+      bool used = j >= n_s;
+      for (int f = 0; f < F && !used; ++f) used |= cb[(int64_t)f * n_s + j] != 0;
+      cand[e] = !used;
+      ok[e] = cand[e] ? ~float_order(a[(int64_t)b * n_s + j]) : ~0u;
     }
-    keys[j] = key;
+    block_topk(ok, cand, k_anchor, sel, sc);
+#pragma unroll
+    for (int e = 0; e < SEL_EPT; ++e)
+      if (j0 + e < n_s) anchor[j0 + e] = sel[e];
   }
-  __syncthreads();
-  bitonic_sort(keys, np);
-  for (int r = threadIdx.x; r < k_anchor; r += blockDim.x) anchor[(int)(keys[r] & 0xFFFFFFFFu)] = 1;
   __syncthreads();
   int32_t* kb = keep + (int64_t)b * l_full;
   for (int64_t t = threadIdx.x; t < n_ctx; t += blockDim.x) kb[t] = 1;
   for (int64_t t = threadIdx.x; t < n_act; t += blockDim.x) kb[l_full - n_act + t] = 1;
-  const int ept = (n_s + blockDim.x - 1) / blockDim.x;
-  for (int f = 0; f < F; ++f) {
+  // retained set of each frame (core or anchor), in position order: one wave
+  // per frame, 64 positions per round compacted by ballot + lane prefix count
+  const int lane = threadIdx.x & 63, nw = blockDim.x >> 6;
+  for (int f = threadIdx.x >> 6; f < F; f += nw) {
     const uint8_t* cf = cb + (int64_t)f * n_s;
-    const int j0 = threadIdx.x * ept;
-    int cnt = 0;
-    for (int j = j0; j < min(j0 + ept, n_s); ++j) cnt += (cf[j] | anchor[j]) != 0;
-    int total;
-    int pos = block_excl_scan(cnt, ws, &total);
     int32_t* out = keep_idx + ((int64_t)b * F + f) * k_max;
-    for (int j = j0; j < min(j0 + ept, n_s); ++j) {
-      const int kf = (cf[j] | anchor[j]) != 0;
-      kb[n_ctx + (int64_t)f * n_s + j] = kf;
-      if (kf) out[pos++] = j;
+    int32_t* kf_out = kb + n_ctx + (int64_t)f * n_s;
+    int total = 0;
+    for (int j0 = 0; j0 < n_s; j0 += 64) {
+      const int j = j0 + lane;
+      const bool kf = j < n_s && (cf[j] | anchor[j]) != 0;
+      if (j < n_s) kf_out[j] = kf;
+      const uint64_t bal = __ballot(kf);
+      if (kf) out[total + (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(bal >> 32),
+                                  __builtin_amdgcn_mbcnt_lo((uint32_t)bal, 0u))] = j;
+      total += __popcll(bal);
     }
-    for (int r = total + threadIdx.x; r < k_max; r += blockDim.x) out[r] = -1;
-    if (threadIdx.x == 0) keep_cnt[b * F + f] = total;
+    for (int r = total + lane; r < k_max; r += 64) out[r] = -1;
+    if (lane == 0) keep_cnt[b * F + f] = total;
   }
 }
 
