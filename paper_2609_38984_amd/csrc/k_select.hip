@@ -807,11 +807,14 @@ hipError_t launch_copy(const void* src, void* dst, int64_t bytes, hipStream_t st
 // Random-selection baseline: one Philox4x64-10 evaluation (Salmon et al.,
 // SC 2011: ten rounds of two 64x64 -> 128-bit products crossed with the other
 // two words and a Weyl-stepped key) per (sequence, frame, position); the
-// selection then takes the largest keys per frame.
+// selection then takes the largest keys per frame.  The same threads clear
+// the n_a anchor keys (n_a <= n), so every anchor ties at zero.
 __global__ void __launch_bounds__(256)
-random_keys_kernel(float* __restrict__ v, int64_t n, uint64_t seed) {
+random_keys_kernel(float* __restrict__ v, int64_t n, float* __restrict__ a, int64_t n_a,
+                   uint64_t seed) {
   const int64_t id = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (id >= n) return;
+  if (id < n_a) a[id] = 0.0f;
   uint64_t x0 = (uint64_t)id, x1 = 0, x2 = 0, x3 = 0, k0 = seed, k1 = 0;
 #pragma unroll
   for (int r = 0; r < 10; ++r) {
@@ -827,10 +830,11 @@ random_keys_kernel(float* __restrict__ v, int64_t n, uint64_t seed) {
   v[id] = (float)(uint32_t)(x0 >> 40) * 0x1p-24f;
 }
 
-hipError_t launch_random_keys(float* v, int64_t n, uint64_t seed, hipStream_t st) {
-  if (n <= 0) return hipSuccess;
+hipError_t launch_random_keys(float* v, int64_t n, float* a, int64_t n_a, uint64_t seed,
+                              hipStream_t st) {
+  if (n <= 0 || n_a > n) return n_a > n ? hipErrorInvalidValue : hipSuccess;
   hipLaunchKernelGGL(random_keys_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, v, n,
-                     seed);
+                     a, n_a, seed);
   return hipGetLastError();
 }
 

@@ -127,8 +127,10 @@ struct SelectArgs {
 };
 hipError_t launch_select(const SelectArgs& a, hipStream_t st);
 // uniform keys in [0, 1) (top 24 bits of word 0 of Philox4x64-10 at counter
-// (i, 0, 0, 0), key (seed, 0)) for i < n
-hipError_t launch_random_keys(float* v, int64_t n, uint64_t seed, hipStream_t st);
+// (i, 0, 0, 0), key (seed, 0)) into v[i] for i < n, and zeros into a[n_a]
+// (n_a <= n)
+hipError_t launch_random_keys(float* v, int64_t n, float* a, int64_t n_a, uint64_t seed,
+                              hipStream_t st);
 // keep flags from an imported selection; rewrites keep_idx / keep_cnt ascending
 hipError_t launch_keep_from_idx(const int32_t* in_idx, int32_t* keep_idx, int32_t* keep_cnt,
                                 int32_t* keep, int B, int F, int n_s, int k_max, int n_ctx,

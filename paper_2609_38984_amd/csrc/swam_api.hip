@@ -678,9 +678,9 @@ int swam_select_random(swam_ctx* c, uint64_t seed, int32_t* keep_idx, int32_t* k
   const int64_t n = c->dv.n_scored * cf.n_frames * c->dv.n_s;
   {
     Timed t(c, SWAM_T_SELECT);
-    SWAM_HIP(c, launch_random_keys(c->ptr<float>(c->lay.v), n, seed, c->st), "random keys");
-    SWAM_HIP(c, hipMemsetAsync(c->ptr<float>(c->lay.a), 0, c->dv.n_scored * c->dv.n_s * 4, c->st),
-             "clear anchor keys");
+    SWAM_HIP(c, launch_random_keys(c->ptr<float>(c->lay.v), n, c->ptr<float>(c->lay.a),
+                                   c->dv.n_scored * c->dv.n_s, seed, c->st),
+             "random keys");
   }
   int rc = run_select(c, c->ptr<float>(c->lay.v), c->ptr<float>(c->lay.a),
                       cf.k_core + cf.k_anchor, 0);

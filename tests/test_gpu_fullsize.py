@@ -85,13 +85,22 @@ def test_block_ragged_batch_sampled():
 
 def test_block_2048_packed_3744_sampled():
     """The packed sequence of the d = 2048 workload at 10% + 64 retention
-    (3,744 rows, 32 heads): the shape that runs the 4-wave attention kernel
-    at four waves per SIMD, the 128x128 QKV tile and the down projection
-    split along K in two."""
+    (3,744 rows, 32 heads): 480 attention workgroups of 8 waves, the 128x128
+    QKV tile and the down projection split along K in two."""
     cfg = W.preset(4, percent=10).replace(n_blocks=1)
     assert cfg.t_pack_fixed == 3744
     x = W.make_inputs(cfg, W.block_weights(cfg, 0)["w_qkv"]).x(0)
     _sampled_block(cfg, np.array([0, cfg.t_pack_fixed]), x, per_seq=24)
+
+
+def test_block_wam_packed_4200_sampled():
+    """4,200 packed rows of the WAM width (24 heads): the 4-wave attention
+    kernel with its four-waves-per-SIMD register cap (33 query tiles per head,
+    too few for the 8-wave kernel), the 128x128 QKV tile and the down
+    projection split along K in two."""
+    cfg = W.preset(3)
+    x = W.make_inputs(cfg, W.block_weights(cfg, 0)["w_qkv"]).x(0)
+    _sampled_block(cfg, np.array([0, 4200]), x)
 
 
 def test_block_2048_dense_sampled():
