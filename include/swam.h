@@ -343,7 +343,9 @@ int swam_block(swam_ctx* ctx, const swam_block_weights* w, const float* temb, vo
 #define SWAM_KIND_REFRESH 1
 #define SWAM_KIND_SPARSE 2
 
-/* One denoising step x_full [B*l_full][d] -> y_full (may alias x_full).
+/* One denoising step x_full [B*l_full][d] -> y_full.  y_full is either
+ * x_full itself (in place) or a buffer disjoint from it; a partial overlap
+ * returns SWAM_E_INVALID.
  * Refresh (tau mod R == 0 or FORCE_REFRESH): dense blocks with scoring of
  * every layer, then score reduce, selection and packing metadata, cached.
  * Sparse: pack -> blocks on the packed sequences -> unpack; pruned rows of

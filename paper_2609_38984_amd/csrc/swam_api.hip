@@ -907,6 +907,14 @@ int check_step(swam_ctx* c, const swam_model* model, const void* x_full, const f
   if (!x_full || !y_full || !temb) return set_err(c, SWAM_E_INVALID, "NULL tensor");
   if (!aligned16(x_full) || !aligned16(y_full))
     return set_err(c, SWAM_E_INVALID, "x_full and y_full must be 16-byte aligned");
+  {
+    // y_full is x_full itself or a disjoint buffer: the pruned rows are copied
+    // and the retained ones scattered assuming one of the two
+    const uintptr_t xa = (uintptr_t)x_full, ya = (uintptr_t)y_full;
+    const uintptr_t nb = (uintptr_t)(c->dv.rows_full * c->dv.d * c->dv.esz);
+    if (xa != ya && xa < ya + nb && ya < xa + nb)
+      return set_err(c, SWAM_E_INVALID, "y_full must be x_full itself or not overlap it");
+  }
   if (tau < 0) return set_err(c, SWAM_E_INVALID, "tau < 0");
   if (flags & SWAM_STEP_FORCE_DENSE) *kind = SWAM_KIND_DENSE;
   else if ((flags & SWAM_STEP_FORCE_REFRESH) || tau % cf.reuse_R == 0) *kind = SWAM_KIND_REFRESH;

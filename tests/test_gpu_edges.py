@@ -99,3 +99,24 @@ def test_misaligned_tensors_are_rejected_before_any_launch():
     assert e.value.code == -1 and "aligned" in str(e.value)
     torch.cuda.synchronize()
     assert bool((buf == 0).all())
+
+
+def test_partially_overlapping_output_is_rejected():
+    """y_full is x_full itself or disjoint from it (the pruned rows are copied
+    and the retained ones scattered on that assumption): an output a few rows
+    into the input must come back as SWAM_E_INVALID with nothing written."""
+    from paper_2609_38984_amd import swam
+    cfg = BASE
+    _, _, model = model_for(cfg)
+    ctx = swam.Context(cfg)
+    n = cfg.l_full * cfg.d_model
+    buf = torch.zeros(n + 4 * cfg.d_model, dtype=torch.float32, device="cuda:0")
+    x = buf[:n].view(cfg.l_full, cfg.d_model)
+    y = buf[4 * cfg.d_model:].view(cfg.l_full, cfg.d_model)
+    temb = dev(W.timestep_embedding(cfg, 0))
+    for a, b in ((x, y), (y, x)):
+        with pytest.raises(swam.SwamError) as e:
+            ctx.step(model, a, temb, 0, b)
+        assert e.value.code == -1 and "overlap" in str(e.value)
+    torch.cuda.synchronize()
+    assert bool((buf == 0).all())
