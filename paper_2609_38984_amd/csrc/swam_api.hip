@@ -266,6 +266,21 @@ int join_score(swam_ctx* c) {
   return SWAM_OK;
 }
 
+// out-of-place sparse step: the pruned rows of y_full are x_full's whatever
+// the blocks compute, so they are copied on the side stream while the blocks
+// run; the scatter of the packed rows waits for it (ev_score)
+int fork_pruned_copy(swam_ctx* c, const void* x_full, void* y_full) {
+  SWAM_HIP(c, hipEventRecord(c->ev_attn, c->st), "fork pruned-row copy");
+  SWAM_HIP(c, hipStreamWaitEvent(c->side, c->ev_attn, 0), "fork pruned-row copy");
+  {
+    Timed t(c, SWAM_T_COPY, c->side);
+    SWAM_HIP(c, launch_copy_pruned(x_full, y_full, c->ptr<int32_t>(c->lay.pack_pos),
+                                   c->dv.rows_full, c->dv.d * c->dv.esz, c->side), "pruned-row copy");
+  }
+  SWAM_HIP(c, hipEventRecord(c->ev_score, c->side), "pruned-row copy done");
+  return SWAM_OK;
+}
+
 bool aligned16(const void* p) { return ((uintptr_t)p & 15) == 0; }
 
 // NULL or not 16-byte aligned (the kernels read weights in 16-byte vectors)
@@ -284,10 +299,14 @@ bool bad_block(const swam_block_weights* w) {
 // score (refresh only): this layer's action-to-future scores, launched right
 // after the attention while the layer's q, k and lambda are fresh in cache
 // pack_src (first block of a sparse step): x is filled from the gather-pack of
-// pack_src (the full latent) by the block's first LayerNorm kernel itself
+// pack_src (the full latent) by the block's first LayerNorm kernel itself;
+// pruned_dst (with pack_src, out of place): the pruned rows of pack_src are
+// copied into it on the side stream, forked after that LayerNorm so the copy
+// overlaps the QKV projection rather than the pack
 int run_block(swam_ctx* c, const swam_block_weights* w, const float* mod, void* x,
               int64_t n_rows, const int32_t* cu, int n_seqs, float* lse_out, void* qkv,
-              int pos_mode, const ScoreArgs* score = nullptr, const void* pack_src = nullptr) {
+              int pos_mode, const ScoreArgs* score = nullptr, const void* pack_src = nullptr,
+              void* pruned_dst = nullptr) {
   const int dt = c->cfg.dtype;
   const int64_t d = c->dv.d, hid = c->dv.hidden;
   void* h = c->ptr<char>(c->lay.h);
@@ -300,9 +319,13 @@ int run_block(swam_ctx* c, const swam_block_weights* w, const float* mod, void* 
   const float *sh2 = mod + 3 * d, *sc2 = mod + 4 * d, *g2 = mod + 5 * d;
   if (n_rows <= 0) return SWAM_OK;
   if (pack_src) {
-    Timed t(c, SWAM_T_PACK);
-    SWAM_HIP(c, launch_ln_mod_gather(dt, pack_src, c->ptr<int32_t>(c->lay.gather), x, h, sh1, sc1,
-                                     n_rows, (int)d, st), "pack + ln_mod");
+    {
+      Timed t(c, SWAM_T_PACK);
+      SWAM_HIP(c, launch_ln_mod_gather(dt, pack_src, c->ptr<int32_t>(c->lay.gather), x, h, sh1,
+                                       sc1, n_rows, (int)d, st), "pack + ln_mod");
+    }
+    if (pruned_dst)
+      if (int rc = fork_pruned_copy(c, pack_src, pruned_dst)) return rc;
   } else {
     Timed t(c, SWAM_T_LNMOD);
     SWAM_HIP(c, launch_ln_mod(dt, x, h, sh1, sc1, n_rows, (int)d, st), "ln_mod");
@@ -978,26 +1001,18 @@ int enqueue_step(swam_ctx* c, const swam_model* model, const void* x_full, const
         return rc;
     }
   } else {
-    // out of place, the pruned rows of y_full are x_full's whatever the blocks
-    // compute: they are copied on the side stream while the blocks run
+    // out of place, the pruned rows are copied on the side stream (forked
+    // inside block 0 after the pack, or here when no row is retained)
     const int64_t rb = d * c->dv.esz;
     const bool fork = y_full != x_full;
-    if (fork) {
-      SWAM_HIP(c, hipEventRecord(c->ev_attn, c->st), "fork pruned-row copy");
-      SWAM_HIP(c, hipStreamWaitEvent(c->side, c->ev_attn, 0), "fork pruned-row copy");
-      {
-        Timed t(c, SWAM_T_COPY, c->side);
-        SWAM_HIP(c, launch_copy_pruned(x_full, y_full, c->ptr<int32_t>(c->lay.pack_pos),
-                                       c->dv.rows_full, rb, c->side), "pruned-row copy");
-      }
-      SWAM_HIP(c, hipEventRecord(c->ev_score, c->side), "pruned-row copy done");
-    }
+    if (fork && c->packed_rows <= 0)
+      if ((rc = fork_pruned_copy(c, x_full, y_full)) != SWAM_OK) return rc;
     // the gather-pack of x_full runs inside block 0's first LayerNorm kernel
     void* xp = c->ptr<char>(c->lay.xp);
     for (int l = 0; l < cf.n_blocks; ++l) {
       rc = run_block(c, &model->blocks[l], mod + (int64_t)l * 6 * d, xp, c->packed_rows,
                      c->ptr<int32_t>(c->lay.cu_packed), cf.batch, nullptr, qkv, 1, nullptr,
-                     l == 0 ? x_full : nullptr);
+                     l == 0 ? x_full : nullptr, l == 0 && fork ? y_full : nullptr);
       if (rc != SWAM_OK) return rc;
     }
     if (fork) SWAM_HIP(c, hipStreamWaitEvent(c->st, c->ev_score, 0), "join pruned-row copy");
