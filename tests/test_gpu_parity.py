@@ -203,7 +203,7 @@ def _select_case(cfg, seed, ties=False):
     print(f"select case {cfg.name} seed {seed} ties {ties}", flush=True)
     rng = np.random.default_rng(seed)
     S = _random_scores(rng, cfg.batch, cfg.n_blocks, cfg.n_frames, cfg.n_s, ties)
-    Vs, As, sels = [], [], []
+    Vs, As = [], []
     for b in range(cfg.batch):
         r = O.score_reduce(S[b], cfg.k_layer, cfg.cv_penalty)
         V, A = r.V.astype(np.float32), r.A.astype(np.float32)
@@ -212,7 +212,13 @@ def _select_case(cfg, seed, ties=False):
             A = np.floor(A * 64) / 64
         Vs.append(V)
         As.append(A)
-        sels.append(O.select(V, A, cfg.k_core, cfg.k_anchor, cfg.mass_threshold))
+    _select_given(cfg, Vs, As)
+
+
+def _select_given(cfg, Vs, As):
+    """swam_select on the given fp32 V [B][F][N_s] and A [B][N_s] against the
+    oracle's selection and pack map, bit for bit."""
+    sels = [O.select(V, A, cfg.k_core, cfg.k_anchor, cfg.mass_threshold) for V, A in zip(Vs, As)]
     pm = O.pack_map(O.keep_mask(cfg, [s.retained for s in sels]), cfg.batch)
     ctx = _ctx(cfg)
     kmax = ctx.k_max
@@ -249,6 +255,50 @@ def test_select_bitexact_retention_sweep(pct):
 
 def test_select_bitexact_heavy_ties():
     _select_case(W.preset(2).replace(n_blocks=2), 71, ties=True)
+
+
+def _adversarial(rng, shape, kind):
+    """fp32 keys built against the radix select's digit passes: values within
+    300 ulps of 1 (every candidate shares the top 16 bits, so the k-th key is
+    found in the last bytes), a mix of signs, signed zeros, subnormals, powers
+    of two and the extremes, and a plateau of one value spanning the k-th rank
+    (its ties are taken lowest index first)."""
+    if kind == "ulp":
+        bits = np.uint32(0x3F800000) + rng.integers(0, 300, shape).astype(np.uint32)
+        return bits.view(np.float32)
+    if kind == "mixed":
+        special = np.array([0.0, -0.0, 1e-40, -1e-40, 2.0 ** -126, 2.0 ** -149, 1.0, -1.0, 2.0,
+                            0.5, 3.0e38, -3.0e38, 1.0 + 2.0 ** -23, 1.0 - 2.0 ** -24], np.float32)
+        x = rng.standard_normal(shape).astype(np.float32)
+        pick = rng.random(shape) < 0.6
+        x[pick] = rng.choice(special, int(pick.sum()))
+        return x
+    assert kind == "plateau"
+    x = rng.random(shape).astype(np.float32)
+    x[rng.random(shape) < 0.5] = np.float32(0.25)
+    return x
+
+
+@pytest.mark.parametrize("kind", ["ulp", "mixed", "plateau"])
+@pytest.mark.parametrize("n", [2, 3])
+def test_select_bitexact_adversarial_keys(kind, n):
+    cfg = W.preset(n).replace(n_blocks=1, batch=2)
+    print(f"select adversarial {kind} {cfg.name}", flush=True)
+    rng = np.random.default_rng(90 + n)
+    Vs = [_adversarial(rng, (cfg.n_frames, cfg.n_s), kind) for _ in range(cfg.batch)]
+    As = [_adversarial(rng, (cfg.n_s,), kind) for _ in range(cfg.batch)]
+    _select_given(cfg, Vs, As)
+
+
+@pytest.mark.parametrize("kind", ["ulp", "plateau"])
+def test_select_mass_threshold_adversarial_keys(kind):
+    cfg = W.preset(5).replace(n_blocks=1, d_model=64, n_heads=1, batch=2, k_anchor=24)
+    print(f"select adversarial mass {kind} {cfg.name}", flush=True)
+    rng = np.random.default_rng(97)
+    Vs = [_adversarial(rng, (cfg.n_frames, cfg.n_s), kind) / np.float32(cfg.n_s)
+          for _ in range(cfg.batch)]
+    As = [_adversarial(rng, (cfg.n_s,), kind) for _ in range(cfg.batch)]
+    _select_given(cfg, Vs, As)
 
 
 def test_select_mass_threshold_ragged():
