@@ -105,6 +105,72 @@ def test_block_bf16_max_width(d):
     _block_case(cfg, np.array([0, 130, 130, 301]), 2e-2, 1e-2)
 
 
+def _block_tail_from_qkv(x, w, temb, cu, n_heads, dtype, qkv):
+    """The block from its stored q, k, v on: the oracle's attention, output
+    projection, modulated LayerNorm and MLP (its primitives, its storage
+    rounding), so a reference that starts from the kernel's own QKV."""
+    st = O.storage_round(dtype)
+    x = np.asarray(x, np.float64)
+    d = x.shape[1]
+    sh1, sc1, g1, sh2, sc2, g2 = O.modulation(w["w_ada"], w["b_ada"], temb)
+    Wt = {k: np.asarray(v, np.float64) for k, v in w.items()}
+    q, k, v = qkv[:, :d], qkv[:, d:2 * d], qkv[:, 2 * d:]
+    o, _ = O.attention(q, k, v, cu, n_heads)
+    o = st(o)
+    x1 = st(x + g1 * (o @ Wt["w_o"].T + Wt["b_o"]))
+    h2 = st(O.layer_norm(x1) * (1.0 + sc2) + sh2)
+    u = st(O.gelu_tanh(h2 @ Wt["w_1"].T + Wt["b_1"]))
+    return st(x1 + g2 * (u @ Wt["w_2"].T + Wt["b_2"]))
+
+
+def test_block_bf16_peaky_attention():
+    """q and k projections scaled by 4 (logits 16x): near one-hot attention
+    whose running maximum moves in the middle of a sequence, the case the
+    kernel's lazy rescaling (a tile redone against a new maximum) exists for.
+    Checked from the kernel's own QKV: the normaliser against their float64
+    log-sum-exp (relative, since it grows with the logits) and the block
+    output against the oracle's remaining steps on that QKV."""
+    from helpers import device_blocks
+    cfg = _small_bf16(batch=4)
+    d = cfg.d_model
+    w = dict(W.block_weights(cfg, 0))
+    w["w_qkv"] = w["w_qkv"].copy()
+    w["b_qkv"] = w["b_qkv"].copy()
+    w["w_qkv"][:2 * d] *= 4.0
+    w["b_qkv"][:2 * d] *= 4.0
+    dw = device_blocks(cfg, [w])[0]
+    cu = np.array([0, 150, 150, 371, 372])
+    n_rows = int(cu[-1])
+    x = W.make_inputs(cfg, w["w_qkv"]).x(1)[:n_rows]
+    temb = W.timestep_embedding(cfg, 1)
+    print(f"peaky block {cfg.name} cu={list(cu)}", flush=True)
+    ctx = _ctx(cfg)
+    xd = dev(x, act_dtype(cfg))
+    lse = torch.empty(n_rows, cfg.n_heads, dtype=torch.float32, device="cuda:0")
+    qkv = torch.empty(n_rows, 3 * d, dtype=act_dtype(cfg), device="cuda:0")
+    ctx.block(dw, dev(temb), xd, n_rows, dev(np.asarray(cu, np.int32)), len(cu) - 1, lse, qkv)
+    torch.cuda.synchronize()
+    q = host(qkv).astype(np.float64)
+    rows = np.arange(n_rows)
+    lam = lse_from_qkv(q, cu, rows, cfg.n_heads)
+    # rows whose maximum logit lies more than 8 ln 2 above their first 64-key tile's
+    moved = 0
+    for a, b in zip(cu[:-1], cu[1:]):
+        if b - a <= 64:
+            continue
+        for h in range(cfg.n_heads):
+            c = slice(h * 64, (h + 1) * 64)
+            lg = q[a:b, c] @ q[a:b, d:2 * d][:, c].T / 8.0
+            moved += int((lg.max(axis=1) - lg[:, :64].max(axis=1) > 8 * math.log(2)).sum())
+    e_lam = float((np.abs(host(lse) - lam) / np.maximum(1.0, np.abs(lam))).max())
+    y_ref = _block_tail_from_qkv(x, w, temb, cu, cfg.n_heads, cfg.dtype, q)
+    e_y = maxrel(host(xd), y_ref)
+    print(f"  max |lambda| {np.abs(lam).max():.1f}, (row, head) pairs with a moved maximum {moved}, "
+          f"lambda rel {e_lam:.2e}, y {e_y:.2e}", flush=True)
+    assert moved >= 20
+    assert e_lam < 2e-6 and e_y < 2e-2
+
+
 # ---------------------------------------------------------------------------
 # (1) scoring
 # ---------------------------------------------------------------------------
