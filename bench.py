@@ -293,14 +293,10 @@ def timed_window(res, cls, units):
     return out
 
 
-def summarize_rocprof(db_path, bench_json):
-    """Per-kernel table of a rocprofv3 kernel trace of this benchmark, the
-    per-class rooflines over exactly the timed steps (dense-layout launches
-    of refresh steps and packed launches of sparse steps apart), and the
-    dominant class's average against the bench's live HIP-event average."""
+def kernel_table(db_path):
+    """Launch rows (dispatch id, name, start, end) of a rocprofv3 kernel trace
+    and the per-kernel table (calls, average and total duration)."""
     import sqlite3
-    res = json.load(open(bench_json))
-    cfg = workload_from_json(res["config"])
     con = sqlite3.connect(db_path)
     rows = con.execute("select dispatch_id, name, start, end from kernels order by start").fetchall()
     agg = {}
@@ -311,6 +307,17 @@ def summarize_rocprof(db_path, bench_json):
     lines = [f"{'calls':>7} {'avg_us':>10} {'total_ms':>10}  kernel"]
     for k, (n, t) in sorted(agg.items(), key=lambda kv: -kv[1][1]):
         lines.append(f"{n:7d} {t / n / 1e3:10.2f} {t / 1e6:10.2f}  {k}")
+    return rows, lines
+
+
+def summarize_rocprof(db_path, bench_json):
+    """Per-kernel table of a rocprofv3 kernel trace of this benchmark, the
+    per-class rooflines over exactly the timed steps (dense-layout launches
+    of refresh steps and packed launches of sparse steps apart), and the
+    dominant class's average against the bench's live HIP-event average."""
+    res = json.load(open(bench_json))
+    cfg = workload_from_json(res["config"])
+    rows, lines = kernel_table(db_path)
     trows = [(rid, name, b - a) for rid, name, a, b in rows]
     full = [cfg.l_full] * cfg.batch
     packed = res["config"]["packed_per_seq"]
@@ -973,6 +980,9 @@ def workload_from_json(cj):
 def main():
     if len(sys.argv) > 1 and sys.argv[1] == "--mfma":
         print(summarize_mfma(sys.argv[2], sys.argv[3]))
+        return
+    if len(sys.argv) > 1 and sys.argv[1] == "--kernels":
+        print("\n".join(kernel_table(sys.argv[2])[1]))
         return
     if len(sys.argv) > 1 and sys.argv[1] == "--summarize":
         print(summarize_rocprof(sys.argv[2], sys.argv[3]))
