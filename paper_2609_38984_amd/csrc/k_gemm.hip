@@ -202,7 +202,6 @@ gemm_bf16_nt(const bf16_t* __restrict__ A, int64_t lda, const bf16_t* __restrict
   constexpr int FM = TM / 32, FN = TN / 32;
   constexpr int A_INS = BM / 8 / NW, B_INS = BN / 8 / NW;
   static_assert(A_INS * 8 * NW == BM && B_INS * 8 * NW == BN, "tile/waves mismatch");
-  static_assert(A_INS % 2 == 0 && B_INS % 2 == 0, "slab pairs");
   __shared__ uint4 lds[2 * (BM + BN) * 8];   // [stage][A rows | B rows][8 chunks]
 
   int tm, tn;
@@ -219,25 +218,51 @@ gemm_bf16_nt(const bf16_t* __restrict__ A, int64_t lda, const bf16_t* __restrict
   const __amdgpu_buffer_rsrc_t rb = __builtin_amdgcn_make_buffer_rsrc(
       (void*)(B + (int64_t)n0 * ldb), (short)0,
       (int)min((int64_t)(N - n0) * ldb * 2, (int64_t)0x7fffffff), SWAM_BUF_DWORD3);
-  int va[2], vb[2];
+  // With an even slab count per wave, a wave's slabs start on a multiple of
+  // 16 rows, so two offsets (even / odd slab) plus a 16-row step address them
+  // all.  With an odd count bit 3 of a slab's first row alternates with the
+  // wave, so every slab keeps its own offset.
+  constexpr int NA = A_INS % 2 == 0 ? 2 : A_INS, NB = B_INS % 2 == 0 ? 2 : B_INS;
+  int va[NA], vb[NB];
+  if constexpr (A_INS % 2 == 0 && B_INS % 2 == 0) {
 #pragma unroll
-  for (int p = 0; p < 2; ++p) {
-    const int ch = (lane & 7) ^ lds_swz(8 * p + lrow);
-    va[p] = (int)(((int64_t)(wave * A_INS * 8 + 8 * p + lrow) * lda + 8 * ch) * 2);
-    vb[p] = (int)(((int64_t)(wave * B_INS * 8 + 8 * p + lrow) * ldb + 8 * ch) * 2);
+    for (int p = 0; p < 2; ++p) {
+      const int ch = (lane & 7) ^ lds_swz(8 * p + lrow);
+      va[p] = (int)(((int64_t)(wave * A_INS * 8 + 8 * p + lrow) * lda + 8 * ch) * 2);
+      vb[p] = (int)(((int64_t)(wave * B_INS * 8 + 8 * p + lrow) * ldb + 8 * ch) * 2);
+    }
+  } else {
+#pragma unroll
+    for (int p = 0; p < NA; ++p) {
+      const int r = wave * A_INS * 8 + 8 * p + lrow;
+      const int ch = (lane & 7) ^ lds_swz(A_INS % 2 == 0 ? 8 * p + lrow : r);
+      va[p] = (int)(((int64_t)r * lda + 8 * ch) * 2);
+    }
+#pragma unroll
+    for (int p = 0; p < NB; ++p) {
+      const int r = wave * B_INS * 8 + 8 * p + lrow;
+      const int ch = (lane & 7) ^ lds_swz(B_INS % 2 == 0 ? 8 * p + lrow : r);
+      vb[p] = (int)(((int64_t)r * ldb + 8 * ch) * 2);
+    }
   }
   const int step_a = (int)(16 * lda * 2), step_b = (int)(16 * ldb * 2);
   auto issue = [&](uint4* as, uint4* bs, int k0) {
 #pragma unroll
-    for (int j = 0; j < A_INS; ++j)
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(
-          ra, (lds_void_t*)(as + (wave * A_INS + j) * 64), 16,
-          vadd_sgpr(va[j & 1], (j >> 1) * step_a + k0 * 2), 0, 0, 0);
+    for (int j = 0; j < A_INS; ++j) {
+      int off;
+      if constexpr (A_INS % 2 == 0) off = vadd_sgpr(va[j & 1], (j >> 1) * step_a + k0 * 2);
+      else off = vadd_sgpr(va[j], k0 * 2);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, (lds_void_t*)(as + (wave * A_INS + j) * 64), 16,
+                                               off, 0, 0, 0);
+    }
 #pragma unroll
-    for (int j = 0; j < B_INS; ++j)
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(
-          rb, (lds_void_t*)(bs + (wave * B_INS + j) * 64), 16,
-          vadd_sgpr(vb[j & 1], (j >> 1) * step_b + k0 * 2), 0, 0, 0);
+    for (int j = 0; j < B_INS; ++j) {
+      int off;
+      if constexpr (B_INS % 2 == 0) off = vadd_sgpr(vb[j & 1], (j >> 1) * step_b + k0 * 2);
+      else off = vadd_sgpr(vb[j], k0 * 2);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rb, (lds_void_t*)(bs + (wave * B_INS + j) * 64), 16,
+                                               off, 0, 0, 0);
+    }
   };
 
   f32x16 acc[FM][FN];
@@ -460,15 +485,19 @@ static hipError_t run_bf16(const void* A, int64_t lda, const void* B, int64_t ld
 // Tile and K-split choice: modelled time = rounds * (per-CU MFMA work of one
 // round / tile efficiency) + (split > 1) the partial-sum pass over HBM.  A
 // round places `per_cu` workgroups on each of the 256 CUs (LDS-limited).  The
-// 256x256 kernel fits one workgroup per CU and runs in whole rounds; two
-// 128x128 workgroups share a CU and start as soon as a slot frees, so their
-// rounds count in halves once a grid spills past one slot per CU.  The
-// efficiencies are the per-CU MFMA rates of the two kernels measured on the
-// block shapes of the d = 1536 and d = 2048 workloads, relative to the
-// 256x256 kernel (whose rate, about 40% of the per-CU peak, is the base); the
-// pass moves splits * M * N fp32 partials plus the bf16 output (and
-// residual) at about 4 TB/s.  (A 256x128 tile measured at 0.72 of that rate
-// never won at any block shape from d = 256 to 4096 and was dropped.)
+// 256x256 and 192x256 kernels fit one workgroup per CU and run in whole
+// rounds; two 128x128 workgroups share a CU and start as soon as a slot
+// frees, so their rounds count in halves once a grid spills past one slot per
+// CU.  The efficiencies are the per-CU MFMA rates of the kernels measured on
+// the block shapes of the d = 1536 and d = 2048 workloads, relative to the
+// 256x256 kernel (whose rate, about 40% of the per-CU peak, is the base; the
+// 192x256 tile, 8 waves of 96 x 64, runs at 0.85-0.92 of it and takes 0.85,
+// which makes it the choice where its 3/4-size tiles fill whole rounds: the
+// packed MLP up projection at 3,472 rows, the out and down projections at
+// 17,472 rows); the pass moves splits * M * N fp32 partials plus the bf16
+// output (and residual) at about 4 TB/s.  (A 256x128 tile measured at 0.72
+// of that rate never won at any block shape from d = 256 to 4096 and was
+// dropped.)
 struct GemmPlan { int tile, splits; };
 static GemmPlan choose_gemm(int64_t M, int64_t N, int64_t K, int64_t ws_floats) {
   static int forced = -2, forced_split = -2;
@@ -479,14 +508,14 @@ static GemmPlan choose_gemm(int64_t M, int64_t N, int64_t K, int64_t ws_floats) 
     forced_split = f ? atoi(f) : -1;
   }
   struct Cand { int bm, bn, per_cu; double eff; };
-  const Cand c[2] = {{256, 256, 1, 1.0}, {128, 128, 2, 0.80}};
+  const Cand c[3] = {{256, 256, 1, 1.0}, {128, 128, 2, 0.80}, {192, 256, 1, 0.85}};
   const int split_opts[6] = {1, 2, 3, 4, 6, 8};
   const int64_t kt = K / GEMM_BK;
   const double cu_flops = 2.5e15 / 256.0 * 0.40;        // sustained MFMA rate per CU
   GemmPlan best{0, 1};
   double best_t = 1e30;
-  for (int i = 0; i < 2; ++i) {
-    if (forced >= 0 && forced <= 1 && i != forced) continue;
+  for (int i = 0; i < 3; ++i) {
+    if (forced >= 0 && forced <= 2 && i != forced) continue;
     const int64_t tiles = ((M + c[i].bm - 1) / c[i].bm) * ((N + c[i].bn - 1) / c[i].bn);
     for (int s : split_opts) {
       if (forced_split >= 1 && s != forced_split) continue;
@@ -518,6 +547,8 @@ static hipError_t dispatch_bf16(const void* A, int64_t lda, const void* B, int64
   const GemmPlan p = choose_gemm(M, N, K, ws ? ws_floats : 0);
   if (p.tile == 0)
     return run_bf16<ROLE, 256, 256, 2, 4, EPI>(A, lda, B, ldb, bias, gate, C, ldc, M, N, K, p.splits, ws, st);
+  if (p.tile == 2)
+    return run_bf16<ROLE, 192, 256, 2, 4, EPI>(A, lda, B, ldb, bias, gate, C, ldc, M, N, K, p.splits, ws, st);
   return run_bf16<ROLE, 128, 128, 2, 2, EPI>(A, lda, B, ldb, bias, gate, C, ldc, M, N, K, p.splits, ws, st);
 }
 
@@ -567,6 +598,8 @@ hipError_t launch_gemm_qkv(int dtype, const void* A, int64_t lda, const void* B,
       const int m = (int)M, n = (int)N, k = (int)K;
       if (p.tile == 0)
         return run_bf16<ROLE_QKV, 256, 256, 2, 4, EPI_BIAS_QKPOST>(A, lda, B, ldb, bias, nullptr, C, ldc, m, n, k, 1, nullptr, st, qp);
+      if (p.tile == 2)
+        return run_bf16<ROLE_QKV, 192, 256, 2, 4, EPI_BIAS_QKPOST>(A, lda, B, ldb, bias, nullptr, C, ldc, m, n, k, 1, nullptr, st, qp);
       return run_bf16<ROLE_QKV, 128, 128, 2, 2, EPI_BIAS_QKPOST>(A, lda, B, ldb, bias, nullptr, C, ldc, m, n, k, 1, nullptr, st, qp);
     }
   }

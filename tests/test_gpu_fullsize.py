@@ -69,6 +69,9 @@ def test_block_wam_dense_10160_sampled():
 
 
 def test_block_wam_packed_3472_sampled():
+    """The packed sequence of the WAM workload as the bench times it: the
+    4-wave attention, the 128x128 out projection, the 192x256 MLP up tile
+    and the down projection split along K in three."""
     cfg = W.preset(3)
     x = W.make_inputs(cfg, W.block_weights(cfg, 0)["w_qkv"]).x(0)
     _sampled_block(cfg, np.array([0, cfg.t_pack_fixed]), x)
@@ -85,7 +88,7 @@ def test_block_ragged_batch_sampled():
 
 def test_block_2048_packed_3744_sampled():
     """The packed sequence of the d = 2048 workload at 10% + 64 retention
-    (3,744 rows, 32 heads): 480 attention workgroups of 8 waves, the 128x128
+    (3,744 rows, 32 heads): 480 attention workgroups of 8 waves, the 192x256
     QKV tile and the down projection split along K in two."""
     cfg = W.preset(4, percent=10).replace(n_blocks=1)
     assert cfg.t_pack_fixed == 3744
