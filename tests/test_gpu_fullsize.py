@@ -106,6 +106,18 @@ def test_block_wam_packed_4200_sampled():
     _sampled_block(cfg, np.array([0, 4200]), x)
 
 
+@pytest.mark.parametrize("pct,rows", [(25, 6208), (50, 10304)])
+def test_block_2048_packed_sampled(pct, rows):
+    """The packed sequences of the d = 2048 workload at 25% + 64 (the bench's
+    second point: 800 workgroups of the 8-wave attention, 256x256 projections)
+    and 50% + 64 retention (the out projection on the 192x256 tile, the down
+    projection split along K in three)."""
+    cfg = W.preset(4, percent=pct).replace(n_blocks=1)
+    assert cfg.t_pack_fixed == rows
+    x = W.make_inputs(cfg, W.block_weights(cfg, 0)["w_qkv"]).x(0)
+    _sampled_block(cfg, np.array([0, rows]), x, per_seq=16)
+
+
 def test_block_2048_dense_sampled():
     cfg = W.preset(4, percent=25).replace(n_blocks=1)
     x = W.make_inputs(cfg, W.block_weights(cfg, 0)["w_qkv"]).x(0)
