@@ -405,8 +405,10 @@ int run_adaln(swam_ctx* c, const swam_block_weights* blocks, int n_blk, const fl
   return SWAM_OK;
 }
 
-int run_reduce(swam_ctx* c, const float* s_all) {
+// on: the stream to enqueue on (the context stream when NULL)
+int run_reduce(swam_ctx* c, const float* s_all, hipStream_t on = nullptr) {
   const swam_config& cf = c->cfg;
+  const hipStream_t st = on ? on : c->st;
   ReduceArgs r{};
   r.s_all = s_all;
   r.frame_sum = c->ptr<double>(c->lay.fsum);
@@ -423,24 +425,27 @@ int run_reduce(swam_ctx* c, const float* s_all) {
   r.n_s = (int)c->dv.n_s;
   r.k_layer = cf.k_layer;
   r.cv_penalty = cf.cv_penalty;
-  Timed t(c, SWAM_T_REDUCE);
-  SWAM_HIP(c, launch_score_reduce(r, c->st), "score_reduce");
+  Timed t(c, SWAM_T_REDUCE, st);
+  SWAM_HIP(c, launch_score_reduce(r, st), "score_reduce");
   return SWAM_OK;
 }
 
 // read the packed sequence offsets back to the host (one synchronisation)
-int read_packed_rows(swam_ctx* c) {
+int read_packed_rows(swam_ctx* c, hipStream_t st) {
   const int B = c->cfg.batch;
   SWAM_HIP(c, hipMemcpyAsync(c->host_cu, c->ptr<int32_t>(c->lay.cu_packed), (B + 1) * 4,
-                             hipMemcpyDeviceToHost, c->st), "read cu_seqlens");
-  SWAM_HIP(c, hipStreamSynchronize(c->st), "synchronise");
+                             hipMemcpyDeviceToHost, st), "read cu_seqlens");
+  SWAM_HIP(c, hipStreamSynchronize(st), "synchronise");
   c->packed_rows = c->host_cu[B];
   return SWAM_OK;
 }
 
-// k_core / k_anchor < 0: the configured budgets
-int run_select(swam_ctx* c, const float* v, const float* a, int k_core = -1, int k_anchor = -1) {
+// k_core / k_anchor < 0: the configured budgets; on: the stream to enqueue on
+// (the context stream when NULL)
+int run_select(swam_ctx* c, const float* v, const float* a, int k_core = -1, int k_anchor = -1,
+               hipStream_t on = nullptr) {
   const swam_config& cf = c->cfg;
+  const hipStream_t st = on ? on : c->st;
   SelectArgs s{};
   s.v = v;
   s.a = a;
@@ -460,26 +465,26 @@ int run_select(swam_ctx* c, const float* v, const float* a, int k_core = -1, int
   s.n_ctx = cf.n_ctx;
   s.n_act = cf.n_act;
   {
-    Timed t(c, SWAM_T_SELECT);
-    SWAM_HIP(c, launch_select(s, c->st), "select");
+    Timed t(c, SWAM_T_SELECT, st);
+    SWAM_HIP(c, launch_select(s, st), "select");
     if (cf.cfg_pairs) {
       // the unconditional partner b + B/2 keeps the positions selected for b
       const int64_t P = c->dv.n_scored;
       const size_t kb = (size_t)(P * c->dv.l_full) * 4, ib = (size_t)(P * cf.n_frames * c->dv.k_max) * 4,
                    cb = (size_t)(P * cf.n_frames) * 4;
-      SWAM_HIP(c, hipMemcpyAsync((char*)s.keep + kb, s.keep, kb, hipMemcpyDeviceToDevice, c->st),
+      SWAM_HIP(c, hipMemcpyAsync((char*)s.keep + kb, s.keep, kb, hipMemcpyDeviceToDevice, st),
                "share keep");
       SWAM_HIP(c, hipMemcpyAsync((char*)s.keep_idx + ib, s.keep_idx, ib, hipMemcpyDeviceToDevice,
-                                 c->st), "share keep_idx");
+                                 st), "share keep_idx");
       SWAM_HIP(c, hipMemcpyAsync((char*)s.keep_cnt + cb, s.keep_cnt, cb, hipMemcpyDeviceToDevice,
-                                 c->st), "share keep_cnt");
+                                 st), "share keep_cnt");
     }
     SWAM_HIP(c, launch_packmap(s.keep, c->ptr<int32_t>(c->lay.pack_pos),
                                c->ptr<int32_t>(c->lay.gather), c->ptr<int32_t>(c->lay.cu_packed),
-                               cf.batch, c->dv.l_full, c->st), "packmap");
+                               cf.batch, c->dv.l_full, st), "packmap");
   }
   if (c->dv.mass_den > 0) {
-    const int rc = read_packed_rows(c);
+    const int rc = read_packed_rows(c, st);
     if (rc != SWAM_OK) return rc;
   } else {
     c->packed_rows = (int64_t)cf.batch * c->dv.t_pack_fixed;
@@ -827,7 +832,7 @@ int swam_set_selection(swam_ctx* c, const int32_t* keep_idx, const int32_t* keep
                                c->ptr<int32_t>(c->lay.gather), c->ptr<int32_t>(c->lay.cu_packed),
                                cf.batch, c->dv.l_full, c->st), "packmap");
   }
-  const int rc = read_packed_rows(c);
+  const int rc = read_packed_rows(c, c->st);
   if (rc != SWAM_OK) return rc;
   c->sel_valid = true;
   return SWAM_OK;
@@ -993,13 +998,20 @@ int enqueue_step(swam_ctx* c, const swam_model* model, const void* x_full, const
                      score ? &a : nullptr);
       if (rc != SWAM_OK) return rc;
     }
-    if ((rc = join_score(c)) != SWAM_OK) return rc;
     if (score) {
+      // the reduce, the selection and the pack map follow the last layer's
+      // scoring on the side stream, overlapping the last block's projections
+      // (they read only the scores and write only selection state); the
+      // context stream waits for them before the step ends
       c->scores_valid = true;
-      if ((rc = run_reduce(c, c->ptr<float>(c->lay.s_all))) != SWAM_OK) return rc;
-      if ((rc = run_select(c, c->ptr<float>(c->lay.v), c->ptr<float>(c->lay.a))) != SWAM_OK)
+      if ((rc = run_reduce(c, c->ptr<float>(c->lay.s_all), c->side)) != SWAM_OK) return rc;
+      if ((rc = run_select(c, c->ptr<float>(c->lay.v), c->ptr<float>(c->lay.a), -1, -1,
+                           c->side)) != SWAM_OK)
         return rc;
+      SWAM_HIP(c, hipEventRecord(c->ev_score, c->side), "selection done");
+      c->score_pending = true;
     }
+    if ((rc = join_score(c)) != SWAM_OK) return rc;
   } else {
     // out of place, the pruned rows are copied on the side stream (forked
     // inside block 0 after the pack, or here when no row is retained)
