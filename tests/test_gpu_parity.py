@@ -171,6 +171,17 @@ def test_block_bf16_peaky_attention():
     assert e_lam < 2e-6 and e_y < 2e-2
 
 
+def _odd_width(**kw):
+    # 25 heads: d = 1600, so every projection's N (4800, 1600, 6400) leaves a
+    # ragged last 256-wide tile and an odd head count meets attention, the
+    # LayerNorm's chunks and the scorer's four-way head split
+    return W.preset(2).replace(name="bf16-d1600", d_model=1600, n_heads=25, **kw)
+
+
+def test_block_bf16_odd_heads_ragged_n():
+    _block_case(_odd_width(n_blocks=1), np.array([0, 130, 130, 301]), 2e-2, 1e-2)
+
+
 # ---------------------------------------------------------------------------
 # (1) scoring
 # ---------------------------------------------------------------------------
@@ -207,6 +218,11 @@ def _score_case(cfg, mode, scale=1.6):
     err = rowwise_maxrel(got, np.stack(S_ref))
     print(f"  rowwise max-rel {err:.2e}", flush=True)
     assert err < 1e-5
+
+
+@pytest.mark.parametrize("mode", ["A", "B"])
+def test_score_bf16_odd_heads(mode):
+    _score_case(_odd_width(n_blocks=1), mode)
 
 
 @pytest.mark.parametrize("mode", ["A", "B"])
