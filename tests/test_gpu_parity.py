@@ -182,6 +182,16 @@ def test_block_bf16_odd_heads_ragged_n():
     _block_case(_odd_width(n_blocks=1), np.array([0, 130, 130, 301]), 2e-2, 1e-2)
 
 
+def _one_head(**kw):
+    # d = 64: the QKV, out and up projections' K is one 64-wide stage (no
+    # prefetch iteration), one attention head, one head for the scorer's four waves
+    return W.preset(2).replace(name="bf16-d64", d_model=64, n_heads=1, **kw)
+
+
+def test_block_bf16_one_head():
+    _block_case(_one_head(n_blocks=1), np.array([0, 130, 130, 301]), 2e-2, 1e-2)
+
+
 # ---------------------------------------------------------------------------
 # (1) scoring
 # ---------------------------------------------------------------------------
@@ -223,6 +233,11 @@ def _score_case(cfg, mode, scale=1.6):
 @pytest.mark.parametrize("mode", ["A", "B"])
 def test_score_bf16_odd_heads(mode):
     _score_case(_odd_width(n_blocks=1), mode)
+
+
+@pytest.mark.parametrize("mode", ["A", "B"])
+def test_score_bf16_one_head(mode):
+    _score_case(_one_head(n_blocks=1), mode)
 
 
 @pytest.mark.parametrize("mode", ["A", "B"])
