@@ -346,7 +346,8 @@ def summarize_rocprof(db_path, bench_json):
     lines.append("")
     lines.append(f"timed window: {cls} {len(timed_window(res, cls, class_units(trows, cls)))} launch units, "
                  f"avg {avgs.get(cls, float('nan')):.2f} us (bench live HIP-event average "
-                 f"{rf['avg_launch_us']:.2f} us)")
+                 f"{rf['avg_launch_us']:.2f} us over {rf['launches']} launches, every "
+                 f"{rf.get('bracketed_every', 1)}th of the class)")
     return "\n".join(lines)
 
 
@@ -379,19 +380,31 @@ def measure(cfg, model, xs, tembs, steps, warmup, reps):
     def run(tau, flags=0):
         return ctx.step(model, xs[tau % n_sched], tembs[tau % n_sched], tau, y, flags)
 
-    warm_kinds = [run(t) for t in range(max(warmup, 2))]
+    n_warm = max(warmup, 2)
+    warm_kinds = [run(t) for t in range(n_warm)]
     torch.cuda.synchronize()
     phase = {cls: ctx.timer_read(cls) for cls in swam.TIMERS}
     dominant = max(BOUND, key=lambda c: phase[c][1])
+    # Each event bracket costs the stream a few microseconds (about 0.2 ms per
+    # step with all 28 attention launches bracketed), so the timed region
+    # brackets every `stride`-th launch of the dominant class: the largest
+    # stride <= 8 dividing its launches per step of every kind, so each step
+    # contributes the same launch positions.
+    per_step = set()
+    for kind in set(warm_kinds):
+        n_kind = ctx.timer_read(dominant, kind)[0]
+        if n_kind:
+            per_step.add(n_kind // warm_kinds.count(kind))
+    stride = max(s for s in range(1, 9) if all(n % s == 0 for n in per_step))
 
-    # timed region: exactly K steps, only the dominant class bracketed by events
+    # timed region: exactly K steps, sampled launches of the dominant class bracketed
     ctx.timer_enable([dominant], capacity=max(64, steps * cfg.n_blocks * 2))
+    ctx.timer_stride(stride)
     torch.cuda.synchronize()
     t_start = time.perf_counter()
     kinds = [run(t) for t in range(steps)]
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t_start
-    n_dom, ms_dom = ctx.timer_read(dominant)
 
     full_rows = [cfg.l_full] * cfg.batch
     cu = torch.empty(cfg.batch + 1, dtype=torch.int32, device=dev)
@@ -399,13 +412,14 @@ def measure(cfg, model, xs, tembs, steps, warmup, reps):
     cuh = cu.cpu().numpy()
     packed_rows = [int(cuh[b + 1] - cuh[b]) for b in range(cfg.batch)]
     rows_of = {swam.KIND_REFRESH: full_rows, swam.KIND_DENSE: full_rows, swam.KIND_SPARSE: packed_rows}
-    if dominant == "SCORE":
-        work = sum(kernel_work(cfg, dominant, full_rows) * cfg.n_blocks
-                   for k in kinds if k == swam.KIND_REFRESH)
-    elif dominant in ("PACK", "UNPACK"):
-        work = sum(kernel_work(cfg, dominant, packed_rows) for k in kinds if k == swam.KIND_SPARSE)
-    else:
-        work = sum(kernel_work(cfg, dominant, rows_of[k]) * cfg.n_blocks for k in kinds)
+    # algorithmic work of exactly the bracketed launches, by the kind of their step
+    work, n_dom, ms_dom = 0.0, 0, 0.0
+    for kind in set(kinds):
+        n_kind, ms_kind = ctx.timer_read(dominant, kind)
+        work += n_kind * kernel_work(cfg, dominant, rows_of[kind])
+        n_dom += n_kind
+        ms_dom += ms_kind
+    ctx.timer_stride(1)
     bound = BOUND[dominant]
     if bound == "mfma":
         achieved = work / (ms_dom * 1e-3) / 1e12
@@ -418,7 +432,8 @@ def measure(cfg, model, xs, tembs, steps, warmup, reps):
     roofline = {"kernel": dominant, "bound": bound, "achieved": round(achieved, 2), "peak": peak,
                 "unit": unit, "frac": round(achieved / peak, 4),
                 "traffic": read_traffic(dominant, cfg.name),
-                "launches": n_dom, "avg_launch_us": round(ms_dom * 1e3 / max(n_dom, 1), 2)}
+                "launches": n_dom, "bracketed_every": stride,
+                "avg_launch_us": round(ms_dom * 1e3 / max(n_dom, 1), 2)}
 
     def median_ms(flags, tau):
         # the paper's protocol: 5 untimed runs, then `reps` timed ones, median

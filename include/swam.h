@@ -457,13 +457,34 @@ enum {
 };
 
 /* Bracket every launch (phase) of the classes in `mask` (bit i = class i)
- * with HIP events on the context stream; mask 0 disables.  Enabling
- * allocates an event pool of `capacity` pairs (dropped beyond that). */
+ * with HIP events on the stream it runs on; mask 0 disables.  Enabling
+ * allocates an event pool of `capacity` pairs (dropped beyond that) and
+ * restarts the per-class launch counts of swam_timer_stride.  Each bracket
+ * costs the stream a few microseconds. */
 int swam_timer_enable(swam_ctx* ctx, uint32_t mask, int32_t capacity);
+/* Forget the recorded brackets and restart the launch counts. */
 int swam_timer_reset(swam_ctx* ctx);
+/* Bracket only launches whose ordinal within their class (0, 1, ... since
+ * the last enable / reset / this call) is a multiple of `stride` (>= 1;
+ * 1, the default, brackets every launch).  Synchronises the stream, drops
+ * the recorded brackets; SWAM_E_INVALID for stride < 1.  With a stride
+ * that divides a class's launches per step, every step contributes the
+ * same launch positions. */
+int swam_timer_stride(swam_ctx* ctx, int32_t stride);
 /* Synchronise the stream and return the launch count and summed duration
- * of class `cls` since the last reset. */
+ * of the bracketed launches of class `cls` since the last reset. */
 int swam_timer_read(swam_ctx* ctx, int32_t cls, int64_t* launches, double* total_ms);
+
+#define SWAM_KIND_NONE (-1)  /* launches outside swam_step / swam_sample_step */
+#define SWAM_KIND_ANY (-2)   /* every launch (swam_timer_read) */
+
+/* As swam_timer_read, restricted to the launches enqueued by steps of one
+ * kind (SWAM_KIND_DENSE / _REFRESH / _SPARSE, from swam_step,
+ * swam_sample_step and the eager path of swam_step_graph), by none
+ * (SWAM_KIND_NONE: swam_block, swam_score, ...), or by any (SWAM_KIND_ANY).
+ * SWAM_E_INVALID for another kind or class. */
+int swam_timer_read_kind(swam_ctx* ctx, int32_t cls, int32_t kind, int64_t* launches,
+                         double* total_ms);
 
 #ifdef __cplusplus
 }

@@ -203,8 +203,12 @@ struct swam_ctx {
   // timers
   uint32_t tmask = 0;
   int tcap = 0, tused = 0;
+  int tstride = 1;                    // bracket every tstride-th launch of a class
+  int64_t tcount[SWAM_T_COUNT] = {};  // launches per class since enable / reset
+  int step_kind = SWAM_KIND_NONE;     // kind of the step being enqueued
   std::vector<hipEvent_t> ev;   // 2 per slot
   std::vector<int> ev_cls;
+  std::vector<int> ev_kind;     // step kind per slot
   // captured steps (swam_step_graph)
   struct GraphEntry {
     int kind;
@@ -247,11 +251,12 @@ struct Timed {
   int slot = -1;
   Timed(swam_ctx* ctx, int cls) : Timed(ctx, cls, ctx->st) {}
   Timed(swam_ctx* ctx, int cls, hipStream_t on) : c(ctx), s(on) {
-    if (!c->capturing && ((c->tmask >> cls) & 1u) && c->tused < c->tcap) {
-      slot = c->tused++;
-      c->ev_cls[slot] = cls;
-      (void)hipEventRecord(c->ev[2 * slot], s);
-    }
+    if (c->capturing || !((c->tmask >> cls) & 1u)) return;
+    if (c->tcount[cls]++ % c->tstride != 0 || c->tused >= c->tcap) return;
+    slot = c->tused++;
+    c->ev_cls[slot] = cls;
+    c->ev_kind[slot] = c->step_kind;
+    (void)hipEventRecord(c->ev[2 * slot], s);
   }
   ~Timed() {
     if (slot >= 0) (void)hipEventRecord(c->ev[2 * slot + 1], s);
@@ -605,14 +610,14 @@ int swam_destroy(swam_ctx* c) {
   if (!c) return SWAM_OK;
   if (c->st || c->arena) (void)hipStreamSynchronize(c->st);
   if (c->side) (void)hipStreamSynchronize(c->side);
-  for (auto& g : c->graphs) hipGraphExecDestroy(g.exec);
-  for (hipEvent_t ev : c->ev) hipEventDestroy(ev);
-  if (c->arena) hipFree(c->arena);
-  if (c->host_cu) hipHostFree(c->host_cu);
-  if (c->order_ev) hipEventDestroy(c->order_ev);
-  if (c->ev_attn) hipEventDestroy(c->ev_attn);
-  if (c->ev_score) hipEventDestroy(c->ev_score);
-  if (c->side) hipStreamDestroy(c->side);
+  for (auto& g : c->graphs) (void)hipGraphExecDestroy(g.exec);
+  for (hipEvent_t ev : c->ev) (void)hipEventDestroy(ev);
+  if (c->arena) (void)hipFree(c->arena);
+  if (c->host_cu) (void)hipHostFree(c->host_cu);
+  if (c->order_ev) (void)hipEventDestroy(c->order_ev);
+  if (c->ev_attn) (void)hipEventDestroy(c->ev_attn);
+  if (c->ev_score) (void)hipEventDestroy(c->ev_score);
+  if (c->side) (void)hipStreamDestroy(c->side);
   delete c;
   return SWAM_OK;
 }
@@ -953,8 +958,25 @@ int check_step(swam_ctx* c, const swam_model* model, const void* x_full, const f
 }
 
 // every launch of one step, in order, on the context stream
+// tags the timer slots of the launches enqueued in its scope with a step kind
+struct StepKindScope {
+  swam_ctx* c;
+  int prev;
+  StepKindScope(swam_ctx* ctx, int kind) : c(ctx), prev(ctx->step_kind) { c->step_kind = kind; }
+  ~StepKindScope() { c->step_kind = prev; }
+};
+
+int enqueue_step_launches(swam_ctx* c, const swam_model* model, const void* x_full,
+                          const float* temb, int kind, void* y_full);
+
 int enqueue_step(swam_ctx* c, const swam_model* model, const void* x_full, const float* temb,
                  int kind, void* y_full) {
+  StepKindScope scope(c, kind);
+  return enqueue_step_launches(c, model, x_full, temb, kind, y_full);
+}
+
+int enqueue_step_launches(swam_ctx* c, const swam_model* model, const void* x_full,
+                          const float* temb, int kind, void* y_full) {
   const swam_config& cf = c->cfg;
   int rc = run_adaln(c, model->blocks, cf.n_blocks, temb);
   if (rc != SWAM_OK) return rc;
@@ -1180,6 +1202,7 @@ int swam_sample_step(swam_ctx* c, const swam_model* model, const swam_latent_io*
     return set_err(c, SWAM_E_INVALID, "x_full must not alias y_full (its context rows are reused)");
   int kind;
   if ((rc = check_step(c, model, x_full, temb, tau, y_full, flags, &kind)) != SWAM_OK) return rc;
+  StepKindScope scope(c, kind);
   if ((rc = swam_embed(c, io, z, x_full)) != SWAM_OK) return rc;
   if ((rc = enqueue_step(c, model, x_full, temb, kind, y_full)) != SWAM_OK) return rc;
   if ((rc = swam_velocity(c, io, y_full, kind == SWAM_KIND_SPARSE, v)) != SWAM_OK) return rc;
@@ -1224,15 +1247,15 @@ int swam_step_graph(swam_ctx* c, const swam_model* model, const void* x_full,
     e = hipStreamEndCapture(c->st, &graph);
     c->capturing = false;
     if (rc != SWAM_OK) {
-      if (graph) hipGraphDestroy(graph);
+      if (graph) (void)hipGraphDestroy(graph);
       return rc;
     }
     if (e != hipSuccess) return hip_check(c, e, "end capture");
     e = hipGraphInstantiate(&exec, graph, nullptr, nullptr, 0);
-    hipGraphDestroy(graph);
+    (void)hipGraphDestroy(graph);
     if (e != hipSuccess) return hip_check(c, e, "graph instantiate");
     if (c->graphs.size() >= MAX_GRAPHS) {
-      hipGraphExecDestroy(c->graphs.front().exec);
+      (void)hipGraphExecDestroy(c->graphs.front().exec);
       c->graphs.erase(c->graphs.begin());
     }
     c->graphs.push_back({kind, x_full, y_full, temb, wsig, packed, exec});
@@ -1250,7 +1273,7 @@ int swam_step_graph(swam_ctx* c, const swam_model* model, const void* x_full,
 int swam_graph_clear(swam_ctx* c) {
   if (!c) return set_err(nullptr, SWAM_E_INVALID, "ctx is NULL");
   SWAM_HIP(c, hipStreamSynchronize(c->st), "synchronise");
-  for (auto& g : c->graphs) hipGraphExecDestroy(g.exec);
+  for (auto& g : c->graphs) (void)hipGraphExecDestroy(g.exec);
   c->graphs.clear();
   return SWAM_OK;
 }
@@ -1259,15 +1282,18 @@ int swam_timer_enable(swam_ctx* c, uint32_t mask, int32_t capacity) {
   if (!c) return set_err(nullptr, SWAM_E_INVALID, "ctx is NULL");
   if (mask && capacity < 1) return set_err(c, SWAM_E_INVALID, "capacity must be >= 1");
   SWAM_HIP(c, hipStreamSynchronize(c->st), "synchronise");
-  for (hipEvent_t ev : c->ev) hipEventDestroy(ev);
+  for (hipEvent_t ev : c->ev) (void)hipEventDestroy(ev);
   c->ev.clear();
   c->ev_cls.clear();
+  c->ev_kind.clear();
   c->tmask = mask;
   c->tcap = 0;
   c->tused = 0;
+  for (int64_t& n : c->tcount) n = 0;
   if (!mask) return SWAM_OK;
   c->ev.resize(2 * (size_t)capacity);
   c->ev_cls.assign(capacity, -1);
+  c->ev_kind.assign(capacity, SWAM_KIND_NONE);
   for (auto& ev : c->ev) SWAM_HIP(c, hipEventCreate(&ev), "event create");
   c->tcap = capacity;
   return SWAM_OK;
@@ -1277,17 +1303,32 @@ int swam_timer_reset(swam_ctx* c) {
   if (!c) return set_err(nullptr, SWAM_E_INVALID, "ctx is NULL");
   SWAM_HIP(c, hipStreamSynchronize(c->st), "synchronise");
   c->tused = 0;
+  for (int64_t& n : c->tcount) n = 0;
   return SWAM_OK;
 }
 
-int swam_timer_read(swam_ctx* c, int32_t cls, int64_t* launches, double* total_ms) {
+int swam_timer_stride(swam_ctx* c, int32_t stride) {
+  if (!c) return set_err(nullptr, SWAM_E_INVALID, "ctx is NULL");
+  if (stride < 1) return set_err(c, SWAM_E_INVALID, "stride must be >= 1");
+  SWAM_HIP(c, hipStreamSynchronize(c->st), "synchronise");
+  c->tstride = stride;
+  c->tused = 0;
+  for (int64_t& n : c->tcount) n = 0;
+  return SWAM_OK;
+}
+
+int swam_timer_read_kind(swam_ctx* c, int32_t cls, int32_t kind, int64_t* launches,
+                         double* total_ms) {
   if (!c || !launches || !total_ms) return set_err(c, SWAM_E_INVALID, "NULL argument");
   if (cls < 0 || cls >= SWAM_T_COUNT) return set_err(c, SWAM_E_INVALID, "bad timer class");
+  if (kind != SWAM_KIND_ANY && kind != SWAM_KIND_NONE && kind != SWAM_KIND_DENSE &&
+      kind != SWAM_KIND_REFRESH && kind != SWAM_KIND_SPARSE)
+    return set_err(c, SWAM_E_INVALID, "bad step kind");
   SWAM_HIP(c, hipStreamSynchronize(c->st), "synchronise");
   int64_t n = 0;
   double ms = 0.0;
   for (int i = 0; i < c->tused; ++i) {
-    if (c->ev_cls[i] != cls) continue;
+    if (c->ev_cls[i] != cls || (kind != SWAM_KIND_ANY && c->ev_kind[i] != kind)) continue;
     float e = 0.0f;
     SWAM_HIP(c, hipEventElapsedTime(&e, c->ev[2 * i], c->ev[2 * i + 1]), "elapsed");
     ms += e;
@@ -1296,6 +1337,10 @@ int swam_timer_read(swam_ctx* c, int32_t cls, int64_t* launches, double* total_m
   *launches = n;
   *total_ms = ms;
   return SWAM_OK;
+}
+
+int swam_timer_read(swam_ctx* c, int32_t cls, int64_t* launches, double* total_ms) {
+  return swam_timer_read_kind(c, cls, SWAM_KIND_ANY, launches, total_ms);
 }
 
 }  // extern "C"

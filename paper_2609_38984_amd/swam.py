@@ -20,6 +20,7 @@ STATUS = {0: "SWAM_OK", -1: "SWAM_E_INVALID", -2: "SWAM_E_SHAPE", -3: "SWAM_E_DT
           -4: "SWAM_E_STATE", -5: "SWAM_E_HIP", -6: "SWAM_E_NOMEM", -7: "SWAM_E_UNSUPPORTED"}
 FORCE_DENSE, FORCE_REFRESH = 1, 2
 KIND_DENSE, KIND_REFRESH, KIND_SPARSE = 0, 1, 2
+KIND_NONE, KIND_ANY = -1, -2   # timer slots outside any step / every slot
 TIMERS = ["ADALN", "LNMOD", "GEMM_QKV", "ATTN", "GEMM_OUT", "GEMM_UP", "GEMM_DOWN", "SCORE",
           "REDUCE", "SELECT", "PACK", "UNPACK", "COPY", "SAMPLE", "QK_POST"]
 T = {name: i for i, name in enumerate(TIMERS)}
@@ -28,7 +29,8 @@ EXPORTS = ["swam_create", "swam_destroy", "swam_set_stream", "swam_plan", "swam_
            "swam_last_error", "swam_score", "swam_score_reduce", "swam_select",
            "swam_set_selection", "swam_packed_rows", "swam_export", "swam_pack", "swam_unpack",
            "swam_block", "swam_step", "swam_step_graph", "swam_graph_clear", "swam_timer_enable",
-           "swam_timer_reset", "swam_timer_read", "swam_embed", "swam_velocity",
+           "swam_timer_reset", "swam_timer_read", "swam_timer_stride",
+           "swam_timer_read_kind", "swam_embed", "swam_velocity",
            "swam_sample_update", "swam_sample_step", "swam_overlap", "swam_select_random",
            "swam_flow_sigmas", "swam_select_noalloc"]
 
@@ -129,6 +131,8 @@ def load_library(path: str = LIB_PATH):
         "swam_graph_clear": [P],
         "swam_timer_enable": [P, C.c_uint32, I32], "swam_timer_reset": [P],
         "swam_timer_read": [P, I32, C.POINTER(I64), C.POINTER(C.c_double)],
+        "swam_timer_stride": [P, I32],
+        "swam_timer_read_kind": [P, I32, I32, C.POINTER(I64), C.POINTER(C.c_double)],
         "swam_overlap": [P, P, P, I64, I64, P],
         "swam_flow_sigmas": [I32, C.c_double, C.POINTER(C.c_double)],
         "swam_select_noalloc": [I32, I32, I32, I32, I32, I32, I32, F, P, P, P, P, P, P, P, P],
@@ -468,8 +472,11 @@ class Context:
     def timer_reset(self):
         self._ok(self.lib.swam_timer_reset(self.h))
 
-    def timer_read(self, cls) -> tuple[int, float]:
+    def timer_stride(self, stride: int):
+        self._ok(self.lib.swam_timer_stride(self.h, int(stride)))
+
+    def timer_read(self, cls, kind: int = KIND_ANY) -> tuple[int, float]:
         n, ms = C.c_int64(), C.c_double()
-        self._ok(self.lib.swam_timer_read(self.h, T[cls] if isinstance(cls, str) else int(cls),
-                                          C.byref(n), C.byref(ms)))
+        self._ok(self.lib.swam_timer_read_kind(self.h, T[cls] if isinstance(cls, str) else int(cls),
+                                               int(kind), C.byref(n), C.byref(ms)))
         return n.value, ms.value

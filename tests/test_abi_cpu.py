@@ -28,7 +28,7 @@ def _declared():
 def test_every_declared_symbol_is_exported(lib):
     from paper_2609_38984_amd import swam
     names = _declared()
-    assert len(names) == 29
+    assert len(names) == 31
     assert sorted(swam.EXPORTS) == names
     for n in names:
         assert hasattr(lib, n), n
@@ -93,6 +93,9 @@ def test_null_context_is_rejected(lib):
     assert lib.swam_set_stream(None, None) == -1
     assert lib.swam_packed_rows(None, None) == -1
     assert lib.swam_graph_clear(None) == -1
+    assert lib.swam_timer_stride(None, 1) == -1
+    n, ms = C.c_int64(), C.c_double()
+    assert lib.swam_timer_read_kind(None, 0, -2, C.byref(n), C.byref(ms)) == -1
     assert lib.swam_destroy(None) == 0
 
 
