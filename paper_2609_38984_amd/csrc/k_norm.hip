@@ -26,42 +26,57 @@ adaln_kernel(AdalnArgs args, const float* __restrict__ temb, int d_temb, int d6,
 }
 
 // bf16 weights, d_temb = 128: 16 lanes per output row (one 16-byte load of 8
-// weights each), 4 rows per wave, 16 rows per workgroup; SiLU(temb) once per
-// lane instead of once per weight
+// weights each), ADALN_RPG rows per 16-lane group (rows g, g + 16, ... of the
+// workgroup's 16 * ADALN_RPG, so each round of loads reads 4 KB of
+// consecutive rows), every load issued before the first reduction; SiLU(temb)
+// once per lane instead of once per weight
+constexpr int ADALN_RPG = 8;
+
 __global__ void __launch_bounds__(256)
 adaln_bf16_t128(AdalnArgs args, const float* __restrict__ temb, int d6,
                 float* __restrict__ mod) {
   const int blk = blockIdx.y;
-  const int row = blockIdx.x * 16 + (threadIdx.x >> 4);
+  const int g = threadIdx.x >> 4;
+  const int row0 = blockIdx.x * (16 * ADALN_RPG) + g;
   const int k0 = (threadIdx.x & 15) * 8;
+  const bf16_t* wb = (const bf16_t*)args.w[blk];
+  uint4 w[ADALN_RPG];
+#pragma unroll
+  for (int j = 0; j < ADALN_RPG; ++j) {
+    const int rr = min(row0 + 16 * j, d6 - 1);   // every lane joins the exchange
+    w[j] = *reinterpret_cast<const uint4*>(wb + (int64_t)rr * 128 + k0);
+  }
   float sl[8];
 #pragma unroll
   for (int e = 0; e < 8; ++e) {
     const float t = temb[k0 + e];
     sl[e] = t / (1.0f + expf(-t));
   }
-  const int rr = min(row, d6 - 1);             // every lane joins the exchange
-  const uint4 w = *reinterpret_cast<const uint4*>((const bf16_t*)args.w[blk] + (int64_t)rr * 128 + k0);
-  const uint32_t p[4] = {w.x, w.y, w.z, w.w};
-  float acc = 0.0f;
+  const bf16_t* bb = (const bf16_t*)args.b[blk];
 #pragma unroll
-  for (int e = 0; e < 4; ++e) {
-    acc = fmaf(__uint_as_float(p[e] << 16), sl[2 * e], acc);
-    acc = fmaf(__uint_as_float(p[e] & 0xFFFF0000u), sl[2 * e + 1], acc);
+  for (int j = 0; j < ADALN_RPG; ++j) {
+    const uint32_t p[4] = {w[j].x, w[j].y, w[j].z, w[j].w};
+    float acc = 0.0f;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      acc = fmaf(__uint_as_float(p[e] << 16), sl[2 * e], acc);
+      acc = fmaf(__uint_as_float(p[e] & 0xFFFF0000u), sl[2 * e + 1], acc);
+    }
+    acc += __shfl_xor(acc, 1);
+    acc += __shfl_xor(acc, 2);
+    acc += __shfl_xor(acc, 4);
+    acc += __shfl_xor(acc, 8);
+    const int row = row0 + 16 * j;
+    if ((threadIdx.x & 15) == 0 && row < d6)
+      mod[(int64_t)blk * d6 + row] = acc + bf16_to_f32(bb[row]);
   }
-  acc += __shfl_xor(acc, 1);
-  acc += __shfl_xor(acc, 2);
-  acc += __shfl_xor(acc, 4);
-  acc += __shfl_xor(acc, 8);
-  if ((threadIdx.x & 15) == 0 && row < d6)
-    mod[(int64_t)blk * d6 + row] = acc + bf16_to_f32(((const bf16_t*)args.b[blk])[row]);
 }
 
 hipError_t launch_adaln(int dtype, const AdalnArgs& a, int n_blk, const float* temb,
                         int d_temb, int d6, float* mod, hipStream_t st) {
   if (dtype == 1 && d_temb == 128) {
-    hipLaunchKernelGGL(adaln_bf16_t128, dim3((d6 + 15) / 16, n_blk), dim3(256), 0, st, a, temb,
-                       d6, mod);
+    hipLaunchKernelGGL(adaln_bf16_t128, dim3((d6 + 16 * ADALN_RPG - 1) / (16 * ADALN_RPG), n_blk),
+                       dim3(256), 0, st, a, temb, d6, mod);
     return hipGetLastError();
   }
   dim3 grid((d6 + 3) / 4, n_blk);
