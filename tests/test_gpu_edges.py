@@ -1,7 +1,8 @@
 """Degenerate cases of the step on the GPU against the oracle (fp32, outputs
 1e-4 max-relative, selection bit-exact, pruned rows byte-identical): no
 retained future token, no context, a single 7-token frame, two-token frames,
-one action query per frame, a mass threshold of 1, and a zero-row block."""
+one action query per frame, a mass threshold of 1, the most blocks a model may
+have (64: every layer scored, K_layer of 64 reduced), and a zero-row block."""
 import numpy as np
 import pytest
 import torch
@@ -20,6 +21,7 @@ CASES = {
     "two_token_frames": BASE.replace(frame_h=1, frame_w=2, k_core=1, k_anchor=1),
     "one_query_per_frame": BASE.replace(n_act=2),
     "mass_threshold_one": BASE.replace(mass_threshold=1.0, k_core=64, k_anchor=0),
+    "max_blocks": BASE.replace(n_blocks=64),
 }
 
 

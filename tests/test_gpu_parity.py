@@ -453,6 +453,45 @@ def test_score_reduce_max_tokens_per_frame(name):
         assert maxrel(host(A).reshape(cfg.batch, cfg.n_s)[b], r.A) < 1e-5
 
 
+# the other declared limits at once: 64 sequences of 64 future frames each,
+# scored by 64 layers (small frames of 3 x 5 tokens, one action query per frame)
+LIMITS = {
+    "fixed": W.preset(2).replace(name="limits-fixed", batch=64, n_blocks=64, d_model=64, n_heads=1,
+                                 n_ctx=4, n_frames=64, frame_h=3, frame_w=5, n_act=64, k_core=6,
+                                 k_anchor=3),
+    "mass": W.preset(2).replace(name="limits-mass", batch=64, n_blocks=64, d_model=64, n_heads=1,
+                                n_ctx=4, n_frames=64, frame_h=3, frame_w=5, n_act=64, k_core=6,
+                                k_anchor=3, mass_threshold=0.5),
+}
+
+
+@pytest.mark.parametrize("name", list(LIMITS))
+def test_select_bitexact_at_batch_frame_and_block_limits(name):
+    cfg = LIMITS[name]
+    assert (cfg.batch, cfg.n_frames, cfg.n_blocks) == (64, 64, 64)
+    _select_case(cfg, 76)
+
+
+def test_score_reduce_at_batch_frame_and_block_limits():
+    cfg = LIMITS["fixed"]
+    print(f"reduce case {cfg.name}", flush=True)
+    rng = np.random.default_rng(77)
+    S = _random_scores(rng, cfg.batch, cfg.n_blocks, cfg.n_frames, cfg.n_s)
+    ctx = _ctx(cfg)
+    V = torch.empty(cfg.batch * cfg.n_frames * cfg.n_s, dtype=torch.float32, device="cuda:0")
+    A = torch.empty(cfg.batch * cfg.n_s, dtype=torch.float32, device="cuda:0")
+    Q = torch.empty(cfg.batch * cfg.n_blocks, dtype=torch.float32, device="cuda:0")
+    core = torch.empty(cfg.batch * 6, dtype=torch.int32, device="cuda:0")
+    ctx.score_reduce(dev(S), V, A, Q, core)
+    torch.cuda.synchronize()
+    for b in range(cfg.batch):
+        r = O.score_reduce(S[b], cfg.k_layer, cfg.cv_penalty)
+        np.testing.assert_array_equal(host(core)[b * 6:(b + 1) * 6], r.L_core)
+        assert maxrel(host(Q)[b * cfg.n_blocks:(b + 1) * cfg.n_blocks], r.Q) < 1e-6
+        assert rowwise_maxrel(host(V).reshape(cfg.batch, cfg.n_frames, cfg.n_s)[b], r.V) < 1e-5
+        assert maxrel(host(A).reshape(cfg.batch, cfg.n_s)[b], r.A) < 1e-5
+
+
 @pytest.mark.parametrize("mode", ["A", "B"])
 def test_score_bf16_max_tokens_per_frame(mode):
     _score_case(MAX_FRAME["ns4096_fixed"].replace(dtype="bf16"), mode)
