@@ -295,13 +295,48 @@ gemm_bf16_nt(const bf16_t* __restrict__ A, int64_t lda, const bf16_t* __restrict
   // each wave parks one 32-row slice of its tile as fp32, then every lane
   // handles 8 consecutive columns with 16-byte loads (bias, gate, residual) and
   // a 16-byte store, so each 8 lanes write one contiguous 128-byte row run.
+  // A lane's column run is the same in every row it handles, so its bias and
+  // gate are loaded once, and each slice's residual rows are requested one
+  // slice ahead (one exposed memory latency per tile, not one per slice).
   constexpr int EP_LD = TN + 4;                       // fp32 row pitch of the staging slice
+  constexpr int CPR = TN / 8;                         // 8-column runs per slice row
+  constexpr int EP_IT = (32 * CPR + 63) / 64;         // runs per lane and slice
+  static_assert((32 * CPR) % 64 == 0, "every lane handles whole runs");
   static_assert(EPI != EPI_BIAS_QKPOST || TN == 64, "a wave's columns must be one head");
   static_assert(NW * 32 * EP_LD * 4 <= (int)sizeof(lds), "epilogue staging exceeds LDS");
   float* stage = reinterpret_cast<float*>(lds) + wave * 32 * EP_LD;
   const int col0 = n0 + wn * TN;
+  const int cl = (lane % CPR) * 8, col = col0 + cl;  // 64 is a multiple of CPR
+  const bool col_ok = col < N;
+  uint32_t bb[4] = {0u, 0u, 0u, 0u};
+  float gg[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+  uint4 res[2][EP_IT];                                // residual runs of slices i and i + 1
+  auto load_res = [&](int i, uint4 (&r)[EP_IT]) {
+#pragma unroll
+    for (int it = 0; it < EP_IT; ++it) {
+      const int row = m0 + wm * TM + i * 32 + (lane + 64 * it) / CPR;
+      r[it] = (row < M && col_ok) ? *reinterpret_cast<const uint4*>(C + (int64_t)row * ldc + col)
+                                  : make_uint4(0u, 0u, 0u, 0u);
+    }
+  };
+  if constexpr (EPI != EPI_PARTIAL && EPI != EPI_BIAS_QKPOST) {
+    if (col_ok) {
+      const uint4 bw = *reinterpret_cast<const uint4*>(bias + col);
+      bb[0] = bw.x; bb[1] = bw.y; bb[2] = bw.z; bb[3] = bw.w;
+      if constexpr (EPI == EPI_BIAS_GATED_RESIDUAL) {
+        const float4 g0 = *reinterpret_cast<const float4*>(gate + col);
+        const float4 g1 = *reinterpret_cast<const float4*>(gate + col + 4);
+        gg[0] = g0.x; gg[1] = g0.y; gg[2] = g0.z; gg[3] = g0.w;
+        gg[4] = g1.x; gg[5] = g1.y; gg[6] = g1.z; gg[7] = g1.w;
+      }
+    }
+    if constexpr (EPI == EPI_BIAS_GATED_RESIDUAL) load_res(0, res[0]);
+  }
 #pragma unroll
   for (int i = 0; i < FM; ++i) {
+    // the next slice's residual rows are requested before this slice is parked
+    if constexpr (EPI == EPI_BIAS_GATED_RESIDUAL)
+      if (i + 1 < FM) load_res(i + 1, res[(i + 1) & 1]);
 #pragma unroll
     for (int j = 0; j < FN; ++j)
 #pragma unroll
@@ -313,34 +348,26 @@ gemm_bf16_nt(const bf16_t* __restrict__ A, int64_t lda, const bf16_t* __restrict
     __builtin_amdgcn_wave_barrier();
     const int row0 = m0 + wm * TM + i * 32;
 #pragma unroll
-    for (int c = lane; c < 32 * TN / 8; c += 64) {
-      const int rl = c / (TN / 8), cl = (c % (TN / 8)) * 8;
-      const int row = row0 + rl, col = col0 + cl;
+    for (int it = 0; it < EP_IT; ++it) {
+      const int rl = (lane + 64 * it) / CPR;
+      const int row = row0 + rl;
       if constexpr (EPI == EPI_BIAS_QKPOST) {
         qkpost_store(stage + rl * EP_LD + cl, bias, C, ldc, row, col, col0, M, N, qp);
         continue;
       }
-      if (EPI == EPI_PARTIAL && row < M && col < N) {
+      if (EPI == EPI_PARTIAL && row < M && col_ok) {
         // fp32 partial sums of this K slice: part[slice][M][N]
         float* q = part + ((int64_t)blockIdx.y * M + row) * N + col;
         reinterpret_cast<float4*>(q)[0] = *reinterpret_cast<const float4*>(stage + rl * EP_LD + cl);
         reinterpret_cast<float4*>(q)[1] = *reinterpret_cast<const float4*>(stage + rl * EP_LD + cl + 4);
-      } else if (EPI != EPI_PARTIAL && row < M && col < N) {
+      } else if (EPI != EPI_PARTIAL && row < M && col_ok) {
         const float4 v0 = *reinterpret_cast<const float4*>(stage + rl * EP_LD + cl);
         const float4 v1 = *reinterpret_cast<const float4*>(stage + rl * EP_LD + cl + 4);
         const float v[8] = {v0.x, v0.y, v0.z, v0.w, v1.x, v1.y, v1.z, v1.w};
-        const uint4 bw = *reinterpret_cast<const uint4*>(bias + col);
-        const uint32_t bb[4] = {bw.x, bw.y, bw.z, bw.w};
-        bf16_t* p = C + (int64_t)row * ldc + col;
         uint32_t rr[4] = {0u, 0u, 0u, 0u};
-        float gg[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-        if (EPI == EPI_BIAS_GATED_RESIDUAL) {
-          const uint4 rw = *reinterpret_cast<const uint4*>(p);
+        if constexpr (EPI == EPI_BIAS_GATED_RESIDUAL) {
+          const uint4 rw = res[i & 1][it];
           rr[0] = rw.x; rr[1] = rw.y; rr[2] = rw.z; rr[3] = rw.w;
-          const float4 g0 = *reinterpret_cast<const float4*>(gate + col);
-          const float4 g1 = *reinterpret_cast<const float4*>(gate + col + 4);
-          gg[0] = g0.x; gg[1] = g0.y; gg[2] = g0.z; gg[3] = g0.w;
-          gg[4] = g1.x; gg[5] = g1.y; gg[6] = g1.z; gg[7] = g1.w;
         }
         uint32_t out[4];
 #pragma unroll
@@ -350,7 +377,8 @@ gemm_bf16_nt(const bf16_t* __restrict__ A, int64_t lda, const bf16_t* __restrict
           out[e] = pack_bf16x2(epi_value<EPI>(v[2 * e], b0, gg[2 * e], x0),
                                epi_value<EPI>(v[2 * e + 1], b1, gg[2 * e + 1], x1));
         }
-        *reinterpret_cast<uint4*>(p) = make_uint4(out[0], out[1], out[2], out[3]);
+        *reinterpret_cast<uint4*>(C + (int64_t)row * ldc + col) =
+            make_uint4(out[0], out[1], out[2], out[3]);
       }
     }
     __builtin_amdgcn_wave_barrier();
