@@ -715,7 +715,7 @@ def second_point(dev, reps):
            "schedule_tokens_per_s_from_medians": round(cfg.l_full / sched * 1e3, 1)}
     for k in ("dense_step_ms", "refresh_step_ms", "sparse_step_ms", "dense_tokens_per_s",
               "sparse_tokens_per_s", "speedup_sparse_vs_dense", "overhead_pct_of_dense",
-              "overhead_exposed_pct_of_dense", "roofline_by_class"):
+              "overhead_exposed_pct_of_dense", "roofline", "roofline_by_class"):
         out[k] = m[k]
     del model, xs
     torch.cuda.empty_cache()
