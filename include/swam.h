@@ -459,8 +459,8 @@ enum {
 /* Bracket every launch (phase) of the classes in `mask` (bit i = class i)
  * with HIP events on the stream it runs on; mask 0 disables.  Enabling
  * allocates an event pool of `capacity` pairs (dropped beyond that) and
- * restarts the per-class launch counts of swam_timer_stride.  Each bracket
- * costs the stream a few microseconds. */
+ * restarts the per-class launch counts of swam_timer_stride (the stride
+ * itself is kept).  Each bracket costs the stream a few microseconds. */
 int swam_timer_enable(swam_ctx* ctx, uint32_t mask, int32_t capacity);
 /* Forget the recorded brackets and restart the launch counts. */
 int swam_timer_reset(swam_ctx* ctx);
