@@ -528,13 +528,6 @@ static hipError_t run_bf16(const void* A, int64_t lda, const void* B, int64_t ld
 // dropped.)
 struct GemmPlan { int tile, splits; };
 static GemmPlan choose_gemm(int64_t M, int64_t N, int64_t K, int64_t ws_floats) {
-  static int forced = -2, forced_split = -2;
-  if (forced == -2) {
-    const char* e = getenv("SWAM_GEMM_TILE");
-    forced = e ? atoi(e) : -1;
-    const char* f = getenv("SWAM_GEMM_SPLIT");
-    forced_split = f ? atoi(f) : -1;
-  }
   struct Cand { int bm, bn, per_cu; double eff; };
   const Cand c[3] = {{256, 256, 1, 1.0}, {128, 128, 2, 0.80}, {192, 256, 1, 0.85}};
   const int split_opts[6] = {1, 2, 3, 4, 6, 8};
@@ -543,10 +536,8 @@ static GemmPlan choose_gemm(int64_t M, int64_t N, int64_t K, int64_t ws_floats) 
   GemmPlan best{0, 1};
   double best_t = 1e30;
   for (int i = 0; i < 3; ++i) {
-    if (forced >= 0 && forced <= 2 && i != forced) continue;
     const int64_t tiles = ((M + c[i].bm - 1) / c[i].bm) * ((N + c[i].bn - 1) / c[i].bn);
     for (int s : split_opts) {
-      if (forced_split >= 1 && s != forced_split) continue;
       if (s > 1 && (kt / s < 4 || (int64_t)s * M * N > ws_floats)) continue;
       const int64_t wgs = tiles * s;
       double rounds;
