@@ -87,3 +87,26 @@ def test_timer_counts_by_kind_and_stride():
         ctx.timer_stride(0)
     with pytest.raises(swam.SwamError):
         ctx.timer_read("ATTN", 7)
+
+
+def test_captured_steps_are_not_bracketed():
+    """Launches recorded into a HIP graph (and its replays) take no event
+    brackets; an eager step on the same context still does."""
+    from paper_2609_38984_amd import swam
+    cfg = CFG
+    blocks, _, model = model_for(cfg)
+    inp = W.make_inputs(cfg, blocks[0]["w_qkv"])
+    stream = torch.cuda.Stream()
+    with torch.cuda.stream(stream):
+        ctx = swam.Context(cfg, stream=stream)
+        ctx.timer_enable(["ATTN"], capacity=64)
+        x = dev(inp.x(0))
+        y = torch.empty_like(x)
+        temb = dev(inp.temb(0))
+        for tau in range(4):                 # refresh and sparse captured, then replayed
+            ctx.step_graph(model, x, temb, tau, y)
+        stream.synchronize()
+        assert ctx.timer_read("ATTN")[0] == 0
+        ctx.step(model, x, temb, 0, y)
+        stream.synchronize()
+        assert ctx.timer_read("ATTN", swam.KIND_REFRESH)[0] == cfg.n_blocks
