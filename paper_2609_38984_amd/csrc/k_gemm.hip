@@ -12,7 +12,7 @@
 // Split K: when the output tiles cannot fill the 256 CUs (few rows, or a
 // narrow N), grid.y workgroups share a tile along K, store fp32 partial sums,
 // and one memory-bound pass sums them and applies the epilogue.
-#include "launchers.h"
+#include "score_unit.h"
 
 #include <algorithm>
 
@@ -191,12 +191,16 @@ __device__ __forceinline__ void mma_stage(const uint4* __restrict__ as, const ui
 // all.
 // ROLE (a GemmRole) only names the instantiation after the block's
 // projection, so a kernel trace tells the four projections apart.
-template <int ROLE, int BM, int BN, int WM, int WN, int EPI>
+// SC: workgroups past the tile count (the grid's tail) score one layer
+// instead (scoring units of score_unit.h, two per 8-wave workgroup at a time),
+// on the CUs that the last round of tiles leaves idle; sa / n_units describe
+// that work.
+template <int ROLE, int BM, int BN, int WM, int WN, int EPI, bool SC = false>
 __global__ void __launch_bounds__(WM * WN * 64)
 gemm_bf16_nt(const bf16_t* __restrict__ A, int64_t lda, const bf16_t* __restrict__ B,
              int64_t ldb, const bf16_t* __restrict__ bias, const float* __restrict__ gate,
              bf16_t* C, int64_t ldc, int M, int N, int K, int tiles_m, int tiles_n,
-             float* __restrict__ part, const QkPost qp) {
+             float* __restrict__ part, const QkPost qp, const ScoreArgs sa, int n_units) {
   constexpr int NW = WM * WN;
   constexpr int TM = BM / WM, TN = BN / WN;
   constexpr int FM = TM / 32, FN = TN / 32;
@@ -204,11 +208,28 @@ gemm_bf16_nt(const bf16_t* __restrict__ A, int64_t lda, const bf16_t* __restrict
   static_assert(A_INS * 8 * NW == BM && B_INS * 8 * NW == BN, "tile/waves mismatch");
   __shared__ uint4 lds[2 * (BM + BN) * 8];   // [stage][A rows | B rows][8 chunks]
 
-  int tm, tn;
-  tile_of(blockIdx.x, gridDim.x, tiles_m, tiles_n, tm, tn);
-  const int m0 = tm * BM, n0 = tn * BN;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave-uniform
+  const int n_tiles = tiles_m * tiles_n;
+  if constexpr (SC) {
+    static_assert(NW % 4 == 0, "scoring units take groups of four waves");
+    if ((int)blockIdx.x >= n_tiles) {
+      constexpr int G = NW / 4;
+      const int group = wave >> 2;
+      float (*sp)[16] = reinterpret_cast<float (*)[16]>(lds) + 4 * group;
+      const int nsw = (int)gridDim.x - n_tiles;
+      for (int base = ((int)blockIdx.x - n_tiles) * G; base < n_units; base += nsw * G) {
+        __syncthreads();                 // the previous units' partial sums are consumed
+        const int unit = base + group;
+        score_unit_bf16(sa, unit, unit < n_units, wave & 3, lane, tid & 255, sp,
+                        [] { __syncthreads(); });
+      }
+      return;
+    }
+  }
+  int tm, tn;
+  tile_of(blockIdx.x, n_tiles, tiles_m, tiles_n, tm, tn);
+  const int m0 = tm * BM, n0 = tn * BN;
   const int wm = wave / WN, wn = wave % WN;
   const int lrow = lane >> 3;
 
@@ -491,7 +512,7 @@ static hipError_t run_bf16(const void* A, int64_t lda, const void* B, int64_t ld
     hipLaunchKernelGGL((gemm_bf16_nt<ROLE, BM, BN, WM, WN, EPI>), dim3(tiles_m * tiles_n),
                        dim3(WM * WN * 64), 0, st, (const bf16_t*)A, lda, (const bf16_t*)B, ldb,
                        (const bf16_t*)bias, gate, (bf16_t*)C, ldc, M, N, K, tiles_m, tiles_n,
-                       (float*)nullptr, qp);
+                       (float*)nullptr, qp, ScoreArgs{}, 0);
     return hipGetLastError();
   }
   if constexpr (EPI == EPI_BIAS_QKPOST) {
@@ -500,7 +521,7 @@ static hipError_t run_bf16(const void* A, int64_t lda, const void* B, int64_t ld
     hipLaunchKernelGGL((gemm_bf16_nt<ROLE, BM, BN, WM, WN, EPI_PARTIAL>), dim3(tiles_m * tiles_n, splits),
                        dim3(WM * WN * 64), 0, st, (const bf16_t*)A, lda, (const bf16_t*)B, ldb,
                        (const bf16_t*)bias, gate, (bf16_t*)C, ldc, M, N, K, tiles_m, tiles_n, part,
-                       QkPost{});
+                       QkPost{}, ScoreArgs{}, 0);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     const int64_t n = (int64_t)M * (N / 8);
@@ -569,6 +590,55 @@ static hipError_t dispatch_bf16(const void* A, int64_t lda, const void* B, int64
   if (p.tile == 2)
     return run_bf16<ROLE, 192, 256, 2, 4, EPI>(A, lda, B, ldb, bias, gate, C, ldc, M, N, K, p.splits, ws, st);
   return run_bf16<ROLE, 128, 128, 2, 2, EPI>(A, lda, B, ldb, bias, gate, C, ldc, M, N, K, p.splits, ws, st);
+}
+
+// The MLP up projection with one layer's scoring in the tail of its grid:
+// the scoring workgroups are dispatched after every tile, i.e. into the last
+// round, on the CUs its tiles leave idle there (at least 16 of them, or the
+// caller scores on its side stream instead).
+static int scored_idle_slots(const GemmPlan& p, int64_t M, int64_t N) {
+  static const int bm[3] = {256, 128, 192}, bn[3] = {256, 128, 256}, per_cu[3] = {1, 2, 1};
+  if (p.splits != 1) return 0;
+  const int64_t tiles = ((M + bm[p.tile] - 1) / bm[p.tile]) * ((N + bn[p.tile] - 1) / bn[p.tile]);
+  const int64_t slots = 256 * per_cu[p.tile];
+  const int64_t idle = (slots - tiles % slots) % slots;
+  return idle >= 16 ? (int)idle : 0;
+}
+
+int gemm_up_scored_slots(int64_t M, int64_t N, int64_t K, int64_t ws_floats) {
+  if (M <= 0) return 0;
+  return scored_idle_slots(choose_gemm(M, N, K, ws_floats), M, N);
+}
+
+template <int BM, int BN, int WM, int WN>
+static hipError_t run_up_scored(const void* A, int64_t lda, const void* B, int64_t ldb,
+                                const void* bias, void* C, int64_t ldc, int M, int N, int K,
+                                const ScoreArgs& sa, int n_sw, hipStream_t st) {
+  const int tiles_m = (M + BM - 1) / BM, tiles_n = (N + BN - 1) / BN;
+  const int ktiles = (sa.n_s + 15) / 16;
+  const int n_units = (sa.n_layers < 1 ? 1 : sa.n_layers) * sa.B * sa.F * ktiles;
+  constexpr int G = WM * WN / 4;
+  n_sw = std::min(n_sw, (n_units + G - 1) / G);
+  hipLaunchKernelGGL((gemm_bf16_nt<ROLE_UP, BM, BN, WM, WN, EPI_BIAS_GELU, true>),
+                     dim3(tiles_m * tiles_n + n_sw), dim3(WM * WN * 64), 0, st, (const bf16_t*)A,
+                     lda, (const bf16_t*)B, ldb, (const bf16_t*)bias, (const float*)nullptr,
+                     (bf16_t*)C, ldc, M, N, K, tiles_m, tiles_n, (float*)nullptr, QkPost{}, sa,
+                     n_units);
+  return hipGetLastError();
+}
+
+hipError_t launch_gemm_up_scored(const void* A, int64_t lda, const void* B, int64_t ldb,
+                                 const void* bias, void* C, int64_t ldc, int64_t M, int64_t N,
+                                 int64_t K, const ScoreArgs& sa, hipStream_t st,
+                                 int64_t ws_floats) {
+  if (M <= 0) return hipSuccess;
+  const GemmPlan p = choose_gemm(M, N, K, ws_floats);
+  const int n_sw = scored_idle_slots(p, M, N);
+  if (n_sw == 0) return hipErrorNotSupported;
+  const int m = (int)M, n = (int)N, k = (int)K;
+  if (p.tile == 0) return run_up_scored<256, 256, 2, 4>(A, lda, B, ldb, bias, C, ldc, m, n, k, sa, n_sw, st);
+  if (p.tile == 2) return run_up_scored<192, 256, 2, 4>(A, lda, B, ldb, bias, C, ldc, m, n, k, sa, n_sw, st);
+  return run_up_scored<128, 128, 2, 2>(A, lda, B, ldb, bias, C, ldc, m, n, k, sa, n_sw, st);
 }
 
 template <int EPI>

@@ -5,95 +5,26 @@
 // against a stream of keys), so it is bound by the single read of the future
 // keys; MFMA only keeps the dot products off the VALU.
 //
-// One launch may score several layers (layer strides in ScoreArgs); the
-// refresh step launches one layer at a time, right after that layer's
-// attention, while its q, k and lambda are fresh.
+// One launch may score several layers (layer strides in ScoreArgs); a
+// bf16 refresh step scores each layer inside that layer's MLP up projection
+// launch (the same units, score_unit.h) and the last layer with this kernel.
 //
-// bf16: workgroup = 4 waves on 16 keys of one frame.  Each wave takes every
-// 4th head: two 16x16x32 MFMAs per head with the keys as the A operand
-// (lane -> key lane&15, 8 hd at 8*(lane>>4)) and the group's queries as the
-// B operand, so the accumulator gives each lane one query (lane & 15) and
-// four keys.  exp2 of the scaled logit minus the query's normaliser is
-// weighted by alpha (0 for padding queries), summed over the wave's heads in
-// registers, reduced over queries with lane shuffles and over waves in LDS in
-// a fixed order (deterministic).
+// bf16: workgroup = 4 waves on 16 keys of one frame (score_unit.h); the MLP
+// up projection of a refresh step can run the same units in extra
+// workgroups of its own launch instead.
 // fp32: one thread per key.
 // Mode B normaliser: lambda over all keys of the sequence, per (query, head),
 // as an online max/sum split over key chunks with wavefront-shuffle
 // reductions, combined in a second pass.
-#include "launchers.h"
+#include "score_unit.h"
 
 namespace swam {
 
-constexpr float LOG2E = 1.4426950408889634f;
-
-__global__ void __launch_bounds__(256)
-score_bf16(const bf16_t* __restrict__ q, int64_t q_seq, int64_t q_row,
-           const bf16_t* __restrict__ k, int64_t k_seq, int64_t k_row,
-           const float* __restrict__ lse, int64_t lse_seq, float* __restrict__ s_out,
-           int64_t s_seq, const float* __restrict__ alpha, int B, int F, int n_s, int H,
-           int n_heads, int64_t q_lay, int64_t k_lay, int64_t lse_lay, int64_t s_lay) {
+// one 16-key unit per workgroup of four waves
+__global__ void __launch_bounds__(256) score_bf16(const ScoreArgs a) {
   __shared__ float part[4][16];
-  const int ktiles = (n_s + 15) >> 4;
-  int bid = blockIdx.x;
-  const int kt = bid % ktiles;
-  bid /= ktiles;
-  const int f = bid % F;
-  bid /= F;
-  const int b = bid % B;
-  const int layer = bid / B;
-  q += layer * q_lay;
-  k += layer * k_lay;
-  lse += layer * lse_lay;
-  s_out += layer * s_lay;
-  const int g = H / F;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int j0 = kt * 16;
-  const int key = min(j0 + (lane & 15), n_s - 1);
-  const bf16_t* kp = k + b * k_seq + (int64_t)(f * n_s + key) * k_row + 8 * (lane >> 4);
-  const int qi = lane & 15;                 // query slot within the group (C column)
-  const int ql = min(qi, g - 1);            // loaded row (padding slots reuse a valid row)
-  const float aw = qi < g ? alpha[qi] : 0.0f;
-  const int qa = f * g + ql;
-  const bf16_t* qp = q + b * q_seq + (int64_t)qa * q_row + 8 * (lane >> 4);
-  const float* lp = lse + (int64_t)b * lse_seq + (int64_t)qa * n_heads;
-
-  float acc[4] = {0.f, 0.f, 0.f, 0.f};
-  for (int h = wave; h < n_heads; h += 4) {
-    const bf16x8 k0 = __builtin_bit_cast(bf16x8, *(const uint4*)(kp + h * 64));
-    const bf16x8 k1 = __builtin_bit_cast(bf16x8, *(const uint4*)(kp + h * 64 + 32));
-    const bf16x8 q0 = __builtin_bit_cast(bf16x8, *(const uint4*)(qp + h * 64));
-    const bf16x8 q1 = __builtin_bit_cast(bf16x8, *(const uint4*)(qp + h * 64 + 32));
-    f32x4 c = {0.f, 0.f, 0.f, 0.f};
-    c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k0, q0, c, 0, 0, 0);
-    c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k1, q1, c, 0, 0, 0);
-    const float lam = lp[h] * LOG2E;
-#pragma unroll
-    for (int r = 0; r < 4; ++r) acc[r] += aw * exp2f(c[r] * (0.125f * LOG2E) - lam);
-  }
-  // sum over the 16 query columns (lanes with equal lane >> 4)
-#pragma unroll
-  for (int r = 0; r < 4; ++r) {
-    float v = acc[r];
-    v += __shfl_xor(v, 8);
-    v += __shfl_xor(v, 4);
-    v += __shfl_xor(v, 2);
-    v += __shfl_xor(v, 1);
-    acc[r] = v;
-  }
-  if ((lane & 15) == 0) {
-#pragma unroll
-    for (int r = 0; r < 4; ++r) part[wave][4 * (lane >> 4) + r] = acc[r];
-  }
-  __syncthreads();
-  if (threadIdx.x < 16) {
-    const int j = j0 + threadIdx.x;
-    if (j < n_s) {
-      const float s = ((part[0][threadIdx.x] + part[1][threadIdx.x]) +
-                       (part[2][threadIdx.x] + part[3][threadIdx.x])) / (float)n_heads;
-      s_out[(int64_t)b * s_seq + (int64_t)f * n_s + j] = s;
-    }
-  }
+  score_unit_bf16(a, (int)blockIdx.x, true, (int)(threadIdx.x >> 6), (int)(threadIdx.x & 63),
+                  (int)threadIdx.x, part, [] { __syncthreads(); });
 }
 
 __global__ void __launch_bounds__(256)
@@ -190,10 +121,7 @@ hipError_t launch_score(int dtype, const ScoreArgs& a, hipStream_t st) {
   const int nl = a.n_layers < 1 ? 1 : a.n_layers;
   if (dtype == 1) {
     const int ktiles = (a.n_s + 15) / 16;
-    hipLaunchKernelGGL(score_bf16, dim3(nl * a.B * a.F * ktiles), dim3(256), 0, st,
-                       (const bf16_t*)a.q, a.q_seq, a.q_row, (const bf16_t*)a.k, a.k_seq,
-                       a.k_row, a.lse, a.lse_seq, a.s_out, a.s_seq, a.alpha, a.B, a.F, a.n_s,
-                       a.H, a.n_heads, a.q_lay, a.k_lay, a.lse_lay, a.s_lay);
+    hipLaunchKernelGGL(score_bf16, dim3(nl * a.B * a.F * ktiles), dim3(256), 0, st, a);
   } else {
     const int64_t n = (int64_t)nl * a.B * a.F * a.n_s;
     hipLaunchKernelGGL(score_f32, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st,

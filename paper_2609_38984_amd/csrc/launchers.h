@@ -91,6 +91,16 @@ struct ScoreArgs {
   int64_t q_lay, k_lay, lse_lay, s_lay;   // element strides between layers
 };
 hipError_t launch_score(int dtype, const ScoreArgs& a, hipStream_t st);
+// MLP up projection (bias + GELU) of a refresh step with one layer's scores
+// (ScoreArgs, bf16) computed by extra workgroups in the tail of its grid, on
+// the CUs its last round of tiles leaves idle; gemm_up_scored_slots returns
+// how many that is for a shape (0: not applicable, the caller scores
+// separately), and launch_gemm_up_scored returns hipErrorNotSupported then.
+int gemm_up_scored_slots(int64_t M, int64_t N, int64_t K, int64_t ws_floats);
+hipError_t launch_gemm_up_scored(const void* A, int64_t lda, const void* B, int64_t ldb,
+                                 const void* bias, void* C, int64_t ldc, int64_t M, int64_t N,
+                                 int64_t K, const ScoreArgs& sa, hipStream_t st,
+                                 int64_t ws_floats);
 hipError_t launch_lse_all(int dtype, const void* q, int64_t q_seq, int64_t q_row,
                           const void* kall, int64_t k_seq, int64_t k_row, int64_t n_keys,
                           int B, int H, int n_heads, float* lse_out, float* part_ws,

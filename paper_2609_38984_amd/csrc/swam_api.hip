@@ -308,10 +308,12 @@ bool bad_block(const swam_block_weights* w) {
 // pruned_dst (with pack_src, out of place): the pruned rows of pack_src are
 // copied into it on the side stream, forked after that LayerNorm so the copy
 // overlaps the QKV projection rather than the pack
+// score_in_up (with score): the scoring runs in the tail of the MLP up
+// projection's grid instead of on the side stream (no fork or join)
 int run_block(swam_ctx* c, const swam_block_weights* w, const float* mod, void* x,
               int64_t n_rows, const int32_t* cu, int n_seqs, float* lse_out, void* qkv,
               int pos_mode, const ScoreArgs* score = nullptr, const void* pack_src = nullptr,
-              void* pruned_dst = nullptr) {
+              void* pruned_dst = nullptr, bool score_in_up = false) {
   const int dt = c->cfg.dtype;
   const int64_t d = c->dv.d, hid = c->dv.hidden;
   void* h = c->ptr<char>(c->lay.h);
@@ -364,7 +366,7 @@ int run_block(swam_ctx* c, const swam_block_weights* w, const float* mod, void* 
     SWAM_HIP(c, launch_attention(dt, qkv, o, lse_out, cu, n_seqs, n_rows, c->cfg.n_heads, st),
              "attention");
   }
-  if (score) {
+  if (score && !score_in_up) {
     // fork: the scores of this layer run on the side stream, concurrently
     // with the rest of the block (memory-bound next to MFMA-bound GEMMs)
     SWAM_HIP(c, hipEventRecord(c->ev_attn, st), "fork scoring");
@@ -385,7 +387,13 @@ int run_block(swam_ctx* c, const swam_block_weights* w, const float* mod, void* 
     Timed t(c, SWAM_T_LNMOD);
     SWAM_HIP(c, launch_ln_mod(dt, x, h, sh2, sc2, n_rows, (int)d, st), "ln_mod 2");
   }
-  {
+  if (score && score_in_up) {
+    // this layer's q, k and lambda stay in place until the next block's QKV
+    // projection, which the stream orders after this launch
+    Timed t(c, SWAM_T_GEMM_UP);
+    SWAM_HIP(c, launch_gemm_up_scored(h, d, w->w_1, d, w->b_1, u, hid, n_rows, hid, d, *score,
+                                      st, sk ? sk_n : 0), "gemm up + scoring");
+  } else {
     Timed t(c, SWAM_T_GEMM_UP);
     SWAM_HIP(c, launch_gemm(dt, ROLE_UP, h, d, w->w_1, d, w->b_1, nullptr, u, hid, n_rows,
                             hid, d, st, sk, sk_n), "gemm up");
@@ -1012,12 +1020,18 @@ int enqueue_step_launches(swam_ctx* c, const swam_model* model, const void* x_fu
       a.n_heads = cf.n_heads;
       a.n_layers = 1;
     }
+    // bf16: every layer but the last scores in the tail of its MLP up
+    // projection where that grid leaves CUs idle; the last layer scores on the
+    // side stream, so that the reduction and selection can follow it there
+    const bool in_up = score && cf.dtype == SWAM_BF16 &&
+                       gemm_up_scored_slots(c->dv.rows_full, c->dv.hidden, d,
+                                            c->dv.splitk_floats) > 0;
     for (int l = 0; l < cf.n_blocks; ++l) {
       a.s_out = c->ptr<float>(c->lay.s_all) + (int64_t)l * cf.n_frames * c->dv.n_s;
       rc = run_block(c, &model->blocks[l], mod + (int64_t)l * 6 * d, y_full, c->dv.rows_full,
                      c->ptr<int32_t>(c->lay.cu_dense), cf.batch,
                      score ? c->ptr<float>(c->lay.lse) : nullptr, qkv, 0,
-                     score ? &a : nullptr);
+                     score ? &a : nullptr, nullptr, nullptr, in_up && l + 1 < cf.n_blocks);
       if (rc != SWAM_OK) return rc;
     }
     if (score) {
