@@ -212,6 +212,47 @@ def test_step_wam_fullsize_properties():
     assert torch.equal(y0b.view(torch.int16), y0.view(torch.int16)) and torch.equal(S2, S)
 
 
+def test_refresh_scores_equal_layerwise_scoring_fullsize():
+    """At the WAM shape a bf16 refresh scores every layer but the last inside
+    its MLP up projection launch and the last one with the scoring kernel on
+    the side stream.  Chaining the blocks one call at a time and scoring each
+    layer's own q, k and lambda with the standalone kernel must give the same
+    S bit for bit (the same scoring arithmetic in a fixed order), and the same
+    step output."""
+    from paper_2609_38984_amd import swam
+    cfg = W.preset(3).replace(n_blocks=4)
+    print(f"refresh scores vs layerwise scoring {cfg.name} L={cfg.n_blocks}", flush=True)
+    blocks, dblocks, model = model_for(cfg)
+    inp = W.make_inputs(cfg, blocks[0]["w_qkv"])
+    ctx = _ctx(cfg)
+    assert cfg.batch == 1 and ctx.n_scored == 1
+    x0, t0 = dev(inp.x(0), torch.bfloat16), dev(inp.temb(0))
+    y0 = torch.empty_like(x0)
+    assert ctx.step(model, x0, t0, 0, y0) == swam.KIND_REFRESH
+    n_s, F, L, d = cfg.n_s, cfg.n_frames, cfg.n_blocks, cfg.d_model
+    S = torch.empty(L * F * n_s, dtype=torch.float32, device="cuda:0")
+    ctx.export(s_all=S)
+    act0 = cfg.n_ctx + cfg.n_fut
+    ld = 3 * d
+    x = x0.clone()
+    lse = torch.empty(cfg.l_full, cfg.n_heads, dtype=torch.float32, device="cuda:0")
+    qkv = torch.empty(cfg.l_full, ld, dtype=torch.bfloat16, device="cuda:0")
+    S_lay = torch.empty(L, F * n_s, dtype=torch.float32, device="cuda:0")
+    ctx2 = _ctx(cfg)
+    for l in range(L):
+        ctx2.block(dblocks[l], t0, x, None, None, 0, lse, qkv)
+        flat = qkv.view(-1)
+        ctx2.score(flat[act0 * ld:], cfg.l_full * ld, ld, flat[cfg.n_ctx * ld + d:],
+                   cfg.l_full * ld, ld, S_lay[l], lse_act=lse[act0:].contiguous())
+    torch.cuda.synchronize()
+    Sh, Lh = host(S).reshape(L, F, n_s), host(S_lay).reshape(L, F, n_s)
+    for l in range(L):
+        diff = float(np.abs(Sh[l] - Lh[l]).max())
+        print(f"  layer {l}: max |S_step - S_layer| {diff:.3e}", flush=True)
+    assert torch.equal(S.view(L, -1), S_lay)
+    assert torch.equal(y0.view(torch.int16), x.view(torch.int16))
+
+
 def test_attention_normalisers_sum_to_one_fullsize():
     """sum over all keys of exp(q.k/8 - lambda) = 1 for the action rows, with the
     kernel's own q, k and lambda (a property at any size)."""
