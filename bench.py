@@ -978,6 +978,103 @@ def summarize_mfma(db_path, bench_json):
     return "\n".join(lines)
 
 
+def library_comparison(args):
+    """Same-process comparison with the libraries torch ships, at the workload's
+    dense and packed row counts: our attention and projections (per-class HIP
+    events around the launches of swam_block, one block, 30 calls) against
+    torch's flash and memory-efficient SDPA (same heads, head dim 64, one
+    sequence, no normaliser output) and F.linear (hipBLASLt; bias only, where
+    ours also fuses GELU or gate + residual).  Two interleaved passes; ours are
+    averages over the bracketed launches, the libraries' over 30 back-to-back
+    calls.  Only the comparison calls the libraries; the step never does."""
+    import torch
+    import workload as W
+    from paper_2609_38984_amd import swam
+    from torch.nn.attention import SDPBackend, sdpa_kernel
+    cfg = workload_from_args(args).replace(n_blocks=1)
+    if cfg.dtype != "bf16" or cfg.batch != 1 or cfg.t_pack_fixed is None:
+        sys.exit("--libcmp: bf16 workloads of one sequence with a fixed token budget only")
+    dev = torch.device("cuda:0")
+    d, hid, nh = cfg.d_model, cfg.mlp_ratio * cfg.d_model, cfg.n_heads
+    blocks_np, model = load_model(cfg, dev, torch.bfloat16)
+    wts = model.blocks[0]
+    temb = torch.from_numpy(W.timestep_embedding(cfg, 0)).to(dev)
+    classes = ["ATTN", "GEMM_QKV", "GEMM_OUT", "GEMM_UP", "GEMM_DOWN"]
+    reps = 30
+    gen = torch.Generator(device=dev).manual_seed(cfg.seed)
+
+    def ours(rows):
+        ctx = swam.Context(cfg)
+        x = torch.randn(rows, d, device=dev, generator=gen).to(torch.bfloat16)
+        cu = torch.tensor([0, rows], dtype=torch.int32, device=dev)
+        lse = torch.empty(rows, nh, dtype=torch.float32, device=dev)
+        qkv = torch.empty(rows, 3 * d, dtype=torch.bfloat16, device=dev)
+        for i in range(3 + reps):
+            if i == 3:
+                torch.cuda.synchronize()
+                ctx.timer_enable(classes, capacity=8 * reps)
+            ctx.block(wts, temb, x.clone(), rows, cu, 1, lse, qkv)
+        torch.cuda.synchronize()
+        res = {}
+        for c in classes:
+            n, ms = ctx.timer_read(c)
+            res[c] = 1000.0 * ms / n
+        return res
+
+    def timed(fn):
+        # back-to-back calls between one pair of events: the host's launch
+        # latency stays hidden behind the queue, which favours the library
+        # (ours carry an event pair around every launch)
+        for _ in range(3):
+            fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) * 1000.0 / reps
+
+    def libs(rows):
+        res = {}
+        q, k, v = (torch.randn(1, nh, rows, 64, device=dev, generator=gen).to(torch.bfloat16)
+                   for _ in range(3))
+        for name, be in (("ATTN_flash", SDPBackend.FLASH_ATTENTION),
+                         ("ATTN_efficient", SDPBackend.EFFICIENT_ATTENTION)):
+            try:
+                with sdpa_kernel([be]):
+                    res[name] = timed(lambda: torch.nn.functional.scaled_dot_product_attention(q, k, v))
+            except RuntimeError as ex:
+                res[name] = f"unavailable: {str(ex)[:60]}"
+        lin = torch.nn.functional.linear
+        for c, (kk, nn) in (("GEMM_QKV", (d, 3 * d)), ("GEMM_OUT", (d, d)), ("GEMM_UP", (d, hid)),
+                            ("GEMM_DOWN", (hid, d))):
+            a = torch.randn(rows, kk, device=dev, generator=gen).to(torch.bfloat16)
+            w = (torch.randn(nn, kk, device=dev, generator=gen) * kk ** -0.5).to(torch.bfloat16)
+            b = torch.zeros(nn, device=dev, dtype=torch.bfloat16)
+            res[c + "_hipblaslt"] = timed(lambda: lin(a, w, b))
+        return res
+
+    out = {"mode": "library comparison", "workload": cfg.name, "reps": reps, "passes": []}
+    for p in range(2):
+        row = {}
+        for kind, rows in (("dense", cfg.l_full), ("packed", cfg.t_pack_fixed)):
+            o, l_ = ours(rows), libs(rows)
+            row[kind] = {"rows": rows, "ours_us": {c: round(v, 2) for c, v in o.items()},
+                         "library_us": {c: (round(v, 2) if isinstance(v, float) else v)
+                                        for c, v in l_.items()}}
+            for c in classes:
+                work = kernel_work(cfg, c, [rows])
+                lib = [v for n, v in l_.items() if n.startswith(c + "_") and isinstance(v, float)]
+                best = min(lib) if lib else float("nan")
+                log(f"[libcmp] pass {p} {kind:6s} {c:9s} ours {o[c]:8.1f} us "
+                    f"({work / o[c] / 1e6:6.1f} TFLOP/s)  library {best:8.1f} us "
+                    f"({work / best / 1e6:6.1f} TFLOP/s)  ours/library {o[c] / best:5.2f}")
+        out["passes"].append(row)
+    print(json.dumps(out))
+
+
 def workload_from_json(cj):
     import workload as W
     for n in (1, 2, 3, 5):
@@ -1022,6 +1119,9 @@ def main():
     ap.add_argument("--sampler", action="store_true",
                     help="closed-loop sampling with the cached-velocity merge (own JSON line)")
     ap.add_argument("--d-latent", type=int, default=16, help="latent channels for --sampler")
+    ap.add_argument("--libcmp", action="store_true",
+                    help="our attention and projections against torch's SDPA and F.linear, "
+                         "same process (own JSON line)")
     ap.add_argument("--rope", action="store_true",
                     help="backbone variant: rotary embedding at the original positions")
     ap.add_argument("--qk-norm", action="store_true", help="backbone variant: per-head QK-norm")
@@ -1040,6 +1140,9 @@ def main():
         return
     if args.sampler:
         sampler_bench(args)
+        return
+    if args.libcmp:
+        library_comparison(args)
         return
     cfg = workload_from_args(args)
     dev = torch.device("cuda:0")
