@@ -576,6 +576,9 @@ def class_rooflines(cfg, per_kind, full_rows, packed_rows):
                             ("sparse", "UNPACK", packed_rows)):
         n, ms = per_kind.get(kind, {}).get(cls, (0, 0.0))
         if not n:
+            if cls == "UNPACK" and cfg.dtype == "bf16" and "sparse" in per_kind:
+                # the scatter rides in the last block's MLP down projection store
+                mem[cls] = {"launches_per_step": 0, "fused_into": "GEMM_DOWN"}
             continue
         us = ms * 1e3 / n
         gbs = kernel_work(cfg, cls, rows) / (us * 1e-6) / 1e9

@@ -200,7 +200,8 @@ __global__ void __launch_bounds__(WM * WN * 64)
 gemm_bf16_nt(const bf16_t* __restrict__ A, int64_t lda, const bf16_t* __restrict__ B,
              int64_t ldb, const bf16_t* __restrict__ bias, const float* __restrict__ gate,
              bf16_t* C, int64_t ldc, int M, int N, int K, int tiles_m, int tiles_n,
-             float* __restrict__ part, const QkPost qp, const ScoreArgs sa, int n_units) {
+             float* __restrict__ part, const QkPost qp, const ScoreArgs sa, int n_units,
+             bf16_t* Cs, const int32_t* __restrict__ smap) {
   constexpr int NW = WM * WN;
   constexpr int TM = BM / WM, TN = BN / WN;
   constexpr int FM = TM / 32, FN = TN / 32;
@@ -398,8 +399,10 @@ gemm_bf16_nt(const bf16_t* __restrict__ A, int64_t lda, const bf16_t* __restrict
           out[e] = pack_bf16x2(epi_value<EPI>(v[2 * e], b0, gg[2 * e], x0),
                                epi_value<EPI>(v[2 * e + 1], b1, gg[2 * e + 1], x1));
         }
-        *reinterpret_cast<uint4*>(C + (int64_t)row * ldc + col) =
-            make_uint4(out[0], out[1], out[2], out[3]);
+        bf16_t* dst = C + (int64_t)row * ldc + col;
+        if constexpr (EPI == EPI_BIAS_GATED_RESIDUAL)
+          if (smap != nullptr) dst = Cs + (int64_t)smap[row] * ldc + col;
+        *reinterpret_cast<uint4*>(dst) = make_uint4(out[0], out[1], out[2], out[3]);
       }
     }
     __builtin_amdgcn_wave_barrier();
@@ -412,7 +415,7 @@ template <int ROLE, int EPI>
 __global__ void __launch_bounds__(256)
 splitk_epilogue(const float* __restrict__ part, int splits, int M, int N,
                 const bf16_t* __restrict__ bias, const float* __restrict__ gate, bf16_t* C,
-                int64_t ldc) {
+                int64_t ldc, bf16_t* Cs, const int32_t* __restrict__ smap) {
   const int64_t id = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   const int cpr = N / 8;
   if (id >= (int64_t)M * cpr) return;
@@ -445,7 +448,9 @@ splitk_epilogue(const float* __restrict__ part, int splits, int M, int N,
     out[e] = pack_bf16x2(epi_value<EPI>(v[2 * e], b0, gg[2 * e], x0),
                          epi_value<EPI>(v[2 * e + 1], b1, gg[2 * e + 1], x1));
   }
-  *reinterpret_cast<uint4*>(p) = make_uint4(out[0], out[1], out[2], out[3]);
+  bf16_t* dst = p;
+  if (EPI == EPI_BIAS_GATED_RESIDUAL && smap != nullptr) dst = Cs + (int64_t)smap[row] * ldc + col;
+  *reinterpret_cast<uint4*>(dst) = make_uint4(out[0], out[1], out[2], out[3]);
 }
 
 // ---------------------------------------------------------------------------
@@ -506,13 +511,14 @@ template <int ROLE, int BM, int BN, int WM, int WN, int EPI>
 static hipError_t run_bf16(const void* A, int64_t lda, const void* B, int64_t ldb,
                            const void* bias, const float* gate, void* C, int64_t ldc, int M,
                            int N, int K, int splits, float* part, hipStream_t st,
-                           const QkPost& qp = QkPost{}) {
+                           const QkPost& qp = QkPost{}, void* Cs = nullptr,
+                           const int32_t* smap = nullptr) {
   const int tiles_m = (M + BM - 1) / BM, tiles_n = (N + BN - 1) / BN;
   if (splits <= 1) {
     hipLaunchKernelGGL((gemm_bf16_nt<ROLE, BM, BN, WM, WN, EPI>), dim3(tiles_m * tiles_n),
                        dim3(WM * WN * 64), 0, st, (const bf16_t*)A, lda, (const bf16_t*)B, ldb,
                        (const bf16_t*)bias, gate, (bf16_t*)C, ldc, M, N, K, tiles_m, tiles_n,
-                       (float*)nullptr, qp, ScoreArgs{}, 0);
+                       (float*)nullptr, qp, ScoreArgs{}, 0, (bf16_t*)Cs, smap);
     return hipGetLastError();
   }
   if constexpr (EPI == EPI_BIAS_QKPOST) {
@@ -521,12 +527,13 @@ static hipError_t run_bf16(const void* A, int64_t lda, const void* B, int64_t ld
     hipLaunchKernelGGL((gemm_bf16_nt<ROLE, BM, BN, WM, WN, EPI_PARTIAL>), dim3(tiles_m * tiles_n, splits),
                        dim3(WM * WN * 64), 0, st, (const bf16_t*)A, lda, (const bf16_t*)B, ldb,
                        (const bf16_t*)bias, gate, (bf16_t*)C, ldc, M, N, K, tiles_m, tiles_n, part,
-                       QkPost{}, ScoreArgs{}, 0);
+                       QkPost{}, ScoreArgs{}, 0, (bf16_t*)nullptr, (const int32_t*)nullptr);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     const int64_t n = (int64_t)M * (N / 8);
     hipLaunchKernelGGL((splitk_epilogue<ROLE, EPI>), dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st,
-                       part, splits, M, N, (const bf16_t*)bias, gate, (bf16_t*)C, ldc);
+                       part, splits, M, N, (const bf16_t*)bias, gate, (bf16_t*)C, ldc,
+                       (bf16_t*)Cs, smap);
     return hipGetLastError();
   }
 }
@@ -583,13 +590,14 @@ template <int ROLE, int EPI>
 static hipError_t dispatch_bf16(const void* A, int64_t lda, const void* B, int64_t ldb,
                                 const void* bias, const float* gate, void* C, int64_t ldc,
                                 int M, int N, int K, float* ws, int64_t ws_floats,
-                                hipStream_t st) {
+                                hipStream_t st, void* Cs = nullptr,
+                                const int32_t* smap = nullptr) {
   const GemmPlan p = choose_gemm(M, N, K, ws ? ws_floats : 0);
   if (p.tile == 0)
-    return run_bf16<ROLE, 256, 256, 2, 4, EPI>(A, lda, B, ldb, bias, gate, C, ldc, M, N, K, p.splits, ws, st);
+    return run_bf16<ROLE, 256, 256, 2, 4, EPI>(A, lda, B, ldb, bias, gate, C, ldc, M, N, K, p.splits, ws, st, QkPost{}, Cs, smap);
   if (p.tile == 2)
-    return run_bf16<ROLE, 192, 256, 2, 4, EPI>(A, lda, B, ldb, bias, gate, C, ldc, M, N, K, p.splits, ws, st);
-  return run_bf16<ROLE, 128, 128, 2, 2, EPI>(A, lda, B, ldb, bias, gate, C, ldc, M, N, K, p.splits, ws, st);
+    return run_bf16<ROLE, 192, 256, 2, 4, EPI>(A, lda, B, ldb, bias, gate, C, ldc, M, N, K, p.splits, ws, st, QkPost{}, Cs, smap);
+  return run_bf16<ROLE, 128, 128, 2, 2, EPI>(A, lda, B, ldb, bias, gate, C, ldc, M, N, K, p.splits, ws, st, QkPost{}, Cs, smap);
 }
 
 // The MLP up projection with one layer's scoring in the tail of its grid:
@@ -623,7 +631,7 @@ static hipError_t run_up_scored(const void* A, int64_t lda, const void* B, int64
                      dim3(tiles_m * tiles_n + n_sw), dim3(WM * WN * 64), 0, st, (const bf16_t*)A,
                      lda, (const bf16_t*)B, ldb, (const bf16_t*)bias, (const float*)nullptr,
                      (bf16_t*)C, ldc, M, N, K, tiles_m, tiles_n, (float*)nullptr, QkPost{}, sa,
-                     n_units);
+                     n_units, (bf16_t*)nullptr, (const int32_t*)nullptr);
   return hipGetLastError();
 }
 
@@ -654,15 +662,17 @@ static hipError_t run_f32(const void* A, int64_t lda, const void* B, int64_t ldb
 hipError_t launch_gemm(int dtype, int role, const void* A, int64_t lda, const void* B,
                        int64_t ldb, const void* bias, const float* gate, void* C,
                        int64_t ldc, int64_t M, int64_t N, int64_t K, hipStream_t st,
-                       float* ws, int64_t ws_floats) {
+                       float* ws, int64_t ws_floats, void* Cs, const int32_t* smap) {
   if (M <= 0) return hipSuccess;
   const int m = (int)M, n = (int)N, k = (int)K;
+  if (smap != nullptr && (dtype != 1 || (role != ROLE_OUT && role != ROLE_DOWN) || Cs == nullptr))
+    return hipErrorNotSupported;             // row scatter: bf16 gated-residual stores only
   if (dtype == 1) {
     switch (role) {
       case ROLE_QKV: return dispatch_bf16<ROLE_QKV, EPI_BIAS>(A, lda, B, ldb, bias, gate, C, ldc, m, n, k, ws, ws_floats, st);
       case ROLE_UP: return dispatch_bf16<ROLE_UP, EPI_BIAS_GELU>(A, lda, B, ldb, bias, gate, C, ldc, m, n, k, ws, ws_floats, st);
-      case ROLE_OUT: return dispatch_bf16<ROLE_OUT, EPI_BIAS_GATED_RESIDUAL>(A, lda, B, ldb, bias, gate, C, ldc, m, n, k, ws, ws_floats, st);
-      case ROLE_DOWN: return dispatch_bf16<ROLE_DOWN, EPI_BIAS_GATED_RESIDUAL>(A, lda, B, ldb, bias, gate, C, ldc, m, n, k, ws, ws_floats, st);
+      case ROLE_OUT: return dispatch_bf16<ROLE_OUT, EPI_BIAS_GATED_RESIDUAL>(A, lda, B, ldb, bias, gate, C, ldc, m, n, k, ws, ws_floats, st, Cs, smap);
+      case ROLE_DOWN: return dispatch_bf16<ROLE_DOWN, EPI_BIAS_GATED_RESIDUAL>(A, lda, B, ldb, bias, gate, C, ldc, m, n, k, ws, ws_floats, st, Cs, smap);
       default: return hipErrorInvalidValue;
     }
   }

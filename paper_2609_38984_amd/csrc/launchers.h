@@ -34,10 +34,15 @@ enum GemmRole { ROLE_QKV = 0, ROLE_OUT = 1, ROLE_UP = 2, ROLE_DOWN = 3 };
 // ws / ws_floats: fp32 workspace the bf16 path may use to split K when the
 // output tiles alone cannot fill the CUs (partial sums, then one reduce +
 // epilogue pass); NULL or too small means no split.
+// smap (bf16 OUT / DOWN only): row m of the result goes to Cs[smap[m]] (same
+// ldc) instead of C[m]; the residual is still read from C[m].  The scatter of
+// a packed sequence's rows back into the full latent rides on the last
+// projection this way.
 hipError_t launch_gemm(int dtype, int role, const void* A, int64_t lda, const void* B,
                        int64_t ldb, const void* bias, const float* gate, void* C,
                        int64_t ldc, int64_t M, int64_t N, int64_t K, hipStream_t st,
-                       float* ws = nullptr, int64_t ws_floats = 0);
+                       float* ws = nullptr, int64_t ws_floats = 0, void* Cs = nullptr,
+                       const int32_t* smap = nullptr);
 
 // QKV projection C = A . B^T + bias followed by the QK-norm / rotary
 // embedding of qp on its q and k columns, with the same bf16 rounding of the

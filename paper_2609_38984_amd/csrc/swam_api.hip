@@ -310,10 +310,13 @@ bool bad_block(const swam_block_weights* w) {
 // overlaps the QKV projection rather than the pack
 // score_in_up (with score): the scoring runs in the tail of the MLP up
 // projection's grid instead of on the side stream (no fork or join)
+// scatter_to (bf16, last block of a sparse step): the MLP down projection
+// stores row r of its result into scatter_to at the cached gather position of
+// r (the scatter back into the full latent) instead of into x
 int run_block(swam_ctx* c, const swam_block_weights* w, const float* mod, void* x,
               int64_t n_rows, const int32_t* cu, int n_seqs, float* lse_out, void* qkv,
               int pos_mode, const ScoreArgs* score = nullptr, const void* pack_src = nullptr,
-              void* pruned_dst = nullptr, bool score_in_up = false) {
+              void* pruned_dst = nullptr, bool score_in_up = false, void* scatter_to = nullptr) {
   const int dt = c->cfg.dtype;
   const int64_t d = c->dv.d, hid = c->dv.hidden;
   void* h = c->ptr<char>(c->lay.h);
@@ -401,7 +404,9 @@ int run_block(swam_ctx* c, const swam_block_weights* w, const float* mod, void* 
   {
     Timed t(c, SWAM_T_GEMM_DOWN);
     SWAM_HIP(c, launch_gemm(dt, ROLE_DOWN, u, hid, w->w_2, hid, w->b_2, g2, x, d,
-                            n_rows, d, hid, st, sk, sk_n), "gemm down");
+                            n_rows, d, hid, st, sk, sk_n, scatter_to,
+                            scatter_to ? c->ptr<int32_t>(c->lay.gather) : nullptr),
+             scatter_to ? "gemm down + unpack" : "gemm down");
   }
   return SWAM_OK;
 }
@@ -1055,16 +1060,22 @@ int enqueue_step_launches(swam_ctx* c, const swam_model* model, const void* x_fu
     const bool fork = y_full != x_full;
     if (fork && c->packed_rows <= 0)
       if ((rc = fork_pruned_copy(c, x_full, y_full)) != SWAM_OK) return rc;
-    // the gather-pack of x_full runs inside block 0's first LayerNorm kernel
+    // the gather-pack of x_full runs inside block 0's first LayerNorm kernel;
+    // bf16: the scatter of the retained rows into y_full inside the last
+    // block's MLP down projection store (the pruned rows of y_full are the
+    // copy's, disjoint from these); fp32: a separate scatter pass
     void* xp = c->ptr<char>(c->lay.xp);
+    const bool fold_unpack = cf.dtype == SWAM_BF16;
     for (int l = 0; l < cf.n_blocks; ++l) {
+      const bool last = l + 1 == cf.n_blocks;
       rc = run_block(c, &model->blocks[l], mod + (int64_t)l * 6 * d, xp, c->packed_rows,
                      c->ptr<int32_t>(c->lay.cu_packed), cf.batch, nullptr, qkv, 1, nullptr,
-                     l == 0 ? x_full : nullptr, l == 0 && fork ? y_full : nullptr);
+                     l == 0 ? x_full : nullptr, l == 0 && fork ? y_full : nullptr, false,
+                     fold_unpack && last ? y_full : nullptr);
       if (rc != SWAM_OK) return rc;
     }
     if (fork) SWAM_HIP(c, hipStreamWaitEvent(c->st, c->ev_score, 0), "join pruned-row copy");
-    {
+    if (!fold_unpack) {
       // scatter of the packed rows (the retained ones) into y_full
       Timed t(c, SWAM_T_UNPACK);
       SWAM_HIP(c, launch_unpack_scatter(xp, y_full, c->ptr<int32_t>(c->lay.gather),
