@@ -470,6 +470,9 @@ def measure(cfg, model, xs, tembs, steps, warmup, reps):
         per_kind["sparse"] = class_times(0, 1)
     by_class = class_rooflines(cfg, per_kind, full_rows, packed_rows)
     by_class["hbm"]["SCORE_isolated"] = score_isolated(cfg, ctx)
+    in_up = score_in_up(cfg, per_kind)
+    if in_up is not None:
+        by_class["hbm"]["SCORE_in_up_marginal"] = in_up
     ctx.timer_enable(swam.TIMERS, capacity=1 << 15)
     for t in range(n_sched):
         run(t)
@@ -539,15 +542,42 @@ def score_isolated(cfg, ctx, n=None):
     k_fut = flat[cfg.n_ctx * ld + d:]
     for _ in range(3):
         ctx.score(q_act, L * ld, ld, k_fut, L * ld, ld, s, lse_act=lse)
-    ctx.timer_enable(["SCORE"], capacity=4 * n)
+    # the n launches back to back between one pair of events on the context
+    # stream (an event pair around every launch would add its own cost to a
+    # launch of about ten microseconds)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
     for _ in range(n):
         ctx.score(q_act, L * ld, ld, k_fut, L * ld, ld, s, lse_act=lse)
-    k, ms = ctx.timer_read("SCORE")
-    ctx.timer_enable([], 1)
-    us = ms * 1e3 / max(k, 1)
+    e1.record()
+    torch.cuda.synchronize()
+    us = e0.elapsed_time(e1) * 1e3 / n
     gbs = kernel_work(cfg, "SCORE", [cfg.l_full] * cfg.batch) / (us * 1e-6) / 1e9
-    return {"us": round(us, 2), "launches": int(k), "GB/s": round(gbs, 1),
+    return {"us": round(us, 2), "launches": n, "GB/s": round(gbs, 1),
             "frac": round(gbs / PEAK_HBM_GBS, 4)}
+
+
+def score_in_up(cfg, per_kind):
+    """What the scoring of the layers that score in the tail of their MLP up
+    projection grid costs the step: the up projection's time in a refresh step
+    minus its time in a dense step (the same launches without the scoring
+    units), per scored layer, and the scoring's algorithmic bytes over that
+    marginal time."""
+    up_r = per_kind.get("refresh", {}).get("GEMM_UP")
+    up_d = per_kind.get("dense", {}).get("GEMM_UP")
+    if not up_r or not up_d:
+        return None
+    n_side = per_kind["refresh"].get("SCORE", (0, 0.0))[0]   # layers scored on the side stream
+    n_in = cfg.n_blocks - int(round(n_side))
+    if n_in <= 0:
+        return None
+    marg_us = (up_r[1] - up_d[1]) * 1e3 / n_in
+    out = {"layers_per_refresh": n_in, "marginal_us_per_layer": round(marg_us, 2)}
+    if marg_us > 0:
+        gbs = kernel_work(cfg, "SCORE", [cfg.l_full] * cfg.batch) / (marg_us * 1e-6) / 1e9
+        out["effective_GB/s"] = round(gbs, 1)
+    return out
 
 
 def class_rooflines(cfg, per_kind, full_rows, packed_rows):
