@@ -9,7 +9,8 @@ step on that packing (Sec. 4.2 compact execution) within 2e-2 max-relative,
 with pruned rows byte-identical to the input; the first refresh's dense output
 is compared with the oracle's dense step the same way.  The same schedule
 replayed from captured HIP graphs (swam_step_graph) is checked against the
-oracle in the same way.
+oracle in the same way.  One-block schedules (the block that packs is the one
+that scatters back), in place and out of place, one and two sequences.
 """
 import numpy as np
 import pytest
@@ -59,7 +60,7 @@ def _check_selection_on_own_scores(cfg, got, kmax):
     return pm
 
 
-def _run_schedule_against_oracle(cfg, use_graph, dense_check_at=(0,)):
+def _run_schedule_against_oracle(cfg, use_graph, dense_check_at=(0,), in_place=False):
     from paper_2609_38984_amd import swam
     blocks, _, model = model_for(cfg)
     inp = W.make_inputs(cfg, blocks[0]["w_qkv"])
@@ -69,7 +70,8 @@ def _run_schedule_against_oracle(cfg, use_graph, dense_check_at=(0,)):
         pm = None
         for tau in range(cfg.n_steps):
             x = dev(inp.x(tau), torch.bfloat16)
-            y = torch.empty_like(x)
+            x_in = x.clone()
+            y = x if in_place else torch.empty_like(x)
             t = dev(inp.temb(tau))
             if use_graph:
                 kind = ctx.step_graph(model, x, t, tau, y)
@@ -92,7 +94,7 @@ def _run_schedule_against_oracle(cfg, use_graph, dense_check_at=(0,)):
                 err = maxrel(host(y), ref)
                 pruned = pm.pack_pos < 0
                 yb = y.view(torch.int16).cpu().numpy()
-                xb = x.view(torch.int16).cpu().numpy()
+                xb = x_in.view(torch.int16).cpu().numpy()
                 print(f"  tau {tau} sparse ({int(pm.cu_seqlens[-1])} rows): max-rel {err:.2e}", flush=True)
                 assert err < 2e-2
                 assert np.array_equal(yb[pruned], xb[pruned])
@@ -102,6 +104,18 @@ def test_bf16_8block_schedule_matches_oracle():
     cfg = W.preset(2)
     print(f"schedule {cfg.name}: {cfg.n_steps} steps, R = {cfg.reuse_R}", flush=True)
     _run_schedule_against_oracle(cfg, use_graph=False)
+
+
+@pytest.mark.parametrize("in_place", [False, True])
+@pytest.mark.parametrize("batch", [1, 2])
+def test_bf16_one_block_schedule_matches_oracle(batch, in_place):
+    # one block: the sparse step's gather-pack (first LayerNorm) and its
+    # scatter back (the MLP down projection's store) are in the same block;
+    # in place the scatter writes into the latent the pack read from, and with
+    # two sequences the scattered rows cross a sequence boundary
+    cfg = W.preset(2).replace(n_blocks=1, batch=batch, n_steps=4)
+    print(f"one-block schedule {cfg.name}: batch {batch}, in place {in_place}", flush=True)
+    _run_schedule_against_oracle(cfg, use_graph=False, in_place=in_place)
 
 
 def test_bf16_graph_schedule_matches_oracle():
