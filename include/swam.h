@@ -349,7 +349,11 @@ int swam_block(swam_ctx* ctx, const swam_block_weights* w, const float* temb, vo
  * Refresh (tau mod R == 0 or FORCE_REFRESH): dense blocks with scoring of
  * every layer, then score reduce, selection and packing metadata, cached.
  * Sparse: pack -> blocks on the packed sequences -> unpack; pruned rows of
- * y_full equal x_full bit for bit.  Returns SWAM_E_STATE for a sparse step
+ * y_full equal x_full bit for bit.  The pack runs inside the first block's
+ * first LayerNorm kernel; in bf16 the unpack runs inside the last block's MLP
+ * down projection, whose store writes each packed row straight to its row of
+ * y_full (fp32: a separate scatter pass), so SWAM_T_UNPACK records no bf16
+ * launch.  Returns SWAM_E_STATE for a sparse step
  * with no cached selection.  *kind_out (optional, host) receives SWAM_KIND_*. */
 int swam_step(swam_ctx* ctx, const swam_model* model, const void* x_full,
               const float* temb, int32_t tau, void* y_full, int32_t flags,
