@@ -138,8 +138,10 @@ __device__ __forceinline__ int vadd_sgpr(int v, int s) {
 template <int BM, int BN, int TM, int TN, int FM, int FN>
 __device__ __forceinline__ void mma_stage(const uint4* __restrict__ as, const uint4* __restrict__ bs,
                                           int wm, int wn, int lane, f32x16 (&acc)[FM][FN]) {
-  static_assert(FM * FN >= FM + FN, "interleave needs an MFMA per fragment read");
   constexpr int KS = GEMM_BK / 16;
+  // fragment reads of the next k-step paired with this k-step's MFMAs; with
+  // fewer MFMAs than reads (the 96 x 32 wave tile) the rest follow as a group
+  constexpr int PAIRS = FM * FN < FM + FN ? FM * FN : FM + FN;
   const int khalf = lane >> 5, r31 = lane & 31;
   const int sw = lds_swz(r31);   // rows differ from r31 by multiples of 32
   bf16x8 af[2][FM], bfr[2][FN];
@@ -169,12 +171,14 @@ __device__ __forceinline__ void mma_stage(const uint4* __restrict__ as, const ui
 #pragma unroll
   for (int s = 0; s + 1 < KS; ++s) {
 #pragma unroll
-    for (int r = 0; r < FM + FN; ++r) {
+    for (int r = 0; r < PAIRS; ++r) {
       __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
       __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
     }
-    if constexpr (FM * FN > FM + FN)
-      __builtin_amdgcn_sched_group_barrier(0x008, FM * FN - (FM + FN), 0);
+    if constexpr (FM + FN > PAIRS)
+      __builtin_amdgcn_sched_group_barrier(0x100, FM + FN - PAIRS, 0);
+    if constexpr (FM * FN > PAIRS)
+      __builtin_amdgcn_sched_group_barrier(0x008, FM * FN - PAIRS, 0);
   }
   __builtin_amdgcn_sched_group_barrier(0x008, FM * FN, 0);
 }
@@ -551,34 +555,48 @@ static hipError_t run_bf16(const void* A, int64_t lda, const void* B, int64_t ld
 // which makes it the choice where its 3/4-size tiles fill whole rounds: the
 // packed MLP up projection at 3,472 rows, the out and down projections at
 // 17,472 rows); the pass moves splits * M * N fp32 partials plus the bf16
-// output (and residual) at about 4 TB/s.  (A 256x128 tile measured at 0.72
-// of that rate never won at any block shape from d = 256 to 4096 and was
+// output (and residual) at about 4 TB/s.  The 192x128 tile (8 waves of
+// 96 x 32, two workgroups per CU) enters at 0.83, which selects it where
+// half-rounds of its small tiles fill the CUs much better than the others:
+// the packed out projection at 3,472 rows and the d = 1024 projections at
+// 1,312 rows (measured 2-9% faster there).  At 0.84 it would also take the
+// packed down projection at 3,472 rows without a K split, measured 11%
+// slower than the three K slices.  (A 256x128 tile measured at 0.72 of the
+// base rate never won at any block shape from d = 256 to 4096 and was
 // dropped.)
 struct GemmPlan { int tile, splits; };
-static GemmPlan choose_gemm(int64_t M, int64_t N, int64_t K, int64_t ws_floats) {
-  struct Cand { int bm, bn, per_cu; double eff; };
-  const Cand c[3] = {{256, 256, 1, 1.0}, {128, 128, 2, 0.80}, {192, 256, 1, 0.85}};
+constexpr int GEMM_TILES = 4;
+static const int TILE_BM[GEMM_TILES] = {256, 128, 192, 192};
+static const int TILE_BN[GEMM_TILES] = {256, 128, 256, 128};
+static const int TILE_PER_CU[GEMM_TILES] = {1, 2, 1, 2};
+// wide_only: only tiles whose waves span 64 columns (the QK post-processing
+// store needs one head per wave)
+static GemmPlan choose_gemm(int64_t M, int64_t N, int64_t K, int64_t ws_floats,
+                            bool wide_only = false) {
+  const double eff[GEMM_TILES] = {1.0, 0.80, 0.85, 0.83};
   const int split_opts[6] = {1, 2, 3, 4, 6, 8};
   const int64_t kt = K / GEMM_BK;
   const double cu_flops = 2.5e15 / 256.0 * 0.40;        // sustained MFMA rate per CU
   GemmPlan best{0, 1};
   double best_t = 1e30;
-  for (int i = 0; i < 3; ++i) {
-    const int64_t tiles = ((M + c[i].bm - 1) / c[i].bm) * ((N + c[i].bn - 1) / c[i].bn);
+  for (int i = 0; i < GEMM_TILES; ++i) {
+    if (wide_only && i == 3) continue;
+    const int bm = TILE_BM[i], bn = TILE_BN[i], per_cu = TILE_PER_CU[i];
+    const int64_t tiles = ((M + bm - 1) / bm) * ((N + bn - 1) / bn);
     for (int s : split_opts) {
       if (s > 1 && (kt / s < 4 || (int64_t)s * M * N > ws_floats)) continue;
       const int64_t wgs = tiles * s;
       double rounds;
-      if (c[i].per_cu == 1) {
+      if (per_cu == 1) {
         rounds = (double)((wgs + 255) / 256);
       } else {
         // whole half-rounds while one slot per CU is not yet filled
-        rounds = std::max((double)wgs / (256.0 * c[i].per_cu),
-                          (double)((wgs + 255) / 256) / c[i].per_cu);
+        rounds = std::max((double)wgs / (256.0 * per_cu),
+                          (double)((wgs + 255) / 256) / per_cu);
       }
       const double k_slice = (double)((kt + s - 1) / s) * GEMM_BK;
-      double t = rounds * 2.0 * c[i].bm * c[i].bn * c[i].per_cu * k_slice /
-                 (cu_flops * c[i].eff);
+      double t = rounds * 2.0 * bm * bn * per_cu * k_slice /
+                 (cu_flops * eff[i]);
       if (s > 1) t += ((double)s * M * N * 4.0 + 4.0 * M * N) / 4.0e12 + 3e-6;
       if (t < best_t) { best_t = t; best = {i, s}; }
     }
@@ -597,6 +615,8 @@ static hipError_t dispatch_bf16(const void* A, int64_t lda, const void* B, int64
     return run_bf16<ROLE, 256, 256, 2, 4, EPI>(A, lda, B, ldb, bias, gate, C, ldc, M, N, K, p.splits, ws, st, QkPost{}, Cs, smap);
   if (p.tile == 2)
     return run_bf16<ROLE, 192, 256, 2, 4, EPI>(A, lda, B, ldb, bias, gate, C, ldc, M, N, K, p.splits, ws, st, QkPost{}, Cs, smap);
+  if (p.tile == 3)
+    return run_bf16<ROLE, 192, 128, 2, 4, EPI>(A, lda, B, ldb, bias, gate, C, ldc, M, N, K, p.splits, ws, st, QkPost{}, Cs, smap);
   return run_bf16<ROLE, 128, 128, 2, 2, EPI>(A, lda, B, ldb, bias, gate, C, ldc, M, N, K, p.splits, ws, st, QkPost{}, Cs, smap);
 }
 
@@ -605,10 +625,10 @@ static hipError_t dispatch_bf16(const void* A, int64_t lda, const void* B, int64
 // round, on the CUs its tiles leave idle there (at least 16 of them, or the
 // caller scores on its side stream instead).
 static int scored_idle_slots(const GemmPlan& p, int64_t M, int64_t N) {
-  static const int bm[3] = {256, 128, 192}, bn[3] = {256, 128, 256}, per_cu[3] = {1, 2, 1};
+  const int bm = TILE_BM[p.tile], bn = TILE_BN[p.tile];
   if (p.splits != 1) return 0;
-  const int64_t tiles = ((M + bm[p.tile] - 1) / bm[p.tile]) * ((N + bn[p.tile] - 1) / bn[p.tile]);
-  const int64_t slots = 256 * per_cu[p.tile];
+  const int64_t tiles = ((M + bm - 1) / bm) * ((N + bn - 1) / bn);
+  const int64_t slots = 256 * TILE_PER_CU[p.tile];
   const int64_t idle = (slots - tiles % slots) % slots;
   return idle >= 16 ? (int)idle : 0;
 }
@@ -646,6 +666,7 @@ hipError_t launch_gemm_up_scored(const void* A, int64_t lda, const void* B, int6
   const int m = (int)M, n = (int)N, k = (int)K;
   if (p.tile == 0) return run_up_scored<256, 256, 2, 4>(A, lda, B, ldb, bias, C, ldc, m, n, k, sa, n_sw, st);
   if (p.tile == 2) return run_up_scored<192, 256, 2, 4>(A, lda, B, ldb, bias, C, ldc, m, n, k, sa, n_sw, st);
+  if (p.tile == 3) return run_up_scored<192, 128, 2, 4>(A, lda, B, ldb, bias, C, ldc, m, n, k, sa, n_sw, st);
   return run_up_scored<128, 128, 2, 2>(A, lda, B, ldb, bias, C, ldc, m, n, k, sa, n_sw, st);
 }
 
@@ -692,7 +713,7 @@ hipError_t launch_gemm_qkv(int dtype, const void* A, int64_t lda, const void* B,
   if (M <= 0) return hipSuccess;
   const bool post = qp.qk_norm || qp.tab != nullptr;
   if (dtype == 1 && post) {
-    const GemmPlan p = choose_gemm(M, N, K, ws ? ws_floats : 0);
+    const GemmPlan p = choose_gemm(M, N, K, ws ? ws_floats : 0, true);
     if (p.splits <= 1) {
       const int m = (int)M, n = (int)N, k = (int)K;
       if (p.tile == 0)
