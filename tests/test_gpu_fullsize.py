@@ -70,7 +70,7 @@ def test_block_wam_dense_10160_sampled():
 
 def test_block_wam_packed_3472_sampled():
     """The packed sequence of the WAM workload as the bench times it: the
-    4-wave attention, the 128x128 out projection, the 192x256 MLP up tile
+    4-wave attention, the 192x128 out projection, the 192x256 MLP up tile
     and the down projection split along K in three."""
     cfg = W.preset(3)
     x = W.make_inputs(cfg, W.block_weights(cfg, 0)["w_qkv"]).x(0)
